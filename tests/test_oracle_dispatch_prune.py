@@ -1,0 +1,118 @@
+"""Pins of the oracle's dispatch (Section 2.1, Eq. 1) and pruning (Section 3.1).
+
+Dispatch is checked against a library stable sort and a histogram, and its
+n_active against the exact expectation of Eq. 1 under uniform independent
+k-subsets.  Pruning is checked against a library lexicographic sort, the
+tie rule, and the shape the paper states for the Qwen3.6-35B-A3B pool.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_34117_amd import inputs as I
+
+
+def _uniform_k_subsets(g, t, m, k):
+    return np.stack([g.choice(m, size=k, replace=False) for _ in range(t)]).astype(np.int32)
+
+
+@pytest.mark.parametrize("t,m,k", [(1, 8, 2), (8, 16, 2), (64, 256, 8), (33, 40, 7), (100, 5, 5)])
+def test_dispatch_matches_stable_sort_and_histogram(t, m, k):
+    g = np.random.default_rng([t, m, k])
+    ids = _uniform_k_subsets(g, t, m, k)
+    counts, offsets, perm, active, n_active = oracle.dispatch(ids, m)
+    flat = ids.ravel()
+    np.testing.assert_array_equal(counts, np.bincount(flat, minlength=m))
+    np.testing.assert_array_equal(offsets, np.concatenate([[0], np.cumsum(counts)]))
+    np.testing.assert_array_equal(perm, np.argsort(flat, kind="stable"))
+    np.testing.assert_array_equal(active, np.flatnonzero(counts))
+    assert n_active == len(np.unique(flat))
+    assert offsets[-1] == t * k
+
+
+def test_dispatch_skewed_ids_with_repeats_across_tokens():
+    ids = np.array([[3, 1], [3, 0], [1, 3], [2, 3]], np.int32)
+    counts, offsets, perm, active, n_active = oracle.dispatch(ids, 5)
+    np.testing.assert_array_equal(counts, [1, 2, 1, 4, 0])
+    np.testing.assert_array_equal(offsets, [0, 1, 3, 4, 8, 8])
+    np.testing.assert_array_equal(perm, [3, 1, 4, 6, 0, 2, 5, 7])
+    np.testing.assert_array_equal(active, [0, 1, 2, 3])
+    assert n_active == 4
+
+
+def test_dispatch_empty_and_invalid():
+    counts, offsets, perm, active, n_active = oracle.dispatch(np.zeros((0, 4), np.int32), 8)
+    assert n_active == 0 and np.all(counts == 0) and np.all(offsets == 0) and perm.size == 0
+    with pytest.raises(ValueError):
+        oracle.dispatch(np.array([[0, 8]], np.int32), 8)
+    with pytest.raises(ValueError):
+        oracle.dispatch(np.array([[-1, 2]], np.int32), 8)
+
+
+@pytest.mark.parametrize("m,k,b", [(256, 8, 64), (128, 8, 64), (256, 8, 8), (128, 8, 1), (16, 2, 8)])
+def test_eq1_expected_distinct_experts(m, k, b):
+    # Eq. 1: with uniform, independent k-subsets per token, each expert is
+    # missed by all B tokens with probability (1 - k/m)^B.
+    g = np.random.default_rng([11, m, k, b])
+    trials = 400
+    na = np.array([oracle.dispatch(_uniform_k_subsets(g, b, m, k), m)[4] for _ in range(trials)], float)
+    expect = m * (1.0 - (1.0 - k / m) ** b)
+    se = max(na.std(ddof=1), 1e-9) / np.sqrt(trials)
+    assert abs(na.mean() - expect) < 4.5 * se + 1e-9, (na.mean(), expect, se)
+
+
+def test_eq1_saturation_large_batch():
+    # Section 2.1: as B grows the union approaches the whole (kept) pool.
+    g = np.random.default_rng(3)
+    ids = _uniform_k_subsets(g, 4096, 128, 8)
+    assert oracle.dispatch(ids, 128)[4] == 128
+
+
+@pytest.mark.parametrize("m,n_keep", [(16, 8), (16, 2), (256, 128), (256, 192), (256, 256), (7, 3)])
+def test_prune_keeps_the_top_by_importance(m, n_keep):
+    imp = np.random.default_rng([m, n_keep]).random(m, dtype=np.float32)
+    kept, remap, mask, *_ = oracle.prune_compact(imp, n_keep, top_k=1)
+    order = np.lexsort((np.arange(m), -imp))  # importance desc, id asc
+    np.testing.assert_array_equal(kept, np.sort(order[:n_keep]))
+    assert np.all(np.diff(kept) > 0)
+    np.testing.assert_array_equal(mask, np.isin(np.arange(m), kept).astype(np.uint8))
+    expect_remap = np.full(m, -1, np.int32)
+    expect_remap[kept] = np.arange(n_keep)
+    np.testing.assert_array_equal(remap, expect_remap)
+
+
+def test_prune_ties_go_to_smaller_ids():
+    imp = np.array([0.5, 0.9, 0.5, 0.5, 0.1, 0.5], np.float32)
+    kept, *_ = oracle.prune_compact(imp, 3, top_k=1)
+    np.testing.assert_array_equal(kept, [0, 1, 2])
+    kept, *_ = oracle.prune_compact(imp, 5, top_k=1)
+    np.testing.assert_array_equal(kept, [0, 1, 2, 3, 5])
+
+
+def test_prune_compacted_arrays_are_the_kept_rows():
+    cfg = I.small_config(hidden=32, n_experts=12, inter=16)
+    L = I.make_layer(cfg)
+    bias = np.linspace(-1, 1, 12).astype(np.float32)
+    kept, remap, mask, w13c, w2c, wrc, bc = oracle.prune_compact(
+        L["importance"], 6, 2, w13=L["w13"], w2=L["w2"], wr=L["wr"], bias=bias)
+    np.testing.assert_array_equal(w13c, L["w13"][kept])
+    np.testing.assert_array_equal(w2c, L["w2"][kept])
+    np.testing.assert_array_equal(wrc, L["wr"][kept])
+    np.testing.assert_array_equal(bc, bias[kept])
+
+
+def test_prune_rejects_bad_counts():
+    imp = np.ones(8, np.float32)
+    with pytest.raises(ValueError):
+        oracle.prune_compact(imp, 1, top_k=2)  # m' < k
+    with pytest.raises(ValueError):
+        oracle.prune_compact(imp, 9, top_k=2)  # m' > m
+
+
+def test_pool_shape_matches_the_paper_60gib():
+    # Section 2.1 / Fig. 2: a 60 GiB bf16 expert pool for m = 256 experts in
+    # each of 40 layers; the synthetic 256-expert shapes reproduce it.
+    for name in ("decode_sweep", "prefill", "skewed_stack"):
+        cfg = I.CONFIGS[name]
+        assert 40 * cfg.n_experts * cfg.expert_bytes() == 60 * 2 ** 30
+    assert I.CONFIGS["skewed_stack"].n_layers == 40
