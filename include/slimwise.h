@@ -1,0 +1,194 @@
+/*
+ * slimwise.h -- C ABI of the SlimWise batched-decode MoE layer on MI355X.
+ *
+ * The layer is the hot path of decode-only expert pruning in "SlimWise:
+ * Decoupling Expert Pruning Across Prefill and Decode for Efficient MoE
+ * Serving" (arXiv 2609.34117): each decode step reads the weights of every
+ * distinct expert chosen across the batch (Section 2.1, Eq. 1), and a pruned
+ * decoder -- a compacted checkpoint, or the full pool behind a router mask
+ * (Section 3.1, Eq. 2) -- shrinks that set.
+ *
+ * Conventions shared by every call:
+ *   - Every array pointer is a DEVICE pointer on the current HIP device;
+ *     the caller allocates and owns all memory.  The library never
+ *     allocates, never synchronises, keeps no mutable global state and is
+ *     re-entrant; calls are ordered on `stream` (a hipStream_t; NULL = the
+ *     default stream).  Calls on one stream that share output or workspace
+ *     buffers must not overlap with calls on other streams.
+ *   - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
+ *   - Layouts are dense row-major:
+ *       x     bf16 [T, H]         token activations
+ *       w13   bf16 [m, 2I, H]     per expert: rows 0..I-1 the gate projection,
+ *                                 rows I..2I-1 the up projection
+ *       w2    bf16 [m, H, I]      per expert: the down projection
+ *       wr    fp32 [m, H]         router gate weight, row e = expert e
+ *       bias  fp32 [m]            optional per-expert router logit bias
+ *     where m is the number of experts in the pool handed to the call
+ *     (`n_experts`): the full pool m, or the compacted pool m' whose ids are
+ *     compact indices (map back through `kept`).
+ *   - Alignment: x, w13, w2, wr, out and workspace must be 16-byte aligned;
+ *     H and I must be multiples of 8.
+ *   - Arguments are validated before anything is launched; a non-SW_OK
+ *     status means nothing was enqueued (SW_ERR_DEVICE: a launch failed).
+ *   - Data-dependent errors that the host cannot see without a sync are
+ *     reported in-band on the device, as documented per call.
+ *   - Limits: 1 <= top_k <= 32, top_k <= n_experts <= 1024, 0 <= T,
+ *     T * top_k < 2^31.
+ */
+#ifndef SLIMWISE_H
+#define SLIMWISE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SW_OK = 0,
+  SW_ERR_NULL = 1,        /* a required pointer is NULL */
+  SW_ERR_SHAPE = 2,       /* a size is out of range (dims <= 0, n_keep < k, ...) */
+  SW_ERR_ALIGN = 3,       /* pointer not 16-byte aligned, or H / I not multiples of 8 */
+  SW_ERR_UNSUPPORTED = 4, /* valid but outside the kernels' limits */
+  SW_ERR_WORKSPACE = 5,   /* workspace smaller than the queried size */
+  SW_ERR_DEVICE = 6       /* a HIP launch failed */
+} sw_status;
+
+typedef struct {
+  int32_t hidden;    /* H */
+  int32_t inter;     /* I, the per-expert intermediate width */
+  int32_t n_experts; /* experts in the pool passed to the call */
+  int32_t top_k;     /* k, experts per token */
+} sw_moe_dims;
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* sw_status_str(int status);
+
+/* ABI version of this header (bumped on any signature change). */
+int32_t sw_abi_version(void);
+
+/*
+ * Prune and compact one layer's pool (Section 3.1: K'_l is the top m' experts
+ * of the layer by an importance criterion; the pruned decoder is either a
+ * checkpoint with only the retained experts and their router entries, or the
+ * full pool with a router mask).  Offline; not on the decode path.
+ *
+ *   full        dims of the full pool (n_experts = m)
+ *   importance  fp32 [m]: higher = more important.  Order is (score desc,
+ *               expert id asc); NaN scores give a valid but unspecified set.
+ *   n_keep      m', with top_k <= m' <= m (else SW_ERR_SHAPE)
+ *   kept        out int32 [m']: retained original ids, ascending
+ *   remap       out int32 [m]: compact index of each original id, -1 if pruned
+ *   keep_mask   out uint8 [m]: 1 = retained (the router mask of Eq. 2)
+ *   w13_c, w2_c, wr_c, bias_c
+ *               out, each nullable: the compacted pool [m', ...] in kept
+ *               order.  A non-NULL output needs its non-NULL source
+ *               (w13, w2, wr, bias); passing all four as NULL gives the
+ *               mask-only form for phase-aware masking.
+ */
+sw_status sw_moe_prune_compact(const sw_moe_dims* full, const float* importance, int32_t n_keep,
+                               const uint16_t* w13, const uint16_t* w2, const float* wr,
+                               const float* bias, int32_t* kept, int32_t* remap, uint8_t* keep_mask,
+                               uint16_t* w13_c, uint16_t* w2_c, float* wr_c, float* bias_c,
+                               void* stream);
+
+/* Workspace bytes sw_moe_route needs for T tokens (0 if T == 0). */
+size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
+
+/*
+ * Route T tokens (Section 3.1, Eq. 2 and the renormalisation after it):
+ * fp32 logits z = wr . x (+ bias); experts with keep_mask[e] == 0 are
+ * excluded from selection (tau = -inf); the top-k by (z desc, id asc) are
+ * emitted in that order; gates are the softmax of the k selected logits
+ * (equal to a softmax over all experts followed by renormalisation over the
+ * k), so a gate never depends on the masked experts.
+ *
+ *   keep_mask  nullable uint8 [m]; NULL = every expert eligible
+ *   bias       nullable fp32 [m]
+ *   topk_ids   out int32 [T, k], pool ids
+ *   topk_w     out fp32  [T, k]
+ *   gap        nullable out fp32 [T]: z_(k) - z_(k+1) over the eligible
+ *              experts (+inf when exactly k are eligible): tokens with a
+ *              tiny gap are near ties whose k-th choice depends on rounding.
+ *   workspace  >= sw_moe_route_workspace_bytes(d, T) bytes, 16-byte aligned
+ * In-band error: if fewer than k experts are eligible, the missing slots get
+ * id -1 and gate 0 and gap is NaN (sw_moe_dispatch then flags the batch).
+ */
+sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
+                       const float* bias, const uint8_t* keep_mask, int32_t* topk_ids,
+                       float* topk_w, float* gap, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/*
+ * Dispatch plan of the step (Section 2.1: the step streams the union of the
+ * experts selected across the batch; n_active is the realised E_distinct
+ * of Eq. 1).
+ *
+ *   topk_ids  int32 [T, k]
+ *   counts    out int32 [m]: pairs (t, j) routed to each expert
+ *   offsets   out int32 [m + 1]: exclusive prefix sum of counts, offsets[m] = T*k
+ *   perm      out int32 [T*k]: flat pair ids p = t*k + j grouped by expert
+ *             (ascending expert id), ascending p within an expert
+ *   active    out int32 [m]: experts with a nonzero count, ascending; the
+ *             first *n_active entries are valid
+ *   n_active  out int32 [1] (device)
+ * In-band error: an id outside [0, m) sets *n_active = -1, counts and
+ * offsets to 0 and perm to the identity; sw_moe_forward then writes NaN.
+ */
+sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t n_tokens,
+                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* active,
+                          int32_t* n_active, void* stream);
+
+/* Workspace bytes sw_moe_forward (and its phases) need for T tokens. */
+size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
+
+/*
+ * Expert FFNs and combine (Section 2.1 / 3.1: each token is processed by
+ * its k experts, whose outputs are combined with the renormalised gates).
+ * For every active expert e and every pair routed to it, the SwiGLU FFN
+ *     g = W13[e, 0:I] x_t,  u = W13[e, I:2I] x_t,  a = silu(g) * u,
+ *     y = W2[e] a                          (fp32 accumulation)
+ * and out[t] = sum_j topk_w[t, j] * y(t, j), summed in slot order.  Each
+ * active expert's weights are read from HBM once per call.  The same call
+ * serves the full pool (prefill shape) and the pruned pool (decode shape).
+ *
+ *   topk_w     fp32 [T, k] gates from sw_moe_route
+ *   counts/offsets/perm/active/n_active  the dispatch plan of the same
+ *              routing, from sw_moe_dispatch
+ *   out        out fp32 [T, H]
+ *   workspace  >= sw_moe_forward_workspace_bytes(d, T) bytes, 16-byte aligned
+ * In-band error: *n_active < 0 (a flagged dispatch) fills out with NaN.
+ * Deterministic: repeated calls on the same inputs give identical bits.
+ */
+sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                         const uint16_t* w13, const uint16_t* w2, const float* topk_w,
+                         const int32_t* counts, const int32_t* offsets,
+                         const int32_t* perm, const int32_t* active, const int32_t* n_active,
+                         float* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The three phases of sw_moe_forward, in order, for callers that time them
+ * or interleave other work between them.  Arguments have the meaning given
+ * for sw_moe_forward, and the phases communicate through `workspace`:
+ *   gate_up: h = silu(W13_gate x) * (W13_up x) for every routed pair
+ *   down:    y = W2 h for every routed pair
+ *   combine: out[t] = sum_j topk_w[t, j] * y(t, j)
+ */
+sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                 const uint16_t* w13, const int32_t* counts,
+                                 const int32_t* offsets, const int32_t* perm,
+                                 const int32_t* active, const int32_t* n_active, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint16_t* w2,
+                              const int32_t* counts, const int32_t* offsets, const int32_t* perm,
+                              const int32_t* active, const int32_t* n_active, void* workspace,
+                              size_t workspace_bytes, void* stream);
+sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
+                                 const int32_t* n_active, float* out, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

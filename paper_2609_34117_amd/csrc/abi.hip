@@ -1,0 +1,212 @@
+// C ABI of libslimwise: argument validation, then kernel launches on the
+// caller's stream.  Nothing is launched unless every check passes.
+#include <hip/hip_runtime.h>
+
+#include "../../include/slimwise.h"
+#include "sw_launch.h"
+
+namespace {
+
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxTopK = 32;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+
+sw_status check_dims(const sw_moe_dims* d) {
+  if (d == nullptr) return SW_ERR_NULL;
+  if (d->hidden <= 0 || d->inter <= 0 || d->n_experts <= 0 || d->top_k <= 0) return SW_ERR_SHAPE;
+  if (d->top_k > d->n_experts) return SW_ERR_SHAPE;
+  if ((d->hidden & 7) != 0 || (d->inter & 7) != 0) return SW_ERR_ALIGN;
+  if (d->n_experts > kMaxExperts || d->top_k > kMaxTopK) return SW_ERR_UNSUPPORTED;
+  return SW_OK;
+}
+
+sw_status check_tokens(const sw_moe_dims* d, int32_t n_tokens) {
+  if (n_tokens < 0) return SW_ERR_SHAPE;
+  if ((int64_t)n_tokens * d->top_k >= ((int64_t)1 << 31)) return SW_ERR_UNSUPPORTED;
+  // keeps the per-pair fp32 workspace (T * k * H elements) under 4 TiB
+  if ((int64_t)n_tokens * d->top_k * d->hidden >= ((int64_t)1 << 40)) return SW_ERR_UNSUPPORTED;
+  return SW_OK;
+}
+
+sw_status launched(hipError_t err) { return err == hipSuccess ? SW_OK : SW_ERR_DEVICE; }
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+#define SW_TRY(expr)                 \
+  do {                               \
+    const sw_status st_ = (expr);    \
+    if (st_ != SW_OK) return st_;    \
+  } while (0)
+
+sw_status check_forward_common(const sw_moe_dims* d, int32_t n_tokens, const int32_t* counts,
+                               const int32_t* offsets, const int32_t* perm,
+                               const int32_t* active, const int32_t* n_active, void* workspace,
+                               size_t workspace_bytes) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0) return SW_OK;
+  if (!counts || !offsets || !perm || !active || !n_active || !workspace) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(perm) || !aligned4(active) ||
+      !aligned4(n_active) || !aligned16(workspace))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k))
+    return SW_ERR_WORKSPACE;
+  return SW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sw_status_str(int status) {
+  switch (status) {
+    case SW_OK: return "SW_OK";
+    case SW_ERR_NULL: return "SW_ERR_NULL: a required pointer is NULL";
+    case SW_ERR_SHAPE: return "SW_ERR_SHAPE: a size is out of range";
+    case SW_ERR_ALIGN: return "SW_ERR_ALIGN: pointer not 16-byte aligned or H/I not a multiple of 8";
+    case SW_ERR_UNSUPPORTED: return "SW_ERR_UNSUPPORTED: outside the kernels' limits";
+    case SW_ERR_WORKSPACE: return "SW_ERR_WORKSPACE: workspace too small";
+    case SW_ERR_DEVICE: return "SW_ERR_DEVICE: a HIP launch failed";
+    default: return "unknown sw_status";
+  }
+}
+
+int32_t sw_abi_version(void) { return 1; }
+
+sw_status sw_moe_prune_compact(const sw_moe_dims* full, const float* importance, int32_t n_keep,
+                               const uint16_t* w13, const uint16_t* w2, const float* wr,
+                               const float* bias, int32_t* kept, int32_t* remap, uint8_t* keep_mask,
+                               uint16_t* w13_c, uint16_t* w2_c, float* wr_c, float* bias_c,
+                               void* stream) {
+  SW_TRY(check_dims(full));
+  if (n_keep < full->top_k || n_keep > full->n_experts) return SW_ERR_SHAPE;
+  if (!importance || !kept || !remap || !keep_mask) return SW_ERR_NULL;
+  if ((w13_c && !w13) || (w2_c && !w2) || (wr_c && !wr) || (bias_c && !bias)) return SW_ERR_NULL;
+  if (!aligned4(importance) || !aligned4(kept) || !aligned4(remap)) return SW_ERR_ALIGN;
+  if ((w13_c && (!aligned16(w13) || !aligned16(w13_c))) ||
+      (w2_c && (!aligned16(w2) || !aligned16(w2_c))) ||
+      (wr_c && (!aligned16(wr) || !aligned16(wr_c))) ||
+      (bias_c && (!aligned4(bias) || !aligned4(bias_c))))
+    return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  const hipStream_t s = as_stream(stream);
+  SW_TRY(launched(sw::launch_prune_select(importance, full->n_experts, n_keep, kept, remap,
+                                          keep_mask, s)));
+  return launched(sw::launch_compact_gather(kept, n_keep, full->hidden, full->inter, w13, w2, wr,
+                                            bias, w13_c, w2_c, wr_c, bias_c, s));
+}
+
+size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
+  if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
+  return sw::route_workspace_bytes(n_tokens, d->n_experts);
+}
+
+sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
+                       const float* bias, const uint8_t* keep_mask, int32_t* topk_ids,
+                       float* topk_w, float* gap, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0) return SW_OK;
+  if (!x || !wr || !topk_ids || !topk_w || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
+      !aligned4(topk_w) || (gap && !aligned4(gap)) || (bias && !aligned4(bias)))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->n_experts)) return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_route(x, n_tokens, wr, bias, keep_mask, d->hidden, d->n_experts,
+                                   d->top_k, topk_ids, topk_w, gap, workspace,
+                                   as_stream(stream)));
+}
+
+sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t n_tokens,
+                          int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* active,
+                          int32_t* n_active, void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
+  if (n_tokens > 0 && (!topk_ids || !perm)) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(active) || !aligned4(n_active) ||
+      (n_tokens > 0 && (!aligned4(topk_ids) || !aligned4(perm))))
+    return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launched(sw::launch_dispatch(topk_ids, n_tokens * d->top_k, d->n_experts, counts,
+                                      offsets, perm, active, n_active, as_stream(stream)));
+}
+
+size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
+  if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
+  return sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k);
+}
+
+sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                 const uint16_t* w13, const int32_t* counts,
+                                 const int32_t* offsets, const int32_t* perm,
+                                 const int32_t* active, const int32_t* n_active, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
+                              workspace_bytes));
+  if (n_tokens == 0) return SW_OK;
+  if (!x || !w13) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w13)) return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launched(sw::launch_gate_up(x, n_tokens, w13, counts, offsets, perm, active, n_active,
+                                     d->hidden, d->inter, d->n_experts, d->top_k, workspace,
+                                     as_stream(stream)));
+}
+
+sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint16_t* w2,
+                              const int32_t* counts, const int32_t* offsets, const int32_t* perm,
+                              const int32_t* active, const int32_t* n_active, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
+                              workspace_bytes));
+  if (n_tokens == 0) return SW_OK;
+  if (!w2) return SW_ERR_NULL;
+  if (!aligned16(w2)) return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launched(sw::launch_down(n_tokens, w2, counts, offsets, perm, active, n_active,
+                                  d->hidden, d->inter, d->n_experts, d->top_k, workspace,
+                                  as_stream(stream)));
+}
+
+sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
+                                 const int32_t* n_active, float* out, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0) return SW_OK;
+  if (!topk_w || !n_active || !out || !workspace) return SW_ERR_NULL;
+  if (!aligned4(topk_w) || !aligned4(n_active) || !aligned16(out) || !aligned16(workspace))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, d->hidden, d->inter,
+                                     d->n_experts, d->top_k, workspace, as_stream(stream)));
+}
+
+sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                         const uint16_t* w13, const uint16_t* w2, const float* topk_w,
+                         const int32_t* counts, const int32_t* offsets,
+                         const int32_t* perm, const int32_t* active, const int32_t* n_active,
+                         float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
+                              workspace_bytes));
+  if (n_tokens == 0) return SW_OK;
+  if (!x || !w13 || !w2 || !topk_w || !out) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) || !aligned4(topk_w))
+    return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  const hipStream_t s = as_stream(stream);
+  const int H = d->hidden, I = d->inter, m = d->n_experts, k = d->top_k;
+  SW_TRY(launched(sw::launch_gate_up(x, n_tokens, w13, counts, offsets, perm, active, n_active, H,
+                                     I, m, k, workspace, s)));
+  SW_TRY(launched(sw::launch_down(n_tokens, w2, counts, offsets, perm, active, n_active, H, I, m,
+                                  k, workspace, s)));
+  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, m, k, workspace, s));
+}
+
+}  // extern "C"

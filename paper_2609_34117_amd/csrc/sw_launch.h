@@ -1,0 +1,40 @@
+// Host-side launchers of the libslimwise kernels.  Each enqueues on `stream`
+// and returns the launch status; arguments are validated by the ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace sw {
+
+__host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+size_t route_workspace_bytes(int T, int m);
+size_t forward_workspace_bytes(int T, int H, int I, int k);
+
+hipError_t launch_prune_select(const float* importance, int m, int n_keep, int32_t* kept,
+                               int32_t* remap, uint8_t* keep_mask, hipStream_t stream);
+hipError_t launch_compact_gather(const int32_t* kept, int n_keep, int H, int I,
+                                 const uint16_t* w13, const uint16_t* w2, const float* wr,
+                                 const float* bias, uint16_t* w13_c, uint16_t* w2_c, float* wr_c,
+                                 float* bias_c, hipStream_t stream);
+
+hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* bias,
+                        const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
+                        float* topk_w, float* gap, void* workspace, hipStream_t stream);
+
+hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts, int* offsets,
+                           int* perm, int* active, int* n_active, hipStream_t stream);
+
+hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, const int* counts,
+                          const int* offsets, const int* perm, const int* active,
+                          const int* n_active, int H, int I, int m, int k, void* workspace,
+                          hipStream_t stream);
+hipError_t launch_down(int T, const uint16_t* w2, const int* counts, const int* offsets,
+                       const int* perm, const int* active, const int* n_active, int H, int I,
+                       int m, int k, void* workspace, hipStream_t stream);
+hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,
+                          int I, int m, int k, void* workspace, hipStream_t stream);
+
+}  // namespace sw

@@ -1,0 +1,248 @@
+"""Thin ctypes binding of libslimwise (the C ABI in ``include/slimwise.h``).
+
+Argument marshalling only: every step of the layer runs in the HIP kernels of
+``libslimwise.so``.  torch supplies device memory and the current stream.
+bf16 tensors may be ``torch.bfloat16`` or ``torch.uint16``/``torch.int16``
+bit patterns.  Importing this module loads the library and raises if it is
+not built -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libslimwise.so")
+
+SW_OK = 0
+
+
+class SlimwiseError(RuntimeError):
+    pass
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is not built: run `python -m paper_2609_34117_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    D = ctypes.POINTER(Dims)
+    sig = {
+        "sw_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "sw_abi_version": ([], I32),
+        "sw_moe_prune_compact": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, P, P], ctypes.c_int),
+        "sw_moe_route_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_route": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_dispatch": ([D, P, I32, P, P, P, P, P, P], ctypes.c_int),
+        "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_forward": ([D, P, I32, P, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_gate_up": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_down": ([D, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = res
+    return lib
+
+
+LIB = _load()
+ABI_VERSION = 1
+if LIB.sw_abi_version() != ABI_VERSION:
+    raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
+
+_BF16 = (torch.bfloat16, torch.uint16, torch.int16)
+
+
+def _check(st: int, what: str):
+    if st != SW_OK:
+        raise SlimwiseError(f"{what}: {LIB.sw_status_str(st).decode()}")
+
+
+def _ptr(t: Optional[torch.Tensor], dtypes=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def dims(hidden: int, inter: int, n_experts: int, top_k: int) -> Dims:
+    return Dims(hidden, inter, n_experts, top_k)
+
+
+def _empty(shape, dtype, device):
+    return torch.empty(shape, dtype=dtype, device=device)
+
+
+def sw_moe_route_workspace_bytes(d: Dims, n_tokens: int) -> int:
+    return LIB.sw_moe_route_workspace_bytes(ctypes.byref(d), n_tokens)
+
+
+def sw_moe_forward_workspace_bytes(d: Dims, n_tokens: int) -> int:
+    return LIB.sw_moe_forward_workspace_bytes(ctypes.byref(d), n_tokens)
+
+
+def workspace(nbytes: int, device) -> torch.Tensor:
+    """A 256-byte-aligned byte buffer (torch's caching allocator aligns to 512)."""
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def sw_moe_prune_compact(importance: torch.Tensor, n_keep: int, top_k: int, *, hidden: int = 8,
+                         inter: int = 8, w13=None, w2=None, wr=None, bias=None, compact=True,
+                         stream=None) -> dict:
+    """Section 3.1: kept set, remap, mask and (if ``compact``) the compacted pool."""
+    dev = importance.device
+    m = importance.shape[0]
+    if w13 is not None:
+        inter, hidden = w13.shape[1] // 2, w13.shape[2]
+    elif wr is not None:
+        hidden = wr.shape[1]
+    d = Dims(hidden, inter, m, top_k)
+    kept = _empty(max(n_keep, 0), torch.int32, dev)
+    remap = _empty(m, torch.int32, dev)
+    mask = _empty(m, torch.uint8, dev)
+    w13_c = _empty((n_keep, 2 * inter, hidden), w13.dtype, dev) if compact and w13 is not None else None
+    w2_c = _empty((n_keep, hidden, inter), w2.dtype, dev) if compact and w2 is not None else None
+    wr_c = _empty((n_keep, hidden), torch.float32, dev) if compact and wr is not None else None
+    bias_c = _empty(n_keep, torch.float32, dev) if compact and bias is not None else None
+    st = LIB.sw_moe_prune_compact(
+        ctypes.byref(d), _ptr(importance, (torch.float32,), "importance"), n_keep,
+        _ptr(w13, _BF16, "w13"), _ptr(w2, _BF16, "w2"), _ptr(wr, (torch.float32,), "wr"),
+        _ptr(bias, (torch.float32,), "bias"), _ptr(kept), _ptr(remap), _ptr(mask),
+        _ptr(w13_c), _ptr(w2_c), _ptr(wr_c), _ptr(bias_c), _stream(stream))
+    _check(st, "sw_moe_prune_compact")
+    return dict(kept=kept, remap=remap, keep_mask=mask, w13=w13_c, w2=w2_c, wr=wr_c, bias=bias_c)
+
+
+def sw_moe_route(x: torch.Tensor, wr: torch.Tensor, top_k: int, *, keep_mask=None, bias=None,
+                 want_gap=True, out=None, ws=None, stream=None):
+    """Section 3.1, Eq. 2: masked top-k and renormalised gates.
+
+    Returns ``(topk_ids, topk_w, gap)``; ``out`` may supply that tuple."""
+    t, hidden = x.shape
+    m = wr.shape[0]
+    d = Dims(hidden, 8, m, top_k)
+    if out is None:
+        out = (_empty((t, top_k), torch.int32, x.device), _empty((t, top_k), torch.float32, x.device),
+               _empty(t, torch.float32, x.device) if want_gap else None)
+    ids, w, gap = out
+    nbytes = sw_moe_route_workspace_bytes(d, t)
+    if ws is None:
+        ws = workspace(nbytes, x.device)
+    st = LIB.sw_moe_route(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
+                          _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
+                          _ptr(ids), _ptr(w), _ptr(gap), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "sw_moe_route")
+    return ids, w, gap
+
+
+@dataclass
+class Plan:
+    """Dispatch plan of one step (device tensors)."""
+    counts: torch.Tensor
+    offsets: torch.Tensor
+    perm: torch.Tensor
+    active: torch.Tensor
+    n_active: torch.Tensor
+
+
+def alloc_plan(n_tokens: int, n_experts: int, top_k: int, device) -> Plan:
+    return Plan(_empty(n_experts, torch.int32, device), _empty(n_experts + 1, torch.int32, device),
+                _empty(max(n_tokens * top_k, 1), torch.int32, device),
+                _empty(n_experts, torch.int32, device), _empty(1, torch.int32, device))
+
+
+def sw_moe_dispatch(topk_ids: torch.Tensor, n_experts: int, *, plan: Optional[Plan] = None,
+                    stream=None) -> Plan:
+    """Section 2.1: histogram, offsets, stable permutation, active set."""
+    t, k = topk_ids.shape
+    d = Dims(8, 8, n_experts, k)
+    if plan is None:
+        plan = alloc_plan(t, n_experts, k, topk_ids.device)
+    st = LIB.sw_moe_dispatch(ctypes.byref(d), _ptr(topk_ids, (torch.int32,), "topk_ids"), t,
+                             _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+                             _ptr(plan.active), _ptr(plan.n_active), _stream(stream))
+    _check(st, "sw_moe_dispatch")
+    return plan
+
+
+def _fwd_dims(x_or_t, w13_or_w2, top_k, which="w13"):
+    if which == "w13":
+        m, two_i, hidden = w13_or_w2.shape
+        return Dims(hidden, two_i // 2, m, top_k)
+    m, hidden, inter = w13_or_w2.shape
+    return Dims(hidden, inter, m, top_k)
+
+
+def sw_moe_forward(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor, topk_w: torch.Tensor,
+                   plan: Plan, *, out=None, ws=None, stream=None) -> torch.Tensor:
+    """Expert SwiGLU FFNs of every routed pair and the gate-weighted combine."""
+    t = x.shape[0]
+    d = _fwd_dims(x, w13, topk_w.shape[1])
+    if out is None:
+        out = _empty((t, d.hidden), torch.float32, x.device)
+    if ws is None:
+        ws = workspace(sw_moe_forward_workspace_bytes(d, t), x.device)
+    st = LIB.sw_moe_forward(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
+                            _ptr(w2, _BF16, "w2"), _ptr(topk_w, (torch.float32,), "topk_w"),
+                            _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+                            _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
+                            _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "sw_moe_forward")
+    return out
+
+
+def sw_moe_forward_gate_up(x, w13, top_k, plan: Plan, ws, stream=None):
+    t = x.shape[0]
+    d = _fwd_dims(x, w13, top_k)
+    st = LIB.sw_moe_forward_gate_up(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
+                                    _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+                                    _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
+                                    _stream(stream))
+    _check(st, "sw_moe_forward_gate_up")
+
+
+def sw_moe_forward_down(n_tokens, w2, top_k, plan: Plan, ws, stream=None):
+    d = _fwd_dims(n_tokens, w2, top_k, which="w2")
+    st = LIB.sw_moe_forward_down(ctypes.byref(d), n_tokens, _ptr(w2, _BF16, "w2"),
+                                 _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+                                 _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
+                                 _stream(stream))
+    _check(st, "sw_moe_forward_down")
+
+
+def sw_moe_forward_combine(topk_w, hidden, inter, n_experts, plan: Plan, out, ws, stream=None):
+    t, k = topk_w.shape
+    d = Dims(hidden, inter, n_experts, k)
+    st = LIB.sw_moe_forward_combine(ctypes.byref(d), t, _ptr(topk_w, (torch.float32,), "topk_w"),
+                                    _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
+                                    _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "sw_moe_forward_combine")
+
+
+def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, stream=None) -> dict:
+    """Route, dispatch and forward of one layer (allocating convenience wrapper)."""
+    ids, w, gap = sw_moe_route(x, wr, top_k, keep_mask=keep_mask, bias=bias, stream=stream)
+    plan = sw_moe_dispatch(ids, wr.shape[0], stream=stream)
+    out = sw_moe_forward(x, w13, w2, w, plan, stream=stream)
+    return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)

@@ -1,0 +1,138 @@
+"""CPU checks of the C ABI: the library loads, exports every symbol the header
+declares, and rejects bad arguments before touching the device (so these
+calls need no GPU and launch nothing)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "slimwise.h")
+LIB_PATH = os.path.join(ROOT, "paper_2609_34117_amd", "libslimwise.so")
+
+SW_OK, SW_ERR_NULL, SW_ERR_SHAPE, SW_ERR_ALIGN, SW_ERR_UNSUPPORTED, SW_ERR_WORKSPACE = range(6)
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32),
+                ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32)]
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sw_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LIB_PATH):
+        from paper_2609_34117_amd import build
+        build.build()
+    return ctypes.CDLL(LIB_PATH)
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("sw_moe_prune_compact", "sw_moe_route", "sw_moe_dispatch", "sw_moe_forward"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    missing = [n for n in declared_functions() if n not in exported]
+    assert not missing, missing
+    for n in declared_functions():
+        getattr(lib, n)
+
+
+def test_status_strings_and_version(lib):
+    lib.sw_status_str.restype = ctypes.c_char_p
+    for s in range(7):
+        assert lib.sw_status_str(s).startswith(b"SW_")
+    assert lib.sw_abi_version() == 1
+
+
+def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
+    f = lib.sw_moe_route
+    P = ctypes.c_void_p
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    return f(ctypes.byref(d) if d is not None else None, x, t, wr, None, None, ids, w, None, ws,
+             nbytes, None)
+
+
+def test_route_validation_precedes_any_launch(lib):
+    ok = Dims(64, 32, 8, 2)
+    assert _route(lib, None) == SW_ERR_NULL
+    assert _route(lib, Dims(0, 32, 8, 2)) == SW_ERR_SHAPE
+    assert _route(lib, Dims(64, 32, 8, 9)) == SW_ERR_SHAPE        # k > m
+    assert _route(lib, Dims(60, 32, 8, 2)) == SW_ERR_ALIGN        # H % 8
+    assert _route(lib, Dims(64, 32, 2048, 2)) == SW_ERR_UNSUPPORTED
+    assert _route(lib, Dims(64, 32, 64, 33)) == SW_ERR_UNSUPPORTED
+    assert _route(lib, ok, t=-1) == SW_ERR_SHAPE
+    assert _route(lib, ok, x=None) == SW_ERR_NULL
+    assert _route(lib, ok, x=24) == SW_ERR_ALIGN                 # not 16-byte aligned
+    assert _route(lib, ok, ids=18) == SW_ERR_ALIGN
+    assert _route(lib, ok, nbytes=16) == SW_ERR_WORKSPACE
+    assert _route(lib, ok, t=0, x=None, wr=None) == SW_OK         # empty batch: nothing to do
+    assert _route(lib, Dims(64, 32, 8, 8), t=(1 << 28)) == SW_ERR_UNSUPPORTED  # T*k >= 2^31
+
+
+def test_workspace_queries(lib):
+    P = ctypes.POINTER(Dims)
+    for name in ("sw_moe_route_workspace_bytes", "sw_moe_forward_workspace_bytes"):
+        f = getattr(lib, name)
+        f.argtypes = [P, ctypes.c_int32]
+        f.restype = ctypes.c_size_t
+        assert f(ctypes.byref(Dims(2048, 512, 256, 8)), 0) == 0
+        assert f(None, 8) == 0
+    f = lib.sw_moe_forward_workspace_bytes
+    # h hi/lo (2 x T*k*I bf16) + y (T*k*H fp32)
+    assert f(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 2 * 512 * 512 * 2 + 512 * 2048 * 4
+    assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 64 * 256 * 4
+
+
+def test_prune_and_dispatch_validation(lib):
+    P = ctypes.c_void_p
+    pc = lib.sw_moe_prune_compact
+    pc.argtypes = [ctypes.POINTER(Dims)] + [P, ctypes.c_int32] + [P] * 11 + [P]
+    d = Dims(64, 32, 16, 4)
+    assert pc(ctypes.byref(d), 16, 3, None, None, None, None, 16, 16, 16, None, None, None, None, None) == SW_ERR_SHAPE
+    assert pc(ctypes.byref(d), 16, 17, None, None, None, None, 16, 16, 16, None, None, None, None, None) == SW_ERR_SHAPE
+    assert pc(ctypes.byref(d), None, 8, None, None, None, None, 16, 16, 16, None, None, None, None, None) == SW_ERR_NULL
+    # a compacted output needs its source
+    assert pc(ctypes.byref(d), 16, 8, None, None, None, None, 16, 16, 16, 16, None, None, None, None) == SW_ERR_NULL
+    assert pc(ctypes.byref(d), 16, 8, 16, None, None, None, 16, 16, 16, 24, None, None, None, None) == SW_ERR_ALIGN
+    dp = lib.sw_moe_dispatch
+    dp.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P]
+    assert dp(ctypes.byref(d), 16, 4, None, 16, 16, 16, 16, None) == SW_ERR_NULL
+    assert dp(ctypes.byref(d), None, 4, 16, 16, 16, 16, 16, None) == SW_ERR_NULL
+    assert dp(ctypes.byref(d), 16, 4, 18, 16, 16, 16, 16, None) == SW_ERR_ALIGN
+
+
+def test_forward_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.sw_moe_forward
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P,
+                  ctypes.c_size_t, P]
+    d = Dims(64, 32, 8, 2)
+    q = lib.sw_moe_forward_workspace_bytes
+    q.argtypes = [ctypes.POINTER(Dims), ctypes.c_int32]
+    q.restype = ctypes.c_size_t
+    need = q(ctypes.byref(d), 4)
+    args = dict(x=16, w13=16, w2=16, tw=16, c=16, o=16, p=16, a=16, na=16, out=16, ws=16)
+
+    def call(nbytes=need, **kw):
+        a = dict(args, **kw)
+        return f(ctypes.byref(d), a["x"], 4, a["w13"], a["w2"], a["tw"], a["c"], a["o"], a["p"],
+                 a["a"], a["na"], a["out"], a["ws"], nbytes, None)
+
+    assert call(nbytes=need - 1) == SW_ERR_WORKSPACE
+    assert call(w2=None) == SW_ERR_NULL
+    assert call(na=None) == SW_ERR_NULL
+    assert call(out=20) == SW_ERR_ALIGN
+    assert call(ws=8) == SW_ERR_ALIGN

@@ -1,0 +1,264 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on the
+same seeded inputs.  Tolerances and the near-tie rule are in parity.py."""
+import functools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_34117_amd import inputs as I
+from parity import compare_out, compare_routing
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def sw():
+    assert torch.cuda.is_available(), "GPU tests need a device"
+    from paper_2609_34117_amd import slimwise
+
+    return slimwise
+
+
+def dev(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).cuda()
+
+
+def host(t):
+    a = t.cpu().numpy()
+    return a.view(np.uint16) if a.dtype == np.int16 else a
+
+
+@functools.lru_cache(maxsize=2)
+def layer_inputs(name, layer=0):
+    cfg = I.CONFIGS[name]
+    L = I.make_layer(cfg, layer=layer)
+    D = {k: dev(v) for k, v in L.items() if isinstance(v, np.ndarray)}
+    return cfg, L, D
+
+
+def small_layer(hidden, n_experts, top_k, inter, tokens, seed=0):
+    cfg = I.MoEConfig("edge", 200 + seed, hidden=hidden, n_experts=n_experts, top_k=top_k,
+                      inter=inter, tokens=tokens)
+    L = I.make_layer(cfg)
+    D = {k: dev(v) for k, v in L.items() if isinstance(v, np.ndarray)}
+    return cfg, L, D
+
+
+def mask_for(cfg, L, pruning):
+    if pruning == 0:
+        return None
+    return oracle.prune_compact(L["importance"], cfg.n_keep(pruning), cfg.top_k)[2]
+
+
+def run_gpu_layer(sw, D, k, mask=None, x=None, bias=None):
+    xm = D["x"] if x is None else x
+    keep = None if mask is None else dev(mask)
+    return sw.moe_layer(xm, D["wr"], D["w13"], D["w2"], k, keep_mask=keep, bias=bias)
+
+
+def check_layer(sw, cfg, L, D, mask, bias=None, sample=None):
+    """Route, dispatch and forward on the GPU vs the oracle; returns stats."""
+    k = cfg.top_k
+    b_dev = None if bias is None else dev(bias)
+    g = run_gpu_layer(sw, D, k, mask=mask, bias=b_dev)
+    g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
+    o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], k, keep_mask=mask, bias=bias,
+                                          want_logits=True)
+    n_near = compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, k)
+    # dispatch: bit-exact against the oracle's dispatch of the GPU's own ids
+    counts, offsets, perm, active, n_active = oracle.dispatch(g_ids, cfg.n_experts)
+    plan = g["plan"]
+    np.testing.assert_array_equal(host(plan.counts), counts)
+    np.testing.assert_array_equal(host(plan.offsets), offsets)
+    np.testing.assert_array_equal(host(plan.perm)[: g_ids.size], perm)
+    assert int(host(plan.n_active)[0]) == n_active
+    np.testing.assert_array_equal(host(plan.active)[:n_active], active)
+    # forward: against the oracle on the GPU's routing (sampled tokens at large T)
+    rows = np.arange(g_ids.shape[0]) if sample is None else sample
+    o_out = oracle.forward(np.ascontiguousarray(L["x"][rows]), L["w13"], L["w2"],
+                           np.ascontiguousarray(g_ids[rows]), np.ascontiguousarray(g_w[rows]))
+    err, rel = compare_out(host(g["out"])[rows], o_out)
+    return dict(n_near=n_near, n_active=n_active, err=err, rel=rel, gpu=g)
+
+
+# --------------------------------------------------------------------------
+# route / dispatch / forward on the named workloads
+
+@pytest.mark.parametrize("name,pruning", [("tiny", 0.0), ("tiny", 0.5), ("decode_b64", 0.0),
+                                          ("decode_b64", 0.5)])
+def test_layer_parity(sw, name, pruning):
+    cfg, L, D = layer_inputs(name)
+    mask = mask_for(cfg, L, pruning)
+    s = check_layer(sw, cfg, L, D, mask)
+    print(f"{name} p={pruning}: n_active={s['n_active']} near_ties={s['n_near']} "
+          f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+@pytest.mark.parametrize("batch", I.SWEEP_BATCHES)
+@pytest.mark.parametrize("pruning", I.SWEEP_PRUNING)
+def test_decode_sweep_parity(sw, batch, pruning):
+    cfg, L, D = layer_inputs("decode_sweep")
+    mask = mask_for(cfg, L, pruning)
+    x = I.make_x(cfg, tokens=batch, rep=batch)
+    L2 = dict(L, x=x)
+    D2 = dict(D, x=dev(x))
+    sample = np.unique(np.linspace(0, batch - 1, min(batch, 6)).astype(int))
+    s = check_layer(sw, cfg, L2, D2, mask, sample=sample)
+    print(f"sweep B={batch} p={pruning}: n_active={s['n_active']} near_ties={s['n_near']} "
+          f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+def test_prefill_shape_parity(sw):
+    cfg, L, D = layer_inputs("decode_sweep")  # same layer shape, 4096 tokens through the full pool
+    pcfg = I.CONFIGS["prefill"]
+    x = I.make_x(pcfg)
+    s = check_layer(sw, cfg, dict(L, x=x), dict(D, x=dev(x)), None,
+                    sample=np.array([0, 1, 777, 2048, 4000, 4095]))
+    assert s["n_active"] == cfg.n_experts
+    print(f"prefill T=4096: near_ties={s['n_near']} max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+# --------------------------------------------------------------------------
+# pruning: masked full pool == compacted pool, 0% == full, GPU compaction
+
+@pytest.mark.parametrize("name,pruning", [("tiny", 0.5), ("decode_b64", 0.5), ("decode_sweep", 0.25)])
+def test_prune_compact_parity_and_masked_equals_compacted(sw, name, pruning):
+    cfg, L, D = layer_inputs(name)
+    n_keep = cfg.n_keep(pruning)
+    g = sw.sw_moe_prune_compact(D["importance"], n_keep, cfg.top_k, w13=D["w13"], w2=D["w2"], wr=D["wr"])
+    kept, remap, mask, w13c, w2c, wrc, _ = oracle.prune_compact(L["importance"], n_keep, cfg.top_k,
+                                                                w13=L["w13"], w2=L["w2"], wr=L["wr"])
+    np.testing.assert_array_equal(host(g["kept"]), kept)
+    np.testing.assert_array_equal(host(g["remap"]), remap)
+    np.testing.assert_array_equal(host(g["keep_mask"]), mask)
+    np.testing.assert_array_equal(host(g["wr"]), wrc)
+    assert torch.equal(g["w13"], dev(w13c)) and torch.equal(g["w2"], dev(w2c))
+    # Eq. 2: the masked router over the full pool picks exactly what the
+    # pruned checkpoint picks, with identical gates and outputs
+    masked = run_gpu_layer(sw, D, cfg.top_k, mask=mask)
+    comp = sw.moe_layer(D["x"], g["wr"], g["w13"], g["w2"], cfg.top_k)
+    kept_t = g["kept"].long()
+    assert torch.equal(masked["topk_ids"].long(), kept_t[comp["topk_ids"].long()])
+    assert torch.equal(masked["topk_w"], comp["topk_w"])
+    assert torch.equal(masked["out"], comp["out"])
+
+
+def test_zero_pruning_is_the_full_model_and_deterministic(sw):
+    cfg, L, D = layer_inputs("decode_b64")
+    a = run_gpu_layer(sw, D, cfg.top_k)
+    b = run_gpu_layer(sw, D, cfg.top_k, mask=np.ones(cfg.n_experts, np.uint8))
+    c = run_gpu_layer(sw, D, cfg.top_k)
+    for key in ("topk_ids", "topk_w", "out"):
+        assert torch.equal(a[key], b[key]), key
+        assert torch.equal(a[key], c[key]), key
+
+
+def test_pruned_experts_never_selected_and_gates_ignore_them(sw):
+    cfg, L, D = layer_inputs("decode_b64")
+    mask = mask_for(cfg, L, 0.5)
+    a = run_gpu_layer(sw, D, cfg.top_k, mask=mask)
+    ids = host(a["topk_ids"])
+    assert np.all(mask[ids] == 1)
+    wr2 = D["wr"].clone()
+    wr2[torch.from_numpy(mask == 0).cuda()] = 5.0
+    b = sw.moe_layer(D["x"], wr2, D["w13"], D["w2"], cfg.top_k, keep_mask=dev(mask))
+    for key in ("topk_ids", "topk_w", "out"):
+        assert torch.equal(a[key], b[key]), key
+
+
+# --------------------------------------------------------------------------
+# edge cases
+
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens", [
+    (72, 5, 5, 8, 3),         # every expert selected; H not a multiple of 32; I = 8
+    (64, 16, 1, 32, 17),      # top-1: gates are exactly 1
+    (256, 1024, 32, 16, 9),   # largest pool and k
+    (128, 3, 2, 24, 1),       # a single token
+    (520, 12, 4, 40, 70),     # ragged H and I tails
+])
+def test_edge_shapes(sw, hidden, n_experts, top_k, inter, tokens):
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens)
+    s = check_layer(sw, cfg, L, D, None)
+    if top_k == 1:
+        assert np.all(host(s["gpu"]["topk_w"]) == 1.0)
+
+
+def test_popular_expert_spans_several_token_passes(sw):
+    # a bias makes expert 3 every token's first choice: 200 pairs on one
+    # expert (4 passes of 64 tokens over its weights)
+    cfg, L, D = small_layer(256, 16, 2, 64, 200, seed=1)
+    bias = np.zeros(16, np.float32)
+    bias[3] = 50.0
+    s = check_layer(sw, cfg, L, D, None, bias=bias)
+    assert int(host(s["gpu"]["plan"].counts)[3]) == 200
+
+
+def test_bias_and_mask_together(sw):
+    cfg = I.CONFIGS["skewed_stack"]
+    small = I.MoEConfig("skew_small", cfg.config_id, hidden=256, n_experts=cfg.n_experts,
+                        top_k=cfg.top_k, inter=64, tokens=96, zipf_s=cfg.zipf_s,
+                        zipf_beta=cfg.zipf_beta)
+    L = I.make_layer(small)
+    D = {k: dev(v) for k, v in L.items() if isinstance(v, np.ndarray)}
+    mask = oracle.prune_compact(L["importance"], 128, small.top_k)[2]
+    check_layer(sw, small, L, D, mask, bias=L["bias"])
+
+
+def test_empty_batch(sw):
+    cfg, L, D = small_layer(64, 8, 2, 32, 1)
+    x0 = D["x"][:0]
+    ids, w, gap = sw.sw_moe_route(x0, D["wr"], 2)
+    plan = sw.sw_moe_dispatch(ids, 8)
+    out = sw.sw_moe_forward(x0, D["w13"], D["w2"], w, plan)
+    assert out.shape == (0, 64)
+    assert int(plan.n_active.item()) == 0
+    assert torch.all(plan.counts == 0) and torch.all(plan.offsets == 0)
+
+
+def test_invalid_ids_flag_the_dispatch_and_poison_the_output(sw):
+    cfg, L, D = small_layer(64, 8, 2, 32, 4)
+    ids = torch.tensor([[0, 1], [2, 9], [3, 4], [5, 6]], dtype=torch.int32, device="cuda")
+    w = torch.full((4, 2), 0.5, device="cuda")
+    plan = sw.sw_moe_dispatch(ids, 8)
+    assert int(plan.n_active.item()) == -1
+    assert torch.all(plan.counts == 0)
+    assert torch.equal(plan.perm.cpu(), torch.arange(8, dtype=torch.int32))
+    out = sw.sw_moe_forward(D["x"], D["w13"], D["w2"], w, plan)
+    assert torch.all(torch.isnan(out))
+
+
+def test_too_few_eligible_experts_in_band(sw):
+    cfg, L, D = small_layer(64, 8, 3, 32, 2)
+    mask = np.zeros(8, np.uint8)
+    mask[[1, 6]] = 1
+    ids, w, gap = sw.sw_moe_route(D["x"], D["wr"], 3, keep_mask=dev(mask))
+    ids = host(ids)
+    assert np.all(ids[:, 2] == -1) and np.all(host(w)[:, 2] == 0)
+    assert np.all(np.isnan(host(gap)))
+    assert set(ids[:, :2].ravel().tolist()) <= {1, 6}
+
+
+def test_dispatch_skewed_and_large(sw):
+    g = np.random.default_rng(5)
+    for t, m, k in [(4096, 256, 8), (3, 1024, 32), (700, 64, 1), (333, 256, 8)]:
+        rows = []
+        for i in range(t):
+            if i % 2 == 0 and k > 1:  # every other token also picks the popular expert 7
+                rest = g.choice(np.delete(np.arange(m), 7), size=k - 1, replace=False)
+                rows.append(np.insert(rest, i % k, 7))
+            else:
+                rows.append(g.choice(m, size=k, replace=False))
+        ids = np.stack(rows).astype(np.int32)
+        plan = sw.sw_moe_dispatch(dev(ids), m)
+        counts, offsets, perm, active, n_active = oracle.dispatch(ids, m)
+        np.testing.assert_array_equal(host(plan.counts), counts)
+        np.testing.assert_array_equal(host(plan.offsets), offsets)
+        np.testing.assert_array_equal(host(plan.perm)[: t * k], perm)
+        assert int(host(plan.n_active)[0]) == n_active
+        np.testing.assert_array_equal(host(plan.active)[:n_active], active)
