@@ -43,7 +43,7 @@ def _load() -> ctypes.CDLL:
         "sw_moe_route": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_dispatch": ([D, P, I32, P, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
-        "sw_moe_forward": ([D, P, I32, P, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_gate_up": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_down": ([D, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
@@ -52,6 +52,7 @@ def _load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = args
         f.restype = res
+    lib.signatures = sig
     return lib
 
 

@@ -136,3 +136,37 @@ def test_forward_validation(lib):
     assert call(na=None) == SW_ERR_NULL
     assert call(out=20) == SW_ERR_ALIGN
     assert call(ws=8) == SW_ERR_ALIGN
+
+
+def _prototypes():
+    """name -> list of parameter declarations, parsed from the header."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    protos = {}
+    for m in re.finditer(r"\b(sw_\w+)\s*\(([^;{]*?)\)\s*;", text, flags=re.S):
+        params = [p.strip() for p in m.group(2).split(",") if p.strip() and p.strip() != "void"]
+        protos[m.group(1)] = params
+    return protos
+
+
+def test_binding_signatures_match_the_header():
+    # A ctypes argtypes list shorter than the C prototype silently passes the
+    # trailing arguments as default-converted C ints (a 64-bit stream handle
+    # would arrive with garbage in its upper half), so check every binding.
+    from paper_2609_34117_amd import slimwise
+
+    protos = _prototypes()
+    assert set(slimwise.LIB.signatures) == set(protos)
+    for name, (args, _res) in slimwise.LIB.signatures.items():
+        params = protos[name]
+        assert len(args) == len(params), (name, len(args), len(params))
+        for a, decl in zip(args, params):
+            if "*" in decl:
+                assert a is ctypes.c_void_p or issubclass(a, ctypes._Pointer), (name, decl, a)
+            elif decl.startswith("size_t"):
+                assert a is ctypes.c_size_t, (name, decl, a)
+            elif decl.startswith("int32_t"):
+                assert a is ctypes.c_int32, (name, decl, a)
+            elif decl.startswith("int "):
+                assert a is ctypes.c_int, (name, decl, a)
+            else:
+                raise AssertionError(f"unhandled parameter {decl} of {name}")
