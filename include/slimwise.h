@@ -33,7 +33,8 @@
  *   - Data-dependent errors that the host cannot see without a sync are
  *     reported in-band on the device, as documented per call.
  *   - Limits: 1 <= top_k <= 32, top_k <= n_experts <= 1024, 0 <= T,
- *     T * top_k < 2^31.
+ *     T * top_k < 2^31, and (in bytes) 4*I*H, 4*m*H, 2*T*H and 2*T*k*I below 2^31
+ *     (else SW_ERR_UNSUPPORTED).
  */
 #ifndef SLIMWISE_H
 #define SLIMWISE_H
@@ -55,6 +56,13 @@ typedef enum {
   SW_ERR_DEVICE = 6       /* a HIP launch failed */
 } sw_status;
 
+/* Layout of the expert weights handed to sw_moe_forward (see
+ * sw_moe_pack_experts). */
+typedef enum {
+  SW_LAYOUT_ROW_MAJOR = 0, /* w13 [m, 2I, H], w2 [m, H, I] as documented above */
+  SW_LAYOUT_TILED = 1      /* the fragment-major layout of sw_moe_pack_experts */
+} sw_weight_layout;
+
 typedef struct {
   int32_t hidden;    /* H */
   int32_t inter;     /* I, the per-expert intermediate width */
@@ -66,6 +74,7 @@ typedef struct {
 const char* sw_status_str(int status);
 
 /* ABI version of this header (bumped on any signature change). */
+#define SW_ABI_VERSION 2
 int32_t sw_abi_version(void);
 
 /*
@@ -140,6 +149,26 @@ sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t
                           int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* active,
                           int32_t* n_active, void* stream);
 
+/*
+ * Re-lay an expert pool out for streaming (offline, once per pool; a device
+ * layout choice, not part of the paper's method).  SW_LAYOUT_TILED stores
+ * each expert's weights so that every 16-row MFMA operand fragment a wave
+ * loads is one contiguous KiB and every tile of 16 rows is contiguous:
+ *   w13_tiled: expert e, tile b (0 <= b < I/8) covers the gate rows 8b..8b+7
+ *     and the up rows I+8b..I+8b+7; its H/32 fragments follow each other;
+ *     fragment s holds, for lane l = 0..63, the 8 bf16 of tile row (l % 16)
+ *     at columns 32s + 8(l / 16) .. +7.  Element offset:
+ *     e*2IH + b*16H + s*512 + l*8 + j.
+ *   w2_tiled: expert e, tile b (0 <= b < H/16) covers output rows
+ *     16b..16b+15 over I the same way: e*HI + b*16I + s*512 + l*8 + j.
+ * Both have the size of their row-major sources.  Requires H and I to be
+ * multiples of 32, H <= 2048 and I <= 1024 (else SW_ERR_UNSUPPORTED).
+ * Either source may be NULL to skip it.  sw_moe_prune_compact copies whole
+ * experts, so it compacts tiled pools as well as row-major ones.
+ */
+sw_status sw_moe_pack_experts(const sw_moe_dims* d, const uint16_t* w13, const uint16_t* w2,
+                              uint16_t* w13_tiled, uint16_t* w2_tiled, void* stream);
+
 /* Workspace bytes sw_moe_forward (and its phases) need for T tokens. */
 size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
 
@@ -153,6 +182,8 @@ size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
  * active expert's weights are read from HBM once per call.  The same call
  * serves the full pool (prefill shape) and the pruned pool (decode shape).
  *
+ *   layout     sw_weight_layout of w13 and w2 (SW_LAYOUT_TILED needs the
+ *              shapes sw_moe_pack_experts accepts, and 4*T*k*H < 2^31)
  *   topk_w     fp32 [T, k] gates from sw_moe_route
  *   counts/offsets/perm/active/n_active  the dispatch plan of the same
  *              routing, from sw_moe_dispatch
@@ -162,8 +193,8 @@ size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
  * Deterministic: repeated calls on the same inputs give identical bits.
  */
 sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
-                         const uint16_t* w13, const uint16_t* w2, const float* topk_w,
-                         const int32_t* counts, const int32_t* offsets,
+                         const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                         const float* topk_w, const int32_t* counts, const int32_t* offsets,
                          const int32_t* perm, const int32_t* active, const int32_t* n_active,
                          float* out, void* workspace, size_t workspace_bytes, void* stream);
 
@@ -176,14 +207,14 @@ sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_toke
  *   combine: out[t] = sum_j topk_w[t, j] * y(t, j)
  */
 sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
-                                 const uint16_t* w13, const int32_t* counts,
+                                 const uint16_t* w13, int32_t layout, const int32_t* counts,
                                  const int32_t* offsets, const int32_t* perm,
                                  const int32_t* active, const int32_t* n_active, void* workspace,
                                  size_t workspace_bytes, void* stream);
 sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint16_t* w2,
-                              const int32_t* counts, const int32_t* offsets, const int32_t* perm,
-                              const int32_t* active, const int32_t* n_active, void* workspace,
-                              size_t workspace_bytes, void* stream);
+                              int32_t layout, const int32_t* counts, const int32_t* offsets,
+                              const int32_t* perm, const int32_t* active, const int32_t* n_active,
+                              void* workspace, size_t workspace_bytes, void* stream);
 sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
                                  const int32_t* n_active, float* out, void* workspace,
                                  size_t workspace_bytes, void* stream);

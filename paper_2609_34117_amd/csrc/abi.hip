@@ -9,6 +9,7 @@ namespace {
 
 constexpr int kMaxExperts = 1024;
 constexpr int kMaxTopK = 32;
+constexpr int64_t kMaxBufferBytes = (int64_t)1 << 31;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -19,18 +20,41 @@ sw_status check_dims(const sw_moe_dims* d) {
   if (d->top_k > d->n_experts) return SW_ERR_SHAPE;
   if ((d->hidden & 7) != 0 || (d->inter & 7) != 0) return SW_ERR_ALIGN;
   if (d->n_experts > kMaxExperts || d->top_k > kMaxTopK) return SW_ERR_UNSUPPORTED;
+  // each expert's gate/up block is addressed through one 32-bit-ranged buffer
+  if (4 * (int64_t)d->inter * d->hidden >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
+  // ... and so is the router weight
+  if (4 * (int64_t)d->n_experts * d->hidden >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
   return SW_OK;
 }
 
 sw_status check_tokens(const sw_moe_dims* d, int32_t n_tokens) {
   if (n_tokens < 0) return SW_ERR_SHAPE;
   if ((int64_t)n_tokens * d->top_k >= ((int64_t)1 << 31)) return SW_ERR_UNSUPPORTED;
+  // token activations and the per-pair intermediate are read through
+  // 32-bit-ranged buffers
+  if (2 * (int64_t)n_tokens * d->hidden >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
+  if (2 * (int64_t)n_tokens * d->top_k * d->inter >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
   // keeps the per-pair fp32 workspace (T * k * H elements) under 4 TiB
   if ((int64_t)n_tokens * d->top_k * d->hidden >= ((int64_t)1 << 40)) return SW_ERR_UNSUPPORTED;
   return SW_OK;
 }
 
 sw_status launched(hipError_t err) { return err == hipSuccess ? SW_OK : SW_ERR_DEVICE; }
+
+bool tiled_shape_ok(const sw_moe_dims* d) {
+  return d->hidden % 32 == 0 && d->inter % 32 == 0 && d->hidden <= sw::kMaxStreamH &&
+         d->inter <= sw::kMaxStreamI;
+}
+
+// Layout argument of the forward calls: known value, and a tiled pool only
+// for the shapes (and token counts) the tiled kernels take.
+sw_status check_layout(const sw_moe_dims* d, int32_t n_tokens, int32_t layout) {
+  if (layout != SW_LAYOUT_ROW_MAJOR && layout != SW_LAYOUT_TILED) return SW_ERR_SHAPE;
+  if (layout == SW_LAYOUT_TILED &&
+      (!tiled_shape_ok(d) || !sw::wave_stream_supported(n_tokens, d->hidden, d->inter, d->top_k)))
+    return SW_ERR_UNSUPPORTED;
+  return SW_OK;
+}
 
 hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
@@ -73,7 +97,7 @@ const char* sw_status_str(int status) {
   }
 }
 
-int32_t sw_abi_version(void) { return 1; }
+int32_t sw_abi_version(void) { return SW_ABI_VERSION; }
 
 sw_status sw_moe_prune_compact(const sw_moe_dims* full, const float* importance, int32_t n_keep,
                                const uint16_t* w13, const uint16_t* w2, const float* wr,
@@ -96,6 +120,19 @@ sw_status sw_moe_prune_compact(const sw_moe_dims* full, const float* importance,
                                           keep_mask, s)));
   return launched(sw::launch_compact_gather(kept, n_keep, full->hidden, full->inter, w13, w2, wr,
                                             bias, w13_c, w2_c, wr_c, bias_c, s));
+}
+
+sw_status sw_moe_pack_experts(const sw_moe_dims* d, const uint16_t* w13, const uint16_t* w2,
+                              uint16_t* w13_tiled, uint16_t* w2_tiled, void* stream) {
+  SW_TRY(check_dims(d));
+  if (!tiled_shape_ok(d)) return SW_ERR_UNSUPPORTED;
+  if ((w13 && !w13_tiled) || (w2 && !w2_tiled)) return SW_ERR_NULL;
+  if ((w13 && (!aligned16(w13) || !aligned16(w13_tiled))) ||
+      (w2 && (!aligned16(w2) || !aligned16(w2_tiled))))
+    return SW_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launched(sw::launch_pack_experts(w13, w2, w13_tiled, w2_tiled, d->hidden, d->inter,
+                                          d->n_experts, as_stream(stream)));
 }
 
 size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
@@ -142,32 +179,36 @@ size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
 }
 
 sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
-                                 const uint16_t* w13, const int32_t* counts,
+                                 const uint16_t* w13, int32_t layout, const int32_t* counts,
                                  const int32_t* offsets, const int32_t* perm,
                                  const int32_t* active, const int32_t* n_active, void* workspace,
                                  size_t workspace_bytes, void* stream) {
   SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
                               workspace_bytes));
   if (n_tokens == 0) return SW_OK;
+  SW_TRY(check_layout(d, n_tokens, layout));
   if (!x || !w13) return SW_ERR_NULL;
   if (!aligned16(x) || !aligned16(w13)) return SW_ERR_ALIGN;
   (void)hipGetLastError();
-  return launched(sw::launch_gate_up(x, n_tokens, w13, counts, offsets, perm, active, n_active,
+  return launched(sw::launch_gate_up(x, n_tokens, w13, layout == SW_LAYOUT_TILED, counts, offsets,
+                                     perm, active, n_active,
                                      d->hidden, d->inter, d->n_experts, d->top_k, workspace,
                                      as_stream(stream)));
 }
 
 sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint16_t* w2,
-                              const int32_t* counts, const int32_t* offsets, const int32_t* perm,
-                              const int32_t* active, const int32_t* n_active, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+                              int32_t layout, const int32_t* counts, const int32_t* offsets,
+                              const int32_t* perm, const int32_t* active, const int32_t* n_active,
+                              void* workspace, size_t workspace_bytes, void* stream) {
   SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
                               workspace_bytes));
   if (n_tokens == 0) return SW_OK;
+  SW_TRY(check_layout(d, n_tokens, layout));
   if (!w2) return SW_ERR_NULL;
   if (!aligned16(w2)) return SW_ERR_ALIGN;
   (void)hipGetLastError();
-  return launched(sw::launch_down(n_tokens, w2, counts, offsets, perm, active, n_active,
+  return launched(sw::launch_down(n_tokens, w2, layout == SW_LAYOUT_TILED, counts, offsets, perm,
+                                  active, n_active,
                                   d->hidden, d->inter, d->n_experts, d->top_k, workspace,
                                   as_stream(stream)));
 }
@@ -189,23 +230,25 @@ sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const f
 }
 
 sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
-                         const uint16_t* w13, const uint16_t* w2, const float* topk_w,
-                         const int32_t* counts, const int32_t* offsets,
+                         const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                         const float* topk_w, const int32_t* counts, const int32_t* offsets,
                          const int32_t* perm, const int32_t* active, const int32_t* n_active,
                          float* out, void* workspace, size_t workspace_bytes, void* stream) {
   SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
                               workspace_bytes));
   if (n_tokens == 0) return SW_OK;
+  SW_TRY(check_layout(d, n_tokens, layout));
   if (!x || !w13 || !w2 || !topk_w || !out) return SW_ERR_NULL;
   if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) || !aligned4(topk_w))
     return SW_ERR_ALIGN;
   (void)hipGetLastError();
   const hipStream_t s = as_stream(stream);
   const int H = d->hidden, I = d->inter, m = d->n_experts, k = d->top_k;
-  SW_TRY(launched(sw::launch_gate_up(x, n_tokens, w13, counts, offsets, perm, active, n_active, H,
-                                     I, m, k, workspace, s)));
-  SW_TRY(launched(sw::launch_down(n_tokens, w2, counts, offsets, perm, active, n_active, H, I, m,
-                                  k, workspace, s)));
+  const bool tiled = layout == SW_LAYOUT_TILED;
+  SW_TRY(launched(sw::launch_gate_up(x, n_tokens, w13, tiled, counts, offsets, perm, active,
+                                     n_active, H, I, m, k, workspace, s)));
+  SW_TRY(launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active, H,
+                                  I, m, k, workspace, s)));
   return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, m, k, workspace, s));
 }
 

@@ -17,7 +17,7 @@ __global__ __launch_bounds__(kSelectThreads) void prune_select_kernel(
     const float* __restrict__ importance, int m, int n_keep, int32_t* __restrict__ kept,
     int32_t* __restrict__ remap, uint8_t* __restrict__ keep_mask) {
   __shared__ uint32_t key[kMaxPool];
-  __shared__ int scan_scratch[17];
+  __shared__ uint32_t scan_scratch[34];
   const int e = threadIdx.x;
   if (e < m) key[e] = f32_order_key(importance[e]);
   __syncthreads();
@@ -31,8 +31,8 @@ __global__ __launch_bounds__(kSelectThreads) void prune_select_kernel(
     }
     keep = rank < n_keep ? 1 : 0;
   }
-  int total;
-  const int pos = block_exclusive_scan(keep, scan_scratch, &total);
+  uint32_t pos, unused_p, total, unused_t;
+  block_exclusive_scan2((uint32_t)keep, 0u, scan_scratch, &pos, &unused_p, &total, &unused_t);
   if (e < m) {
     keep_mask[e] = static_cast<uint8_t>(keep);
     remap[e] = keep ? pos : -1;

@@ -29,16 +29,15 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(
     int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
     int* __restrict__ n_active) {
   __shared__ int cursor[kMaxPool];                        // running output position per expert
-  __shared__ int wave_base[kDispatchWaves][kMaxPool];     // per-chunk position of each wave's run
-  __shared__ uint8_t wave_cnt[kDispatchWaves][kMaxPool];  // per-chunk pairs of a wave per expert
-  __shared__ int scan_scratch[17];
+  __shared__ int wave_base[kDispatchWaves * kMaxPool];    // [wave][e]: this chunk's run start
+  __shared__ uint8_t wave_cnt[kDispatchWaves * kMaxPool]; // [wave][e]: this chunk's run length
+  __shared__ uint32_t scan_scratch[34];
   __shared__ int bad;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (tid == 0) bad = 0;
-  for (int e = tid; e < kMaxPool; e += kDispatchThreads) cursor[e] = 0;
-  for (int i = tid; i < kDispatchWaves * kMaxPool; i += kDispatchThreads)
-    (&wave_cnt[0][0])[i] = 0;
+  if (tid < m) cursor[tid] = 0;
+  for (int i = tid; i < kDispatchWaves * m; i += kDispatchThreads) wave_cnt[i] = 0;
   __syncthreads();
 
   // histogram (integer LDS atomics: order-independent) and id validation
@@ -62,21 +61,19 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(
   }
 
   // offsets = exclusive scan of counts; active = ascending compaction of
-  // the experts with a nonzero count
-  const int c = tid < m ? cursor[tid] : 0;
-  int total;
-  const int off = block_exclusive_scan(c, scan_scratch, &total);
-  int n_act;
-  const int apos = block_exclusive_scan(c > 0 ? 1 : 0, scan_scratch, &n_act);
+  // the experts with a nonzero count (one fused two-value block scan)
+  const uint32_t c = tid < m ? (uint32_t)cursor[tid] : 0u;
+  uint32_t off, apos, total, n_act;
+  block_exclusive_scan2(c, c > 0 ? 1u : 0u, scan_scratch, &off, &apos, &total, &n_act);
   if (tid < m) {
-    counts[tid] = c;
-    offsets[tid] = off;
-    cursor[tid] = off;
+    counts[tid] = (int)c;
+    offsets[tid] = (int)off;
+    cursor[tid] = (int)off;
     if (c > 0) active[apos] = tid;
   }
   if (tid == 0) {
-    offsets[m] = total;
-    *n_active = n_act;
+    offsets[m] = (int)total;
+    *n_active = (int)n_act;
   }
   __syncthreads();
 
@@ -92,19 +89,19 @@ __global__ __launch_bounds__(kDispatchThreads) void dispatch_kernel(
     const int e = valid ? ids[p] : 0;
     const uint64_t peers = match_peers(e, valid, nbits);
     const int rank = __popcll(peers & lt_mask);
-    if (valid && rank == 0) wave_cnt[wave][e] = static_cast<uint8_t>(__popcll(peers));
+    if (valid && rank == 0) wave_cnt[wave * m + e] = static_cast<uint8_t>(__popcll(peers));
     __syncthreads();
     if (tid < m) {
       int run = cursor[tid];
       for (int w = 0; w < kDispatchWaves; ++w) {
-        wave_base[w][tid] = run;
-        run += wave_cnt[w][tid];
-        wave_cnt[w][tid] = 0;
+        wave_base[w * m + tid] = run;
+        run += wave_cnt[w * m + tid];
+        wave_cnt[w * m + tid] = 0;
       }
       cursor[tid] = run;
     }
     __syncthreads();
-    if (valid) perm[wave_base[wave][e] + rank] = p;
+    if (valid) perm[wave_base[wave * m + e] + rank] = p;
   }
 }
 

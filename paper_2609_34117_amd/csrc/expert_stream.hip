@@ -1,0 +1,485 @@
+// Wave-streaming expert FFN kernels for gfx950: the decode fast path of the
+// MoE layer (Section 2.1: a decode step reads every distinct expert chosen
+// across the batch, so the step is bound by streaming expert weights).
+//
+// Design:
+//   - A persistent grid of one 8-wave block per compute unit.  The tiles of
+//     all active experts form one list; block b owns the contiguous,
+//     equal-sized range b*per .. (b+1)*per of it, which crosses at most a few
+//     expert boundaries ("segments").
+//   - Per segment, the block stages the expert's token activations (gate/up:
+//     x rows; down: h hi/lo rows) in LDS once, up to 32 tokens per pass.
+//   - Each wave then owns whole tiles (16 weight rows over the full K) and
+//     streams them as 8 KiB chunks through a three-deep register pipeline:
+//     the chunk two steps ahead is always in flight.  The B operand (tokens)
+//     comes from LDS, so waiting for activations never waits on weights, and
+//     there is no cross-wave reduction and no barrier inside a segment.
+//   - Every step issues the same memory operations (out-of-range offsets
+//     for missing chunks and for epilogue stores on non-final chunks), so
+//     the compiler's wait counts are exact and the pipeline never drains on
+//     a conservative wait.
+// Tiles:  gate_up: 8 gate rows + the 8 matching up rows; epilogue writes
+//         h = silu(g) * u as a bf16 hi/lo pair.
+//         down: 16 output rows of W2; epilogue writes y (fp32) per pair.
+#include "sw_device.h"
+#include "sw_launch.h"
+
+namespace sw {
+namespace {
+
+constexpr int kWv = 8;            // waves per block
+constexpr int kBlk = 64 * kWv;    // threads per block
+constexpr int kKC = 8;            // 32-wide K steps per streamed chunk
+constexpr int kNT = 32;           // tokens staged per pass
+constexpr int kNBk = kNT / 16;    // MFMA column blocks per pass
+constexpr int kPad = 8;           // bf16 elements of padding per staged row
+
+struct Segment {
+  int lo, hi;  // tile range [lo, hi) inside one expert
+  int a, e, cnt, base;
+  bool ok;
+};
+
+// Next segment of the block's tile range starting at tile `lo`.
+__device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const int* active,
+                                                const int* counts, const int* offsets, int m,
+                                                int n_pairs) {
+  Segment s;
+  s.lo = lo;
+  s.a = lo / tpe;
+  s.hi = min(r_hi, (s.a + 1) * tpe);
+  s.e = active[s.a];
+  s.ok = s.e >= 0 && s.e < m;
+  s.cnt = s.ok ? counts[s.e] : 0;
+  s.base = s.ok ? offsets[s.e] : 0;
+  s.ok = s.ok && s.cnt > 0 && s.base >= 0 && s.cnt <= n_pairs - s.base;
+  if (!s.ok) {
+    s.e = 0;
+    s.cnt = 0;
+    s.base = 0;
+  }
+  return s;
+}
+
+// Balanced contiguous tile range of this block.
+__device__ __forceinline__ void block_range(int total, int* r_lo, int* r_hi) {
+  const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
+  *r_lo = min(total, (int)blockIdx.x * per);
+  *r_hi = min(total, *r_lo + per);
+}
+
+// ---------------------------------------------------------------------------
+// gate/up + SwiGLU
+
+struct GuWave {
+  __amdgpu_buffer_rsrc_t w, hh, hl;
+  const uint16_t* xs;  // LDS activations [kNT][H + kPad]
+  int H, I, nsteps, cpt, lane, r, kg, wave;
+  int seg_lo, seg_hi, a, tpe, p0, cnt, nbn;
+};
+
+// Weight chunk q of this wave's tiles.  Row-major: lane (r, kg) reads 16 B
+// of weight row r at 64-byte K steps.  Tiled: the tile's fragments are
+// contiguous, so the wave reads 1 KiB per load (non-temporal: read once).
+template <bool kTiled>
+__device__ __forceinline__ void gu_issue(const GuWave& g, int q, int Q, u32x4 (&A)[kKC]) {
+  const int j = q / g.cpt, c = q - j * g.cpt;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const int ib = tile - g.a * g.tpe;
+  uint32_t row, stride;
+  if (kTiled) {
+    row = (uint32_t)ib * 32u * g.H + (uint32_t)g.lane * 16u;
+    stride = 1024u;
+  } else {
+    const int wrow = g.r < 8 ? ib * 8 + g.r : g.I + ib * 8 + (g.r - 8);
+    row = (uint32_t)wrow * g.H * 2u + g.kg * 16u;
+    stride = 64u;
+  }
+#pragma unroll
+  for (int s = 0; s < kKC; ++s) {
+    const int step = c * kKC + s;
+    const uint32_t off = (q < Q && step < g.nsteps) ? row + (uint32_t)step * stride : kOutOfRange;
+    A[s] = kTiled ? buf_ld128_stream(g.w, off) : buf_ld128(g.w, off);
+  }
+}
+
+__device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (&A)[kKC],
+                                           f32x4 (&acc)[kNBk]) {
+  const int j = q / g.cpt, c = q - j * g.cpt;
+  if (c == 0) {
+#pragma unroll
+    for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int nb = 0; nb < kNBk; ++nb) {
+    if (nb < g.nbn) {
+      const uint16_t* row = g.xs + (nb * 16 + g.r) * (g.H + kPad) + g.kg * 8;
+      u32x4 B[kKC];
+#pragma unroll
+      for (int s = 0; s < kKC; ++s) {
+        const int step = c * kKC + s;
+        const bool ok = step < g.nsteps;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(row + (ok ? step * 32 : 0));
+        B[s] = ok ? v : zero4();
+      }
+#pragma unroll
+      for (int s = 0; s < kKC; ++s) acc[nb] = mfma_16x16x32(A[s], B[s], acc[nb]);
+    }
+  }
+  // epilogue on the tile's last chunk: SwiGLU of the 8 (gate, up) row pairs
+  // for every token column; lanes 0-31 own the results
+  const bool last = c == g.cpt - 1;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const int ib = tile - g.a * g.tpe;
+#pragma unroll
+  for (int nb = 0; nb < kNBk; ++nb) {
+    uint32_t off = kOutOfRange;
+    u32x2 hw = {0u, 0u}, lw = {0u, 0u};
+    if (last && nb < g.nbn) {
+      const f32x4 v = acc[nb];
+      f32x4 u;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) u[i] = __shfl_xor(v[i], 32);
+      uint16_t hb[4], lb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float gt = v[i];
+        const float hv = (gt / (1.0f + expf(-gt))) * u[i];
+        hb[i] = f32_to_bf16(hv);
+        lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
+      }
+      hw = u32x2{(uint32_t)hb[0] | ((uint32_t)hb[1] << 16), (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
+      lw = u32x2{(uint32_t)lb[0] | ((uint32_t)lb[1] << 16), (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+      const int slot = g.p0 + nb * 16 + g.r;
+      if (g.lane < 32 && slot < g.cnt)
+        off = ((uint32_t)slot * g.I + (uint32_t)(ib * 8 + g.kg * 4)) * 2u;
+    }
+    __builtin_amdgcn_raw_buffer_store_b64(hw, g.hh, off, 0, 0);
+    __builtin_amdgcn_raw_buffer_store_b64(lw, g.hl, off, 0, 0);
+  }
+}
+
+template <bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
+    const int* __restrict__ counts, const int* __restrict__ offsets,
+    const int* __restrict__ perm, const int* __restrict__ active,
+    const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
+    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
+  __shared__ uint16_t xs[kNT * (kMaxStreamH + kPad)];
+  __shared__ int pid[kNT];
+  const int n_act = *n_active_p;
+  if (n_act <= 0 || n_act > m) return;
+  const int tpe = I / 8;
+  int r_lo, r_hi;
+  block_range(n_act * tpe, &r_lo, &r_hi);
+
+  GuWave g;
+  g.xs = xs;
+  g.H = H;
+  g.I = I;
+  g.nsteps = H / 32;
+  g.cpt = (g.nsteps + kKC - 1) / kKC;
+  g.lane = threadIdx.x & 63;
+  g.wave = threadIdx.x >> 6;
+  g.r = g.lane & 15;
+  g.kg = g.lane >> 4;
+  g.tpe = tpe;
+
+  for (int lo = r_lo; lo < r_hi;) {
+    const Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m, n_pairs);
+    lo = sg.hi;
+    g.seg_lo = sg.lo;
+    g.seg_hi = sg.hi;
+    g.a = sg.a;
+    g.cnt = sg.cnt;
+    g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
+    const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
+    g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
+    g.hl = make_rsrc(h_lo + (size_t)sg.base * I, hbytes);
+    // this wave's tiles of the segment: seg_lo + wave, + kWv, ...
+    const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
+    const int Q = ntw * g.cpt;
+    for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
+      // stage this pass's token rows of x in LDS
+      g.p0 = p0;
+      g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
+      __syncthreads();
+      if ((int)threadIdx.x < kNT) {
+        const int slot = p0 + threadIdx.x;
+        const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
+        pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+      }
+      __syncthreads();
+      const int row8 = H / 8;
+      for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
+        const int tok = idx / row8, c8 = idx - tok * row8;
+        const int p = pid[tok];
+        const u32x4 v = p >= 0 ? ld128(x + (size_t)(p / k) * H + c8 * 8) : zero4();
+        *reinterpret_cast<u32x4*>(xs + tok * (H + kPad) + c8 * 8) = v;
+      }
+      __syncthreads();
+
+      u32x4 A0[kKC], A1[kKC], A2[kKC];
+      f32x4 acc[kNBk];
+#pragma unroll
+      for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      gu_issue<kTiled>(g, 0, Q, A0);
+      gu_issue<kTiled>(g, 1, Q, A1);
+      for (int q = 0; q < Q; q += 3) {
+        gu_issue<kTiled>(g, q + 2, Q, A2);
+        gu_compute(g, q, A0, acc);
+        gu_issue<kTiled>(g, q + 3, Q, A0);
+        if (q + 1 < Q) gu_compute(g, q + 1, A1, acc);
+        gu_issue<kTiled>(g, q + 4, Q, A1);
+        if (q + 2 < Q) gu_compute(g, q + 2, A2, acc);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down projection
+
+struct DnWave {
+  __amdgpu_buffer_rsrc_t w, y;
+  const uint16_t* hs;  // LDS h hi rows [kNT][I + kPad], then the lo rows
+  const int* pid;      // LDS pair ids of the pass
+  int H, I, nsteps, cpt, lane, r, kg, wave;
+  int seg_lo, a, tpe, nbn;
+};
+
+template <bool kTiled>
+__device__ __forceinline__ void dn_issue(const DnWave& g, int q, int Q, u32x4 (&A)[kKC]) {
+  const int j = q / g.cpt, c = q - j * g.cpt;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const int ob = tile - g.a * g.tpe;
+  const int o = ob * 16 + g.r;
+  uint32_t row, stride;
+  if (kTiled) {
+    row = (uint32_t)ob * 32u * g.I + (uint32_t)g.lane * 16u;
+    stride = 1024u;
+  } else {
+    row = (uint32_t)o * g.I * 2u + g.kg * 16u;
+    stride = 64u;
+  }
+#pragma unroll
+  for (int s = 0; s < kKC; ++s) {
+    const int step = c * kKC + s;
+    const bool ok = q < Q && step < g.nsteps && o < g.H;
+    const uint32_t off = ok ? row + (uint32_t)step * stride : kOutOfRange;
+    A[s] = kTiled ? buf_ld128_stream(g.w, off) : buf_ld128(g.w, off);
+  }
+}
+
+__device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (&A)[kKC],
+                                           f32x4 (&acc)[kNBk]) {
+  const int j = q / g.cpt, c = q - j * g.cpt;
+  if (c == 0) {
+#pragma unroll
+    for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int lo_rows = kNT * (g.I + kPad);
+#pragma unroll
+  for (int nb = 0; nb < kNBk; ++nb) {
+    if (nb < g.nbn) {
+      const uint16_t* row = g.hs + (nb * 16 + g.r) * (g.I + kPad) + g.kg * 8;
+#pragma unroll
+      for (int s = 0; s < kKC; ++s) {
+        const int step = c * kKC + s;
+        const bool ok = step < g.nsteps;
+        const int col = ok ? step * 32 : 0;
+        const u32x4 bh = *reinterpret_cast<const u32x4*>(row + col);
+        const u32x4 bl = *reinterpret_cast<const u32x4*>(row + lo_rows + col);
+        acc[nb] = mfma_16x16x32(A[s], ok ? bh : zero4(), acc[nb]);
+        acc[nb] = mfma_16x16x32(A[s], ok ? bl : zero4(), acc[nb]);
+      }
+    }
+  }
+  const bool last = c == g.cpt - 1;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const int o = (tile - g.a * g.tpe) * 16 + g.kg * 4;
+#pragma unroll
+  for (int nb = 0; nb < kNBk; ++nb) {
+    uint32_t off = kOutOfRange;
+    if (last && nb < g.nbn) {
+      const int p = g.pid[nb * 16 + g.r];
+      if (p >= 0 && o < g.H) off = ((uint32_t)p * g.H + (uint32_t)o) * 4u;
+    }
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[nb]), g.y, off, 0, 0);
+  }
+}
+
+template <bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
+    const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
+    const uint16_t* __restrict__ w2, const int* __restrict__ counts,
+    const int* __restrict__ offsets, const int* __restrict__ perm,
+    const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
+    int H, int I, int m, int n_pairs) {
+  __shared__ uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
+  __shared__ int pid[kNT];
+  const int n_act = *n_active_p;
+  if (n_act <= 0 || n_act > m) return;
+  const int tpe = (H + 15) / 16;
+  int r_lo, r_hi;
+  block_range(n_act * tpe, &r_lo, &r_hi);
+
+  DnWave g;
+  g.hs = hs;
+  g.pid = pid;
+  g.y = make_rsrc(y, 4u * (uint32_t)n_pairs * (uint32_t)H);
+  g.H = H;
+  g.I = I;
+  g.nsteps = I / 32;
+  g.cpt = (g.nsteps + kKC - 1) / kKC;
+  g.lane = threadIdx.x & 63;
+  g.wave = threadIdx.x >> 6;
+  g.r = g.lane & 15;
+  g.kg = g.lane >> 4;
+  g.tpe = tpe;
+  const int lo_rows = kNT * (I + kPad);
+
+  for (int lo = r_lo; lo < r_hi;) {
+    const Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m, n_pairs);
+    lo = sg.hi;
+    g.seg_lo = sg.lo;
+    g.a = sg.a;
+    g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
+    const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
+    const int Q = ntw * g.cpt;
+    for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
+      g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
+      __syncthreads();
+      if ((int)threadIdx.x < kNT) {
+        const int slot = p0 + threadIdx.x;
+        const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
+        pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+      }
+      // h rows of the pass are contiguous in dispatch-slot order
+      const int row8 = I / 8;
+      for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
+        const int tok = idx / row8, c8 = idx - tok * row8;
+        const int slot = p0 + tok;
+        u32x4 vh = zero4(), vl = zero4();
+        if (slot < sg.cnt) {
+          const size_t off = (size_t)(sg.base + slot) * I + c8 * 8;
+          vh = ld128(h_hi + off);
+          vl = ld128(h_lo + off);
+        }
+        *reinterpret_cast<u32x4*>(hs + tok * (I + kPad) + c8 * 8) = vh;
+        *reinterpret_cast<u32x4*>(hs + lo_rows + tok * (I + kPad) + c8 * 8) = vl;
+      }
+      __syncthreads();
+
+      u32x4 A0[kKC], A1[kKC], A2[kKC];
+      f32x4 acc[kNBk];
+#pragma unroll
+      for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      dn_issue<kTiled>(g, 0, Q, A0);
+      dn_issue<kTiled>(g, 1, Q, A1);
+      for (int q = 0; q < Q; q += 3) {
+        dn_issue<kTiled>(g, q + 2, Q, A2);
+        dn_compute(g, q, A0, acc);
+        dn_issue<kTiled>(g, q + 3, Q, A0);
+        if (q + 1 < Q) dn_compute(g, q + 1, A1, acc);
+        dn_issue<kTiled>(g, q + 4, Q, A1);
+        if (q + 2 < Q) dn_compute(g, q + 2, A2, acc);
+      }
+    }
+  }
+}
+
+// Tiled ("fragment-major") expert layout.  Gate/up: tile ib of an expert
+// holds the 16 A rows (gate rows 8ib..8ib+7, then up rows I+8ib..) over all
+// of H as H/32 consecutive 1 KiB fragments; fragment s stores, for lane l =
+// 0..63, the 8 bf16 of row (l % 16), columns 32s + 8(l / 16) .. +7.  Down:
+// tile ob holds output rows 16ob..16ob+15 over I the same way.  One thread
+// moves one 16-byte fragment piece.
+__global__ __launch_bounds__(256) void pack_w13_kernel(const uint16_t* __restrict__ src,
+                                                      uint16_t* __restrict__ dst, int H, int I,
+                                                      size_t n_frag) {
+  const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (f >= n_frag) return;
+  const size_t per_e = (size_t)2 * I * H / 8, per_tile = (size_t)2 * H;
+  const size_t e = f / per_e, rem = f - e * per_e;
+  const int ib = (int)(rem / per_tile), rem2 = (int)(rem - (size_t)ib * per_tile);
+  const int s = rem2 >> 6, l = rem2 & 63;
+  const int rr = l & 15;
+  const int row = rr < 8 ? ib * 8 + rr : I + ib * 8 + (rr - 8);
+  const int col = s * 32 + (l >> 4) * 8;
+  *reinterpret_cast<u32x4*>(dst + f * 8) =
+      ld128(src + e * 2 * I * H + (size_t)row * H + col);
+}
+
+__global__ __launch_bounds__(256) void pack_w2_kernel(const uint16_t* __restrict__ src,
+                                                     uint16_t* __restrict__ dst, int H, int I,
+                                                     size_t n_frag) {
+  const size_t f = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (f >= n_frag) return;
+  const size_t per_e = (size_t)H * I / 8, per_tile = (size_t)2 * I;
+  const size_t e = f / per_e, rem = f - e * per_e;
+  const int ob = (int)(rem / per_tile), rem2 = (int)(rem - (size_t)ob * per_tile);
+  const int s = rem2 >> 6, l = rem2 & 63;
+  const int row = ob * 16 + (l & 15);
+  const int col = s * 32 + (l >> 4) * 8;
+  *reinterpret_cast<u32x4*>(dst + f * 8) = ld128(src + e * H * I + (size_t)row * I + col);
+}
+
+int stream_grid() {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  return cus;
+}
+
+}  // namespace
+
+bool wave_stream_supported(int T, int H, int I, int k) {
+  return H % 32 == 0 && I % 32 == 0 && H <= kMaxStreamH && I <= kMaxStreamI &&
+         4 * (int64_t)T * k * H < ((int64_t)1 << 31);
+}
+
+hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                               const int* counts, const int* offsets, const int* perm,
+                               const int* active, const int* n_active, int H, int I, int m, int k,
+                               uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+  if (tiled)
+    gate_up_wave_kernel<true><<<stream_grid(), kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
+  else
+    gate_up_wave_kernel<false><<<stream_grid(), kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* counts,
+                            const int* offsets, const int* perm, const int* active,
+                            const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
+                            const uint16_t* h_lo, float* y, hipStream_t stream) {
+  if (tiled)
+    down_wave_kernel<true><<<stream_grid(), kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
+  else
+    down_wave_kernel<false><<<stream_grid(), kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack_experts(const uint16_t* w13, const uint16_t* w2, uint16_t* w13_t,
+                               uint16_t* w2_t, int H, int I, int m, hipStream_t stream) {
+  if (w13 != nullptr) {
+    const size_t n = (size_t)m * 2 * I * H / 8;
+    pack_w13_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(w13, w13_t, H, I, n);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+  }
+  if (w2 != nullptr) {
+    const size_t n = (size_t)m * H * I / 8;
+    pack_w2_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(w2, w2_t, H, I, n);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sw

@@ -9,6 +9,7 @@ namespace sw {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
@@ -23,6 +24,31 @@ __device__ __forceinline__ u32x4 ld128(const uint16_t* p) {
 // mark it non-temporal and keep L2 for activations.
 __device__ __forceinline__ u32x4 ld128_stream(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+// Buffer resources: a 128-bit descriptor (base, byte size) with hardware
+// range checking.  A load whose byte offset lies outside the buffer returns
+// zeros and a store there is dropped, so per-lane predicates become an
+// out-of-range offset instead of a branch.
+constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9-family descriptor word 3
+constexpr int kGlc = 1, kNonTemporal = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRsrcWord3);
+}
+
+__device__ __forceinline__ u32x4 buf_ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+// Streaming variant for data read once per call (expert weights).
+__device__ __forceinline__ u32x4 buf_ld128_stream(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kNonTemporal);
+}
+
+__device__ __forceinline__ uint32_t buf_ld32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
 }
 
 // D = A(16x32) * B(32x16) + C on the bf16 matrix cores, fp32 accumulate.
@@ -64,6 +90,62 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// Wave-wide reductions with DPP lane moves: swaps within quads, mirrors
+// within 8- and 16-lane rows, then the row broadcasts of lanes 15 and 31;
+// lane 63 ends with the total, which is returned to every lane.  Each step
+// is one cross-lane ALU move, far cheaper than an LDS-crossbar shuffle.
+namespace dpp {
+constexpr int kXor1 = 0xb1;         // quad_perm [1,0,3,2]
+constexpr int kXor2 = 0x4e;         // quad_perm [2,3,0,1]
+constexpr int kHalfMirror = 0x141;  // row_half_mirror
+constexpr int kMirror = 0x140;      // row_mirror
+constexpr int kBcast15 = 0x142;     // row_bcast:15
+constexpr int kBcast31 = 0x143;     // row_bcast:31
+}  // namespace dpp
+
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t identity, uint32_t v) {
+  return __builtin_amdgcn_update_dpp(identity, v, CTRL, ROW_MASK, 0xf, false);
+}
+
+template <typename Op>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v, uint32_t identity, Op op) {
+  v = op(v, dpp_mov<dpp::kXor1>(identity, v));
+  v = op(v, dpp_mov<dpp::kXor2>(identity, v));
+  v = op(v, dpp_mov<dpp::kHalfMirror>(identity, v));
+  v = op(v, dpp_mov<dpp::kMirror>(identity, v));
+  v = op(v, dpp_mov<dpp::kBcast15, 0xa>(identity, v));
+  v = op(v, dpp_mov<dpp::kBcast31, 0xc>(identity, v));
+  return __builtin_amdgcn_readlane(v, 63);
+}
+
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  return wave_reduce_u32(v, 0u, [](uint32_t a, uint32_t b) { return a > b ? a : b; });
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) {
+  return wave_reduce_u32(v, 0xffffffffu, [](uint32_t a, uint32_t b) { return a < b ? a : b; });
+}
+
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  const uint32_t r = wave_reduce_u32(__float_as_uint(v), 0u, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+  });
+  return __uint_as_float(r);
+}
+
+// Inclusive prefix sum over the 64 lanes with DPP: Hillis-Steele shifts
+// inside each 16-lane row, then the row broadcasts carry row totals upward.
+__device__ __forceinline__ uint32_t wave_inclusive_scan_u32(uint32_t v) {
+  v += dpp_mov<0x111>(0u, v);  // row_shr:1
+  v += dpp_mov<0x112>(0u, v);  // row_shr:2
+  v += dpp_mov<0x114>(0u, v);  // row_shr:4
+  v += dpp_mov<0x118>(0u, v);  // row_shr:8
+  v += dpp_mov<dpp::kBcast15, 0xa>(0u, v);
+  v += dpp_mov<dpp::kBcast31, 0xc>(0u, v);
+  return v;
+}
+
 // Work-tile mapping for memory-streaming grids.  Blocks are dispatched
 // round-robin over the eight XCDs (block b runs on XCD b % 8); each XCD is
 // given one contiguous range of the `valid` tiles, so tiles that read the
@@ -75,34 +157,39 @@ __device__ __forceinline__ int xcd_tile(int bid, int valid) {
   return (j < per && tile < valid) ? tile : -1;
 }
 
-// Exclusive prefix sum over a block of blockDim.x (<= 1024) threads.
-// `scratch` holds >= 17 ints of LDS.  Returns the prefix of v and writes the
-// block total to *total.  Must be called by every thread of the block.
-__device__ __forceinline__ int block_exclusive_scan(int v, int* scratch, int* total) {
+// Exclusive prefix sums of two values over a block of blockDim.x (a
+// multiple of 64, <= 1024) threads.  `scratch` holds >= 34 uint32 of LDS.
+// Returns the prefixes in *pa / *pb and the block totals in *ta / *tb.
+// Must be called by every thread of the block.
+__device__ __forceinline__ void block_exclusive_scan2(uint32_t a, uint32_t b, uint32_t* scratch,
+                                                      uint32_t* pa, uint32_t* pb, uint32_t* ta,
+                                                      uint32_t* tb) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int nwaves = (blockDim.x + 63) >> 6;
-  int incl = v;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const int o = __shfl_up(incl, d);
-    if (lane >= d) incl += o;
+  const int nwaves = blockDim.x >> 6;
+  const uint32_t ia = wave_inclusive_scan_u32(a), ib = wave_inclusive_scan_u32(b);
+  if (lane == 63) {
+    scratch[wave] = ia;
+    scratch[16 + wave] = ib;
   }
-  if (lane == 63) scratch[wave] = incl;
   __syncthreads();
   if (threadIdx.x == 0) {
-    int run = 0;
+    uint32_t ra = 0, rb = 0;
     for (int w = 0; w < nwaves; ++w) {
-      const int c = scratch[w];
-      scratch[w] = run;
-      run += c;
+      const uint32_t ca = scratch[w], cb = scratch[16 + w];
+      scratch[w] = ra;
+      scratch[16 + w] = rb;
+      ra += ca;
+      rb += cb;
     }
-    scratch[16] = run;
+    scratch[32] = ra;
+    scratch[33] = rb;
   }
   __syncthreads();
-  const int excl = scratch[wave] + incl - v;
-  *total = scratch[16];
+  *pa = scratch[wave] + ia - a;
+  *pb = scratch[16 + wave] + ib - b;
+  *ta = scratch[32];
+  *tb = scratch[33];
   __syncthreads();
-  return excl;
 }
 
 }  // namespace sw

@@ -10,6 +10,11 @@ namespace sw {
 
 __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Largest H and I whose 32-token activation tiles fit the wave-streaming
+// kernels' LDS staging.
+constexpr int kMaxStreamH = 2048;
+constexpr int kMaxStreamI = 1024;
+
 size_t route_workspace_bytes(int T, int m);
 size_t forward_workspace_bytes(int T, int H, int I, int k);
 
@@ -27,13 +32,26 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
 hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts, int* offsets,
                            int* perm, int* active, int* n_active, hipStream_t stream);
 
-hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, const int* counts,
-                          const int* offsets, const int* perm, const int* active,
-                          const int* n_active, int H, int I, int m, int k, void* workspace,
-                          hipStream_t stream);
-hipError_t launch_down(int T, const uint16_t* w2, const int* counts, const int* offsets,
-                       const int* perm, const int* active, const int* n_active, int H, int I,
-                       int m, int k, void* workspace, hipStream_t stream);
+// `tiled`: weights in the fragment-major layout of sw_moe_pack_experts.
+hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                          const int* counts, const int* offsets, const int* perm,
+                          const int* active, const int* n_active, int H, int I, int m, int k,
+                          void* workspace, hipStream_t stream);
+hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
+                       const int* offsets, const int* perm, const int* active,
+                       const int* n_active, int H, int I, int m, int k, void* workspace,
+                       hipStream_t stream);
+bool wave_stream_supported(int T, int H, int I, int k);
+hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                               const int* counts, const int* offsets, const int* perm,
+                               const int* active, const int* n_active, int H, int I, int m, int k,
+                               uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
+hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* counts,
+                            const int* offsets, const int* perm, const int* active,
+                            const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
+                            const uint16_t* h_lo, float* y, hipStream_t stream);
+hipError_t launch_pack_experts(const uint16_t* w13, const uint16_t* w2, uint16_t* w13_t,
+                               uint16_t* w2_t, int H, int I, int m, hipStream_t stream);
 hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,
                           int I, int m, int k, void* workspace, hipStream_t stream);
 

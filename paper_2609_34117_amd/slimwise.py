@@ -43,9 +43,10 @@ def _load() -> ctypes.CDLL:
         "sw_moe_route": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_dispatch": ([D, P, I32, P, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
-        "sw_moe_forward": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
-        "sw_moe_forward_gate_up": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
-        "sw_moe_forward_down": ([D, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_pack_experts": ([D, P, P, P, P, P], ctypes.c_int),
+        "sw_moe_forward": ([D, P, I32, P, P, I32, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_gate_up": ([D, P, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_down": ([D, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -57,7 +58,8 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 1
+ABI_VERSION = 2
+ROW_MAJOR, TILED = 0, 1
 if LIB.sw_abi_version() != ABI_VERSION:
     raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
 
@@ -135,6 +137,26 @@ def sw_moe_prune_compact(importance: torch.Tensor, n_keep: int, top_k: int, *, h
     return dict(kept=kept, remap=remap, keep_mask=mask, w13=w13_c, w2=w2_c, wr=wr_c, bias=bias_c)
 
 
+def sw_moe_pack_experts(w13=None, w2=None, *, top_k: int = 1, stream=None):
+    """Re-lay expert pools out in the tiled (fragment-major) device layout.
+
+    Returns ``(w13_tiled, w2_tiled)`` (None where the input was None)."""
+    ref = w13 if w13 is not None else w2
+    if w13 is not None:
+        m, two_i, hidden = w13.shape
+        inter = two_i // 2
+    else:
+        m, hidden, inter = w2.shape
+    d = Dims(hidden, inter, m, min(top_k, m))
+    w13_t = torch.empty_like(w13) if w13 is not None else None
+    w2_t = torch.empty_like(w2) if w2 is not None else None
+    st = LIB.sw_moe_pack_experts(ctypes.byref(d), _ptr(w13, _BF16, "w13"), _ptr(w2, _BF16, "w2"),
+                                 _ptr(w13_t), _ptr(w2_t), _stream(stream))
+    _check(st, "sw_moe_pack_experts")
+    del ref
+    return w13_t, w2_t
+
+
 def sw_moe_route(x: torch.Tensor, wr: torch.Tensor, top_k: int, *, keep_mask=None, bias=None,
                  want_gap=True, out=None, ws=None, stream=None):
     """Section 3.1, Eq. 2: masked top-k and renormalised gates.
@@ -196,8 +218,11 @@ def _fwd_dims(x_or_t, w13_or_w2, top_k, which="w13"):
 
 
 def sw_moe_forward(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor, topk_w: torch.Tensor,
-                   plan: Plan, *, out=None, ws=None, stream=None) -> torch.Tensor:
-    """Expert SwiGLU FFNs of every routed pair and the gate-weighted combine."""
+                   plan: Plan, *, layout: int = ROW_MAJOR, out=None, ws=None,
+                   stream=None) -> torch.Tensor:
+    """Expert SwiGLU FFNs of every routed pair and the gate-weighted combine.
+
+    ``layout``: ROW_MAJOR or TILED (weights from sw_moe_pack_experts)."""
     t = x.shape[0]
     d = _fwd_dims(x, w13, topk_w.shape[1])
     if out is None:
@@ -205,7 +230,7 @@ def sw_moe_forward(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor, topk_w:
     if ws is None:
         ws = workspace(sw_moe_forward_workspace_bytes(d, t), x.device)
     st = LIB.sw_moe_forward(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
-                            _ptr(w2, _BF16, "w2"), _ptr(topk_w, (torch.float32,), "topk_w"),
+                            _ptr(w2, _BF16, "w2"), layout, _ptr(topk_w, (torch.float32,), "topk_w"),
                             _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
                             _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
                             _ptr(ws), ws.numel(), _stream(stream))
@@ -213,19 +238,21 @@ def sw_moe_forward(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor, topk_w:
     return out
 
 
-def sw_moe_forward_gate_up(x, w13, top_k, plan: Plan, ws, stream=None):
+def sw_moe_forward_gate_up(x, w13, top_k, plan: Plan, ws, *, layout: int = ROW_MAJOR, stream=None):
     t = x.shape[0]
     d = _fwd_dims(x, w13, top_k)
     st = LIB.sw_moe_forward_gate_up(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
+                                    layout,
                                     _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
                                     _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
                                     _stream(stream))
     _check(st, "sw_moe_forward_gate_up")
 
 
-def sw_moe_forward_down(n_tokens, w2, top_k, plan: Plan, ws, stream=None):
+def sw_moe_forward_down(n_tokens, w2, top_k, plan: Plan, ws, *, layout: int = ROW_MAJOR,
+                        stream=None):
     d = _fwd_dims(n_tokens, w2, top_k, which="w2")
-    st = LIB.sw_moe_forward_down(ctypes.byref(d), n_tokens, _ptr(w2, _BF16, "w2"),
+    st = LIB.sw_moe_forward_down(ctypes.byref(d), n_tokens, _ptr(w2, _BF16, "w2"), layout,
                                  _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
                                  _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
                                  _stream(stream))
@@ -241,9 +268,10 @@ def sw_moe_forward_combine(topk_w, hidden, inter, n_experts, plan: Plan, out, ws
     _check(st, "sw_moe_forward_combine")
 
 
-def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, stream=None) -> dict:
+def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, layout: int = ROW_MAJOR,
+              stream=None) -> dict:
     """Route, dispatch and forward of one layer (allocating convenience wrapper)."""
     ids, w, gap = sw_moe_route(x, wr, top_k, keep_mask=keep_mask, bias=bias, stream=stream)
     plan = sw_moe_dispatch(ids, wr.shape[0], stream=stream)
-    out = sw_moe_forward(x, w13, w2, w, plan, stream=stream)
+    out = sw_moe_forward(x, w13, w2, w, plan, layout=layout, stream=stream)
     return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)

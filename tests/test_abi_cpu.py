@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 1
+    assert lib.sw_abi_version() == 2
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -117,25 +117,39 @@ def test_prune_and_dispatch_validation(lib):
 def test_forward_validation(lib):
     P = ctypes.c_void_p
     f = lib.sw_moe_forward
-    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P,
-                  ctypes.c_size_t, P]
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P, P, P,
+                  P, P, ctypes.c_size_t, P]
     d = Dims(64, 32, 8, 2)
     q = lib.sw_moe_forward_workspace_bytes
     q.argtypes = [ctypes.POINTER(Dims), ctypes.c_int32]
     q.restype = ctypes.c_size_t
     need = q(ctypes.byref(d), 4)
-    args = dict(x=16, w13=16, w2=16, tw=16, c=16, o=16, p=16, a=16, na=16, out=16, ws=16)
+    args = dict(x=16, w13=16, w2=16, lay=0, tw=16, c=16, o=16, p=16, a=16, na=16, out=16, ws=16)
 
     def call(nbytes=need, **kw):
         a = dict(args, **kw)
-        return f(ctypes.byref(d), a["x"], 4, a["w13"], a["w2"], a["tw"], a["c"], a["o"], a["p"],
-                 a["a"], a["na"], a["out"], a["ws"], nbytes, None)
+        return f(ctypes.byref(d), a["x"], 4, a["w13"], a["w2"], a["lay"], a["tw"], a["c"], a["o"],
+                 a["p"], a["a"], a["na"], a["out"], a["ws"], nbytes, None)
 
     assert call(nbytes=need - 1) == SW_ERR_WORKSPACE
     assert call(w2=None) == SW_ERR_NULL
     assert call(na=None) == SW_ERR_NULL
     assert call(out=20) == SW_ERR_ALIGN
     assert call(ws=8) == SW_ERR_ALIGN
+    assert call(lay=2) == SW_ERR_SHAPE           # unknown layout
+    d.hidden, d.inter = 72, 40                   # tiled layout needs multiples of 32
+    need2 = q(ctypes.byref(d), 4)
+    assert call(nbytes=need2, lay=1) == SW_ERR_UNSUPPORTED
+
+
+def test_pack_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.sw_moe_pack_experts
+    f.argtypes = [ctypes.POINTER(Dims), P, P, P, P, P]
+    assert f(ctypes.byref(Dims(72, 32, 4, 2)), 16, 16, 16, 16, None) == SW_ERR_UNSUPPORTED
+    assert f(ctypes.byref(Dims(4096, 32, 4, 2)), 16, 16, 16, 16, None) == SW_ERR_UNSUPPORTED
+    assert f(ctypes.byref(Dims(64, 32, 4, 2)), 16, None, None, None, None) == SW_ERR_NULL
+    assert f(ctypes.byref(Dims(64, 32, 4, 2)), 16, None, 24, None, None) == SW_ERR_ALIGN
 
 
 def _prototypes():

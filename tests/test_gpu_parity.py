@@ -262,3 +262,95 @@ def test_dispatch_skewed_and_large(sw):
         np.testing.assert_array_equal(host(plan.perm)[: t * k], perm)
         assert int(host(plan.n_active)[0]) == n_active
         np.testing.assert_array_equal(host(plan.active)[:n_active], active)
+
+
+def test_exact_logit_ties_break_to_smaller_id(sw):
+    # identical router rows give bit-identical logits on both sides
+    cfg, L, D = small_layer(256, 40, 6, 32, 33, seed=2)
+    wr = L["wr"].copy()
+    for dup in (7, 19, 33):
+        wr[dup] = wr[3]
+    wr[39] = wr[0]
+    ids, w, gap = sw.sw_moe_route(D["x"], dev(wr), 6)
+    o_ids, o_w, o_gap = oracle.route(L["x"], wr, 6)
+    np.testing.assert_array_equal(host(ids), o_ids)
+    np.testing.assert_allclose(host(w), o_w, atol=1e-5)
+    for r in host(ids):
+        pos = {int(e): j for j, e in enumerate(r)}
+        if 3 in pos and 7 in pos:
+            assert pos[3] < pos[7]
+
+
+def test_dispatch_every_pair_on_one_expert(sw):
+    for t, k in [(300, 1), (64, 1), (2000, 1)]:
+        ids = np.full((t, k), 5, np.int32)
+        plan = sw.sw_moe_dispatch(dev(ids), 9)
+        counts, offsets, perm, active, n_active = oracle.dispatch(ids, 9)
+        np.testing.assert_array_equal(host(plan.counts), counts)
+        np.testing.assert_array_equal(host(plan.offsets), offsets)
+        np.testing.assert_array_equal(host(plan.perm)[: t * k], perm)
+        assert int(host(plan.n_active)[0]) == n_active == 1
+
+
+# --------------------------------------------------------------------------
+# tiled (fragment-major) weight layout
+
+def np_tile(rows16):
+    """[16, K] -> [K/32 * 64 * 8]: fragment s, lane l = 16*kg + row, 8 values."""
+    k = rows16.shape[1]
+    return rows16.reshape(16, k // 32, 4, 8).transpose(1, 2, 0, 3).reshape(-1)
+
+
+def np_tile_w13(w13):
+    m, two_i, h = w13.shape
+    inter = two_i // 2
+    out = []
+    for e in range(m):
+        for b in range(inter // 8):
+            rows = np.concatenate([w13[e, 8 * b:8 * b + 8], w13[e, inter + 8 * b:inter + 8 * b + 8]])
+            out.append(np_tile(rows))
+    return np.concatenate(out).reshape(w13.shape)
+
+
+def np_tile_w2(w2):
+    m, h, inter = w2.shape
+    return np.concatenate([np_tile(w2[e, 16 * b:16 * b + 16]) for e in range(m)
+                           for b in range(h // 16)]).reshape(w2.shape)
+
+
+@pytest.mark.parametrize("hidden,inter,m", [(64, 32, 3), (256, 128, 5), (2048, 96, 2)])
+def test_pack_matches_layout_definition(sw, hidden, inter, m):
+    cfg, L, D = small_layer(hidden, m, 1, inter, 1, seed=3)
+    t13, t2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    np.testing.assert_array_equal(host(t13), np_tile_w13(L["w13"]))
+    np.testing.assert_array_equal(host(t2), np_tile_w2(L["w2"]))
+
+
+@pytest.mark.parametrize("name,pruning,batch", [("tiny", 0.5, None), ("decode_b64", 0.0, None),
+                                                ("decode_b64", 0.5, None), ("decode_sweep", 0.5, 64),
+                                                ("decode_sweep", 0.0, 256), ("decode_sweep", 0.5, 1)])
+def test_tiled_forward_parity_and_bitwise_equal_to_row_major(sw, name, pruning, batch):
+    cfg, L, D = layer_inputs(name)
+    mask = mask_for(cfg, L, pruning)
+    x_np = L["x"] if batch is None else I.make_x(cfg, tokens=batch, rep=7)
+    x = dev(x_np)
+    t13, t2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    keep = None if mask is None else dev(mask)
+    rm = sw.moe_layer(x, D["wr"], D["w13"], D["w2"], cfg.top_k, keep_mask=keep)
+    tl = sw.moe_layer(x, D["wr"], t13, t2, cfg.top_k, keep_mask=keep, layout=sw.TILED)
+    assert torch.equal(rm["out"], tl["out"])
+    ids, w = host(tl["topk_ids"]), host(tl["topk_w"])
+    rows = np.unique(np.linspace(0, x_np.shape[0] - 1, min(x_np.shape[0], 8)).astype(int))
+    o_out = oracle.forward(np.ascontiguousarray(x_np[rows]), L["w13"], L["w2"],
+                           np.ascontiguousarray(ids[rows]), np.ascontiguousarray(w[rows]))
+    compare_out(host(tl["out"])[rows], o_out)
+
+
+def test_compacting_a_tiled_pool_equals_tiling_the_compacted_pool(sw):
+    cfg, L, D = layer_inputs("decode_b64")
+    n_keep = cfg.n_keep(0.5)
+    t13, t2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    a = sw.sw_moe_prune_compact(D["importance"], n_keep, cfg.top_k, w13=t13, w2=t2, wr=D["wr"])
+    b = sw.sw_moe_prune_compact(D["importance"], n_keep, cfg.top_k, w13=D["w13"], w2=D["w2"], wr=D["wr"])
+    bt13, bt2 = sw.sw_moe_pack_experts(b["w13"], b["w2"])
+    assert torch.equal(a["w13"], bt13) and torch.equal(a["w2"], bt2)
