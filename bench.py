@@ -13,12 +13,18 @@ Infinity Cache cannot serve expert bytes from one step to the next.
 
 Prints one JSON line.  `roofline` describes the dominant kernel (gate_up,
 which streams 2/3 of each active expert's bytes): algorithmic bytes per
-launch over its mean duration measured with HIP events on the launch stream.
-`cpu_baseline` is the single-threaded C oracle timed on a bounded sample.
+launch (the unique expert bytes n_active * 2 * I * H * 2) over its mean
+launch duration, measured with HIP events around back-to-back launches on the
+launch stream.  `traffic` is the HBM byte count of one such launch from the
+FETCH_SIZE / WRITE_SIZE hardware counters, scaled by what those counters read
+for plain device copies of known size; it is reported only while the kernel
+sources hash to the ones the counters were taken on.  `cpu_baseline` is the
+single-threaded C oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -36,6 +42,20 @@ METRIC = "MoE decode-layer tokens/s + achieved HBM GB/s, batch 64, 0% vs 50% pru
 HBM_PEAK_GBS = 8000.0
 N_X = 16
 N_COPIES = 4
+
+# HBM traffic of one gate_up launch on the default workload (batch 64, 50%
+# pruned, tiled pool), from two rocprofv3 --pmc passes of
+# `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197772.3 KiB x
+# 1.99984 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
+# of 192-768 MiB) + WRITE_SIZE 1570.8 KiB x 1.0 (WRITE_SIZE of the copies is
+# exact).
+KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
+                  "paper_2609_34117_amd/csrc/sw_device.h",
+                  "paper_2609_34117_amd/csrc/sw_launch.h")
+GATE_UP_TRAFFIC = dict(sources_sha256="51344da6e89b309d875556ae8f6083dcbf626c1e34c7be99e651febb59c55164",
+                       workload=("decode_b64", 64, 0.5, "tiled"),
+                       bytes_per_launch=int(round((197772.3 * 1.99984 + 1570.8) * 1024)))
 
 
 def parse():
@@ -78,6 +98,15 @@ class Runner:
         d = sw.dims(H, Iw, pool.m, k)
         self.rws = sw.workspace(sw.sw_moe_route_workspace_bytes(d, T), dev)
         self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(d, T), dev)
+
+    def plan_for(self, x):
+        """A dispatch plan of its own for batch `x` (route + dispatch)."""
+        sw, p = self.sw, self.pool
+        plan = sw.alloc_plan(self.T, p.m, self.cfg.top_k, x.device)
+        sw.sw_moe_route(x, p.wr, self.cfg.top_k, bias=p.bias, out=(self.ids, self.w, self.gap),
+                        ws=self.rws)
+        sw.sw_moe_dispatch(self.ids, p.m, plan=plan)
+        return plan
 
     def step(self, x, c, ev=None):
         sw, p = self.sw, self.pool
@@ -122,7 +151,45 @@ def time_runner(torch, r: Runner, xs, steps, warmup):
         r.step(xs[j], 0)
         n_act.append(int(r.plan.n_active.item()))
     n_act_steps = np.array([n_act[s % N_X] for s in range(steps)], float)
-    return t_step, phase, n_act_steps, n_act
+    kern = time_kernels(torch, r, xs, steps)
+    return t_step, phase, n_act_steps, n_act, kern
+
+
+def time_kernels(torch, r: Runner, xs, steps):
+    """Mean launch duration of gate_up and of down: `steps` launches of one
+    kernel back to back between two HIP events on the launch stream, rotating
+    the batches (each with its own plan) and the pool copies."""
+    sw, p, k = r.sw, r.pool, r.cfg.top_k
+    plans = [r.plan_for(x) for x in xs]
+    torch.cuda.synchronize()
+    out = {}
+    for name in ("gate_up", "down"):
+        for s in range(4):
+            j, c = s % N_X, s % N_COPIES
+            if name == "gate_up":
+                sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
+            else:
+                sw.sw_moe_forward_down(r.T, p.w2[c], k, plans[j], r.fws, layout=p.layout)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for s in range(steps):
+            j, c = s % N_X, s % N_COPIES
+            if name == "gate_up":
+                sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
+            else:
+                sw.sw_moe_forward_down(r.T, p.w2[c], k, plans[j], r.fws, layout=p.layout)
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = e0.elapsed_time(e1) / 1e3 / steps
+    return out
+
+
+def sources_sha256():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def cpu_baseline(cfg, L, pruning, seconds):
@@ -189,15 +256,17 @@ def main():
     gate_up_bytes = 2 * H * Iw * 2
 
     def summary(name):
-        t_step, phase, nact_steps, nact = res[name]
+        t_step, phase, nact_steps, nact, kern = res[name]
         t_gu, t_dn, t_cb = phase.mean(axis=0)
         fwd = phase.sum(axis=1)
         U = nact_steps * expert_bytes
+        n_mean = float(nact_steps.mean())
         return dict(t_step_us=t_step * 1e6, tokens_per_s=T / t_step,
                     t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
-                    n_active_mean=float(nact_steps.mean()),
-                    gate_up_GBps=float((nact_steps * gate_up_bytes).sum() / phase[:, 0].sum() / 1e9),
-                    down_GBps=float((nact_steps * H * Iw * 2).sum() / phase[:, 1].sum() / 1e9),
+                    n_active_mean=n_mean,
+                    gate_up_launch_us=kern["gate_up"] * 1e6, down_launch_us=kern["down"] * 1e6,
+                    gate_up_GBps=n_mean * gate_up_bytes / kern["gate_up"] / 1e9,
+                    down_GBps=n_mean * H * Iw * 2 / kern["down"] / 1e9,
                     fwd_GBps=float(U.sum() / fwd.sum() / 1e9),
                     layer_GBps=float(U.mean() / t_step / 1e9),
                     eq1_expected=float(pools[name] * (1 - (1 - cfg.top_k / pools[name]) ** T)))
@@ -205,6 +274,11 @@ def main():
     pools = {"pruned": n_keep, "full": cfg.n_experts}
     sp, sf = summary("pruned"), summary("full")
     achieved = sp["gate_up_GBps"]
+    algo_bytes = sp["n_active_mean"] * gate_up_bytes
+    traffic = None
+    if (GATE_UP_TRAFFIC["sources_sha256"] == sources_sha256()
+            and GATE_UP_TRAFFIC["workload"] == (cfg.name, T, args.pruning, args.layout)):
+        traffic = GATE_UP_TRAFFIC["bytes_per_launch"]
     line = {
         "metric": METRIC,
         "value": round(sp["tokens_per_s"], 1),
@@ -226,9 +300,11 @@ def main():
             "parallelism": "none (1 GPU)",
         },
         "roofline": {
-            "bound": "hbm", "kernel": "gate_up_kernel",
+            "bound": "hbm", "kernel": "gate_up_wave_kernel",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "traffic_unit": "bytes/launch", "algorithmic_bytes_per_launch": int(round(algo_bytes)),
+            "launch_us": round(sp["gate_up_launch_us"], 3),
         },
         "detail": {
             "pruned": {k: round(v, 3) for k, v in sp.items()},
