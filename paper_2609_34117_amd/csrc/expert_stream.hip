@@ -10,10 +10,12 @@
 //   - Per segment, the block stages the expert's token activations (gate/up:
 //     x rows; down: h hi/lo rows) in LDS once, up to 32 tokens per pass.
 //   - Each wave then owns whole tiles (16 weight rows over the full K) and
-//     streams them as 8 KiB chunks through a three-deep register pipeline:
-//     the chunk two steps ahead is always in flight.  The B operand (tokens)
-//     comes from LDS, so waiting for activations never waits on weights, and
-//     there is no cross-wave reduction and no barrier inside a segment.
+//     streams them as 8 KiB chunks through a kDepth-deep register pipeline:
+//     the kDepth - 1 chunks ahead are always in flight.  The B operand
+//     (tokens) comes from LDS, so waiting for activations never waits on
+//     weights, and there is no cross-wave reduction and no barrier inside a
+//     segment.  The first chunks of a segment are issued as soon as its
+//     expert id is known, before the activation staging and its barriers.
 //   - Every step issues the same memory operations (out-of-range offsets
 //     for missing chunks and for epilogue stores on non-final chunks), so
 //     the compiler's wait counts are exact and the pipeline never drains on
@@ -33,32 +35,38 @@ constexpr int kKC = 8;            // 32-wide K steps per streamed chunk
 constexpr int kNT = 32;           // tokens staged per pass
 constexpr int kNBk = kNT / 16;    // MFMA column blocks per pass
 constexpr int kPad = 8;           // bf16 elements of padding per staged row
+constexpr int kDepth = 3;         // streamed chunks held in registers per wave
 
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
-  bool ok;
+  bool e_ok;   // expert id in range: its weights may be read
 };
 
-// Next segment of the block's tile range starting at tile `lo`.
+// Next segment of the block's tile range starting at tile `lo`.  The loads
+// of the expert's count and offset are issued here but consumed only by
+// finish_segment, so the first weight chunks can go out in between.
 __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const int* active,
-                                                const int* counts, const int* offsets, int m,
-                                                int n_pairs) {
+                                                const int* counts, const int* offsets, int m) {
   Segment s;
   s.lo = lo;
   s.a = lo / tpe;
   s.hi = min(r_hi, (s.a + 1) * tpe);
-  s.e = active[s.a];
-  s.ok = s.e >= 0 && s.e < m;
-  s.cnt = s.ok ? counts[s.e] : 0;
-  s.base = s.ok ? offsets[s.e] : 0;
-  s.ok = s.ok && s.cnt > 0 && s.base >= 0 && s.cnt <= n_pairs - s.base;
-  if (!s.ok) {
-    s.e = 0;
+  const int e = active[s.a];
+  s.e_ok = e >= 0 && e < m;
+  s.e = s.e_ok ? e : 0;
+  s.cnt = counts[s.e];
+  s.base = offsets[s.e];
+  return s;
+}
+
+// A segment whose pair range is not inside [0, n_pairs) has no tokens.
+__device__ __forceinline__ void finish_segment(Segment& s, int n_pairs) {
+  const bool ok = s.e_ok && s.cnt > 0 && s.base >= 0 && s.cnt <= n_pairs - s.base;
+  if (!ok) {
     s.cnt = 0;
     s.base = 0;
   }
-  return s;
 }
 
 // Balanced contiguous tile range of this block.
@@ -187,20 +195,28 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   g.tpe = tpe;
 
   for (int lo = r_lo; lo < r_hi;) {
-    const Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m, n_pairs);
+    Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m);
     lo = sg.hi;
     g.seg_lo = sg.lo;
     g.seg_hi = sg.hi;
     g.a = sg.a;
-    g.cnt = sg.cnt;
-    g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
-    const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
-    g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
-    g.hl = make_rsrc(h_lo + (size_t)sg.base * I, hbytes);
+    g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.e_ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
     // this wave's tiles of the segment: seg_lo + wave, + kWv, ...
     const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
     const int Q = ntw * g.cpt;
+    u32x4 A[kDepth][kKC];
+#pragma unroll
+    for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
+    finish_segment(sg, n_pairs);
+    g.cnt = sg.cnt;
+    const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
+    g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
+    g.hl = make_rsrc(h_lo + (size_t)sg.base * I, hbytes);
     for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
+      if (p0 > 0) {
+#pragma unroll
+        for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
+      }
       // stage this pass's token rows of x in LDS
       g.p0 = p0;
       g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
@@ -220,19 +236,17 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
       }
       __syncthreads();
 
-      u32x4 A0[kKC], A1[kKC], A2[kKC];
       f32x4 acc[kNBk];
 #pragma unroll
       for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      gu_issue<kTiled>(g, 0, Q, A0);
-      gu_issue<kTiled>(g, 1, Q, A1);
-      for (int q = 0; q < Q; q += 3) {
-        gu_issue<kTiled>(g, q + 2, Q, A2);
-        gu_compute(g, q, A0, acc);
-        gu_issue<kTiled>(g, q + 3, Q, A0);
-        if (q + 1 < Q) gu_compute(g, q + 1, A1, acc);
-        gu_issue<kTiled>(g, q + 4, Q, A1);
-        if (q + 2 < Q) gu_compute(g, q + 2, A2, acc);
+      // chunk q lives in A[q % kDepth]; the issue for q + kDepth - 1 goes
+      // out before the compute of q
+      for (int q = 0; q < Q; q += kDepth) {
+#pragma unroll
+        for (int d = 0; d < kDepth; ++d) {
+          gu_issue<kTiled>(g, q + d + kDepth - 1, Q, A[(d + kDepth - 1) % kDepth]);
+          if (d == 0 || q + d < Q) gu_compute(g, q + d, A[d], acc);
+        }
       }
     }
   }
@@ -341,14 +355,22 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   const int lo_rows = kNT * (I + kPad);
 
   for (int lo = r_lo; lo < r_hi;) {
-    const Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m, n_pairs);
+    Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m);
     lo = sg.hi;
     g.seg_lo = sg.lo;
     g.a = sg.a;
-    g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
+    g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.e_ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
     const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
     const int Q = ntw * g.cpt;
+    u32x4 A[kDepth][kKC];
+#pragma unroll
+    for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
+    finish_segment(sg, n_pairs);
     for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
+      if (p0 > 0) {
+#pragma unroll
+        for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
+      }
       g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
       __syncthreads();
       if ((int)threadIdx.x < kNT) {
@@ -372,19 +394,15 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
       }
       __syncthreads();
 
-      u32x4 A0[kKC], A1[kKC], A2[kKC];
       f32x4 acc[kNBk];
 #pragma unroll
       for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      dn_issue<kTiled>(g, 0, Q, A0);
-      dn_issue<kTiled>(g, 1, Q, A1);
-      for (int q = 0; q < Q; q += 3) {
-        dn_issue<kTiled>(g, q + 2, Q, A2);
-        dn_compute(g, q, A0, acc);
-        dn_issue<kTiled>(g, q + 3, Q, A0);
-        if (q + 1 < Q) dn_compute(g, q + 1, A1, acc);
-        dn_issue<kTiled>(g, q + 4, Q, A1);
-        if (q + 2 < Q) dn_compute(g, q + 2, A2, acc);
+      for (int q = 0; q < Q; q += kDepth) {
+#pragma unroll
+        for (int d = 0; d < kDepth; ++d) {
+          dn_issue<kTiled>(g, q + d + kDepth - 1, Q, A[(d + kDepth - 1) % kDepth]);
+          if (d == 0 || q + d < Q) dn_compute(g, q + d, A[d], acc);
+        }
       }
     }
   }
