@@ -3,9 +3,9 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode_b64]
 
-One step = one pass of the whole decode layer over one batch of synthetic
-tokens, with every input already resident in HBM.  The default workload is
-the batch-64 decode layer (H 2048, 128 experts, top-8, I 768) with a 50%
+One step = one pass of the whole decode layer (route + dispatch in one call,
+then gate_up, down, combine) over one batch of synthetic tokens, with every
+input already resident in HBM.  The default workload is the batch-64 decode layer (H 2048, 128 experts, top-8, I 768) with a 50%
 pruned decoder (64 kept experts, compacted pool); the unpruned pool is timed
 in the same run for the speedup.  Batches rotate over 16 pre-generated token
 sets and the pool over 4 copies at distinct addresses, so the 256 MB
@@ -46,16 +46,16 @@ N_COPIES = 4
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
 # `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
-# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197772.3 KiB x
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197790.6 KiB x
 # 1.99984 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
-# of 192-768 MiB) + WRITE_SIZE 1570.8 KiB x 1.0 (WRITE_SIZE of the copies is
+# of 192-768 MiB) + WRITE_SIZE 1569.4 KiB x 1.0 (WRITE_SIZE of the copies is
 # exact).
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h",
                   "paper_2609_34117_amd/csrc/sw_launch.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="51344da6e89b309d875556ae8f6083dcbf626c1e34c7be99e651febb59c55164",
+GATE_UP_TRAFFIC = dict(sources_sha256="ae6a55f70cdea8345d6f87ca691d0a4a0bad63d18a15e006df7957172f2a15f5",
                        workload=("decode_b64", 64, 0.5, "tiled"),
-                       bytes_per_launch=int(round((197772.3 * 1.99984 + 1570.8) * 1024)))
+                       bytes_per_launch=int(round((197790.6 * 1.99984 + 1569.4) * 1024)))
 
 
 def parse():
@@ -103,16 +103,14 @@ class Runner:
         """A dispatch plan of its own for batch `x` (route + dispatch)."""
         sw, p = self.sw, self.pool
         plan = sw.alloc_plan(self.T, p.m, self.cfg.top_k, x.device)
-        sw.sw_moe_route(x, p.wr, self.cfg.top_k, bias=p.bias, out=(self.ids, self.w, self.gap),
-                        ws=self.rws)
-        sw.sw_moe_dispatch(self.ids, p.m, plan=plan)
+        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias,
+                                 out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
         return plan
 
     def step(self, x, c, ev=None):
         sw, p = self.sw, self.pool
-        sw.sw_moe_route(x, p.wr, self.cfg.top_k, bias=p.bias, out=(self.ids, self.w, self.gap),
-                        ws=self.rws)
-        sw.sw_moe_dispatch(self.ids, p.m, plan=self.plan)
+        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias,
+                                 out=(self.ids, self.w, self.gap), plan=self.plan, ws=self.rws)
         if ev is None:
             sw.sw_moe_forward(x, p.w13[c], p.w2[c], self.w, self.plan, layout=p.layout,
                               out=self.out, ws=self.fws)
@@ -158,7 +156,9 @@ def time_runner(torch, r: Runner, xs, steps, warmup):
 def time_kernels(torch, r: Runner, xs, steps):
     """Mean launch duration of gate_up and of down: `steps` launches of one
     kernel back to back between two HIP events on the launch stream, rotating
-    the batches (each with its own plan) and the pool copies."""
+    the batches (each with its own plan) and the pool copies.  (The small
+    kernels are shorter than a host call, so their durations come from the
+    kernel trace instead.)"""
     sw, p, k = r.sw, r.pool, r.cfg.top_k
     plans = [r.plan_for(x) for x in xs]
     torch.cuda.synchronize()

@@ -74,7 +74,7 @@ typedef struct {
 const char* sw_status_str(int status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 2
+#define SW_ABI_VERSION 3
 int32_t sw_abi_version(void);
 
 /*
@@ -148,6 +148,22 @@ sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
 sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t n_tokens,
                           int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* active,
                           int32_t* n_active, void* stream);
+
+/*
+ * Route, then dispatch, in one call (Section 3.1, Eq. 2; Section 2.1, Eq. 1):
+ * every output is bit for bit what sw_moe_route followed by sw_moe_dispatch
+ * of its topk_ids would write, with the same arguments, workspace
+ * (sw_moe_route_workspace_bytes) and in-band errors.  For decode-sized
+ * batches (m <= 256, k <= 16, T*k <= 4096) the selection and the dispatch
+ * plan are built by one block, which saves two kernel launches per step.
+ * T = 0 writes the empty plan (counts and offsets 0, *n_active = 0).
+ */
+sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                const float* wr, const float* bias, const uint8_t* keep_mask,
+                                int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                                int32_t* offsets, int32_t* perm, int32_t* active,
+                                int32_t* n_active, void* workspace, size_t workspace_bytes,
+                                void* stream);
 
 /*
  * Re-lay an expert pool out for streaming (offline, once per pool; a device

@@ -137,7 +137,7 @@ sw_status sw_moe_pack_experts(const sw_moe_dims* d, const uint16_t* w13, const u
 
 size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
   if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
-  return sw::route_workspace_bytes(n_tokens, d->n_experts);
+  return sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts);
 }
 
 sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
@@ -151,7 +151,8 @@ sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
   if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
       !aligned4(topk_w) || (gap && !aligned4(gap)) || (bias && !aligned4(bias)))
     return SW_ERR_ALIGN;
-  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->n_experts)) return SW_ERR_WORKSPACE;
+  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts))
+    return SW_ERR_WORKSPACE;
   (void)hipGetLastError();
   return launched(sw::launch_route(x, n_tokens, wr, bias, keep_mask, d->hidden, d->n_experts,
                                    d->top_k, topk_ids, topk_w, gap, workspace,
@@ -171,6 +172,36 @@ sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t
   (void)hipGetLastError();
   return launched(sw::launch_dispatch(topk_ids, n_tokens * d->top_k, d->n_experts, counts,
                                       offsets, perm, active, n_active, as_stream(stream)));
+}
+
+sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                const float* wr, const float* bias, const uint8_t* keep_mask,
+                                int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                                int32_t* offsets, int32_t* perm, int32_t* active,
+                                int32_t* n_active, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(active) || !aligned4(n_active))
+    return SW_ERR_ALIGN;
+  if (n_tokens == 0) {
+    (void)hipGetLastError();
+    return launched(sw::launch_dispatch(nullptr, 0, d->n_experts, counts, offsets, nullptr,
+                                        active, n_active, as_stream(stream)));
+  }
+  if (!x || !wr || !topk_ids || !topk_w || !perm || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
+      !aligned4(topk_w) || !aligned4(perm) || (gap && !aligned4(gap)) ||
+      (bias && !aligned4(bias)))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, d->hidden,
+                                            d->n_experts, d->top_k, topk_ids, topk_w, gap, counts,
+                                            offsets, perm, active, n_active, workspace,
+                                            as_stream(stream)));
 }
 
 size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {

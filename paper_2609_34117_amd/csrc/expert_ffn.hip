@@ -39,7 +39,11 @@ __host__ __device__ inline size_t h_bytes(int n_pairs, int I) {
   return align_up((size_t)n_pairs * I * sizeof(uint16_t), 256);
 }
 
-__host__ __device__ inline ForwardWs carve(void* ws, int n_pairs, int I) {
+__host__ __device__ inline size_t y_bytes(int n_pairs, int H) {
+  return align_up((size_t)n_pairs * H * sizeof(float), 256);
+}
+
+__host__ __device__ inline ForwardWs carve(void* ws, int n_pairs, int H, int I) {
   char* p = static_cast<char*>(ws);
   ForwardWs w;
   w.h_hi = reinterpret_cast<uint16_t*>(p);
@@ -735,34 +739,35 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
   const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (size_t)T * hq) return;
   const int t = (int)(idx / hq), c = (int)(idx - (size_t)t * hq);
+  // the n_active load and the y / gate loads go out together; an invalid
+  // plan (n_active outside [0, m]) turns the result into NaN afterwards
   const int na = *n_active_p;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  const float* yt = y + (size_t)t * k * H + 4 * c;
+  const float* wt = topk_w + (size_t)t * k;
+  for (int j0 = 0; j0 < k; j0 += 8) {
+    float4 v[8];
+    float w[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (j0 + q < k) {
+        v[q] = *reinterpret_cast<const float4*>(yt + (size_t)(j0 + q) * H);
+        w[q] = wt[j0 + q];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      if (j0 + q < k) {
+        acc.x = fmaf(w[q], v[q].x, acc.x);
+        acc.y = fmaf(w[q], v[q].y, acc.y);
+        acc.z = fmaf(w[q], v[q].z, acc.z);
+        acc.w = fmaf(w[q], v[q].w, acc.w);
+      }
+    }
+  }
   if (na < 0 || na > m) {
     const float nan = __builtin_nanf("");
     acc = make_float4(nan, nan, nan, nan);
-  } else {
-    const float* yt = y + (size_t)t * k * H + 4 * c;
-    const float* wt = topk_w + (size_t)t * k;
-    for (int j0 = 0; j0 < k; j0 += 8) {
-      float4 v[8];
-      float w[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (j0 + q < k) {
-          v[q] = *reinterpret_cast<const float4*>(yt + (size_t)(j0 + q) * H);
-          w[q] = wt[j0 + q];
-        }
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        if (j0 + q < k) {
-          acc.x = fmaf(w[q], v[q].x, acc.x);
-          acc.y = fmaf(w[q], v[q].y, acc.y);
-          acc.z = fmaf(w[q], v[q].z, acc.z);
-          acc.w = fmaf(w[q], v[q].w, acc.w);
-        }
-      }
-    }
   }
   *reinterpret_cast<float4*>(out + (size_t)t * H + 4 * c) = acc;
 }
@@ -774,7 +779,7 @@ int round8(long v) { return (int)align_up((size_t)v, 8); }
 size_t forward_workspace_bytes(int T, int H, int I, int k) {
   if (T <= 0) return 0;
   const int n_pairs = T * k;
-  return 2 * h_bytes(n_pairs, I) + align_up((size_t)n_pairs * H * sizeof(float), 256);
+  return 2 * h_bytes(n_pairs, I) + y_bytes(n_pairs, H);
 }
 
 // Persistent grid: `per_cu` resident blocks on every compute unit, a
@@ -792,7 +797,7 @@ hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool ti
                           const int* active, const int* n_active, int H, int I, int m, int k,
                           void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  const ForwardWs ws = carve(workspace, T * k, I);
+  const ForwardWs ws = carve(workspace, T * k, H, I);
   // the tiled layout is only produced for shapes the wave kernels take
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_gate_up_wave(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m,
@@ -833,7 +838,7 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        const int* n_active, int H, int I, int m, int k, void* workspace,
                        hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  const ForwardWs ws = carve(workspace, T * k, I);
+  const ForwardWs ws = carve(workspace, T * k, H, I);
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_down_wave(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                             ws.h_hi, ws.h_lo, ws.y, stream);
@@ -856,7 +861,7 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
 hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,
                           int I, int m, int k, void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  const ForwardWs ws = carve(workspace, T * k, I);
+  const ForwardWs ws = carve(workspace, T * k, H, I);
   const size_t threads = (size_t)T * (H / 4);
   const unsigned blocks = (unsigned)((threads + 255) / 256);
   combine_kernel<<<blocks, 256, 0, stream>>>(ws.y, topk_w, n_active, out, T, H, k, m);

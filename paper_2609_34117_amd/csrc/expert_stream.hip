@@ -43,16 +43,19 @@ struct Segment {
   bool e_ok;   // expert id in range: its weights may be read
 };
 
-// Next segment of the block's tile range starting at tile `lo`.  The loads
-// of the expert's count and offset are issued here but consumed only by
+// Next segment of the block's tile range starting at tile `lo`.  With
+// `all_active` (n_active == m) the active list is the identity, so the
+// expert is the slot itself and active[] is not read.  The loads of the
+// expert's count and offset are issued here but consumed only by
 // finish_segment, so the first weight chunks can go out in between.
 __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const int* active,
-                                                const int* counts, const int* offsets, int m) {
+                                                const int* counts, const int* offsets, int m,
+                                                bool all_active) {
   Segment s;
   s.lo = lo;
   s.a = lo / tpe;
   s.hi = min(r_hi, (s.a + 1) * tpe);
-  const int e = active[s.a];
+  const int e = all_active ? s.a : active[s.a];
   s.e_ok = e >= 0 && e < m;
   s.e = s.e_ok ? e : 0;
   s.cnt = counts[s.e];
@@ -176,11 +179,8 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
   __shared__ uint16_t xs[kNT * (kMaxStreamH + kPad)];
   __shared__ int pid[kNT];
-  const int n_act = *n_active_p;
-  if (n_act <= 0 || n_act > m) return;
   const int tpe = I / 8;
-  int r_lo, r_hi;
-  block_range(n_act * tpe, &r_lo, &r_hi);
+  const int n_act = *n_active_p;
 
   GuWave g;
   g.xs = xs;
@@ -194,19 +194,41 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   g.kg = g.lane >> 4;
   g.tpe = tpe;
 
-  for (int lo = r_lo; lo < r_hi;) {
-    Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m);
-    lo = sg.hi;
+  u32x4 A[kDepth][kKC];
+  int Q = 0;
+  // weight resource of the segment's expert and its first kDepth - 1 chunks
+  auto begin_segment = [&](const Segment& sg) {
     g.seg_lo = sg.lo;
     g.seg_hi = sg.hi;
     g.a = sg.a;
     g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.e_ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
     // this wave's tiles of the segment: seg_lo + wave, + kWv, ...
     const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
-    const int Q = ntw * g.cpt;
-    u32x4 A[kDepth][kKC];
+    Q = ntw * g.cpt;
 #pragma unroll
     for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
+  };
+
+  // Speculate a fully active pool (n_active == m, the usual saturated decode
+  // batch): the block's tile range and its first expert then follow from m
+  // alone, so that segment's plan loads and weight chunks go out together
+  // with the n_active load.  A wrong guess redoes the first segment.
+  int r_lo, r_hi;
+  block_range(m * tpe, &r_lo, &r_hi);
+  Segment sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
+  begin_segment(sg);
+  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
+  const bool all = n_act == m;
+  if (!all) {
+    block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo >= r_hi) return;
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+    begin_segment(sg);
+  } else if (r_lo >= r_hi) {
+    return;
+  }
+
+  for (;;) {
     finish_segment(sg, n_pairs);
     g.cnt = sg.cnt;
     const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
@@ -217,15 +239,18 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
 #pragma unroll
         for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
       }
-      // stage this pass's token rows of x in LDS
       g.p0 = p0;
       g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
-      __syncthreads();
+      // stage this pass's token rows of x in LDS (the pair ids are loaded
+      // before the barrier that waits for the previous pass's readers)
+      int pv = -1;
       if ((int)threadIdx.x < kNT) {
         const int slot = p0 + threadIdx.x;
         const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
-        pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+        pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
+      __syncthreads();
+      if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
       __syncthreads();
       const int row8 = H / 8;
       for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
@@ -249,6 +274,9 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
         }
       }
     }
+    if (sg.hi >= r_hi) break;
+    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    begin_segment(sg);
   }
 }
 
@@ -333,11 +361,8 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     int H, int I, int m, int n_pairs) {
   __shared__ uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
   __shared__ int pid[kNT];
-  const int n_act = *n_active_p;
-  if (n_act <= 0 || n_act > m) return;
   const int tpe = (H + 15) / 16;
-  int r_lo, r_hi;
-  block_range(n_act * tpe, &r_lo, &r_hi);
+  const int n_act = *n_active_p;
 
   DnWave g;
   g.hs = hs;
@@ -354,17 +379,35 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   g.tpe = tpe;
   const int lo_rows = kNT * (I + kPad);
 
-  for (int lo = r_lo; lo < r_hi;) {
-    Segment sg = next_segment(lo, r_hi, tpe, active, counts, offsets, m);
-    lo = sg.hi;
+  u32x4 A[kDepth][kKC];
+  int Q = 0;
+  auto begin_segment = [&](const Segment& sg) {
     g.seg_lo = sg.lo;
     g.a = sg.a;
     g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.e_ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
     const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
-    const int Q = ntw * g.cpt;
-    u32x4 A[kDepth][kKC];
+    Q = ntw * g.cpt;
 #pragma unroll
     for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
+  };
+
+  // Speculate a fully active pool, as in gate_up_wave_kernel.
+  int r_lo, r_hi;
+  block_range(m * tpe, &r_lo, &r_hi);
+  Segment sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
+  begin_segment(sg);
+  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
+  const bool all = n_act == m;
+  if (!all) {
+    block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo >= r_hi) return;
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+    begin_segment(sg);
+  } else if (r_lo >= r_hi) {
+    return;
+  }
+
+  for (;;) {
     finish_segment(sg, n_pairs);
     for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
       if (p0 > 0) {
@@ -372,13 +415,16 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
       }
       g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
-      __syncthreads();
+      // the pass's pair ids (for the y rows) and its h rows, which are
+      // contiguous in dispatch-slot order
+      int pv = -1;
       if ((int)threadIdx.x < kNT) {
         const int slot = p0 + threadIdx.x;
         const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
-        pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+        pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
-      // h rows of the pass are contiguous in dispatch-slot order
+      __syncthreads();  // the previous pass's readers of hs and pid are done
+      if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
       const int row8 = I / 8;
       for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
         const int tok = idx / row8, c8 = idx - tok * row8;
@@ -405,6 +451,9 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         }
       }
     }
+    if (sg.hi >= r_hi) break;
+    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    begin_segment(sg);
   }
 }
 

@@ -1,12 +1,11 @@
 // Router of the MoE layer on gfx950: fp32 logits, masked top-k selection and
-// renormalised gates (Section 3.1, Eq. 2 and the renormalisation after it).
-#include "sw_device.h"
+// renormalised gates (Section 3.1, Eq. 2 and the renormalisation after it),
+// and the fused route + dispatch of small (decode-sized) batches.
+#include "dispatch_block.h"
 #include "sw_launch.h"
 
 namespace sw {
 namespace {
-
-constexpr int kMaxPool = 1024;
 
 // fp32 w = hi + mid + lo exactly, each piece a bf16 (truncating split: hi
 // keeps the top 8 significand bits, mid the next 8, lo the last 8), for
@@ -31,19 +30,20 @@ __device__ __forceinline__ void split3_bf16x8(const float4& a, const float4& b, 
   }
 }
 
-// z[t, e] = sum_h x[t, h] * wr[e, h]  (+ bias[e]), fp32.
-// Block = KW waves; tile = 16 experts x 16 tokens; the waves split H.  The
-// router row is split exactly into three bf16 pieces, so each 32-wide K
-// step is three bf16 MFMAs whose products are exact in fp32.
+// Partial logits part[ks][t][e] = sum over the ks-th slice of H of
+// x[t, h] * wr[e, h], fp32.  Grid (token tiles, expert tiles, KS); a block
+// is KW waves that split its slice; tile = 16 experts x 16 tokens.  The
+// router row is split exactly into three bf16 pieces, so each 32-wide K step
+// is three bf16 MFMAs whose products are exact in fp32.  Spreading H over KS
+// blocks lets a decode-sized batch (few tiles) use many compute units.
 template <int KW>
 __global__ __launch_bounds__(64 * KW) void route_logits_kernel(const uint16_t* __restrict__ x,
                                                               const float* __restrict__ wr,
-                                                              const float* __restrict__ bias,
-                                                              float* __restrict__ z, int T, int H,
-                                                              int m) {
+                                                              float* __restrict__ part, int T,
+                                                              int H, int m) {
   constexpr int kChunk = 4;  // K steps whose loads are issued together
-  __shared__ f32x4 part[KW][kWave];
-  const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 16;
+  __shared__ f32x4 red[KW][kWave];
+  const int t0 = blockIdx.x * 16, e0 = blockIdx.y * 16, ks = blockIdx.z, KS = gridDim.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r = lane & 15, kg = lane >> 4;
   const auto w_rsrc = make_rsrc(wr, 4u * (uint32_t)m * (uint32_t)H);
@@ -51,7 +51,9 @@ __global__ __launch_bounds__(64 * KW) void route_logits_kernel(const uint16_t* _
   const bool e_ok = e0 + r < m, t_ok = t0 + r < T;
   const uint32_t w_row = (uint32_t)(e0 + r) * H * 4u, x_row = (uint32_t)(t0 + r) * H * 2u;
   const int nsteps = (H + 31) >> 5;
-  const int s_lo = (wave * nsteps) / KW, s_hi = ((wave + 1) * nsteps) / KW;
+  const int b_lo = (ks * nsteps) / KS, b_hi = ((ks + 1) * nsteps) / KS;
+  const int s_lo = b_lo + (wave * (b_hi - b_lo)) / KW;
+  const int s_hi = b_lo + ((wave + 1) * (b_hi - b_lo)) / KW;
 
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   for (int sb = s_lo; sb < s_hi; sb += kChunk) {
@@ -74,130 +76,344 @@ __global__ __launch_bounds__(64 * KW) void route_logits_kernel(const uint16_t* _
       acc = mfma_16x16x32(lo, xb[c], acc);
     }
   }
-  part[wave][lane] = acc;
+  red[wave][lane] = acc;
   __syncthreads();
   if (wave == 0) {
-    f32x4 c = part[0][lane];
+    f32x4 c = red[0][lane];
 #pragma unroll
-    for (int w = 1; w < KW; ++w) c += part[w][lane];
-    // c[i] = z for expert e0 + 4*kg + i, token t0 + r
+    for (int w = 1; w < KW; ++w) c += red[w][lane];
+    // c[i] = partial z of expert e0 + 4*kg + i, token t0 + r
     const int t = t0 + r;
     if (t < T) {
+      float* dst = part + ((size_t)ks * T + t) * m;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int e = e0 + 4 * kg + i;
-        if (e < m) z[(size_t)t * m + e] = bias ? c[i] + bias[e] : c[i];
+        if (e < m) dst[e] = c[i];
       }
     }
   }
 }
 
-// One wave per token: top-k over the eligible experts by (z desc, id asc),
-// then softmax over the k selected logits.  Each round takes the largest
-// remaining order key with a DPP max and, among lanes holding it, the
-// smallest expert id with a DPP min.  KPL = keys per lane (ceil(m / 64)).
-template <int KPL>
-__global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ z,
-                                                        const uint8_t* __restrict__ keep_mask,
-                                                        int T, int m, int k,
-                                                        int* __restrict__ topk_ids,
-                                                        float* __restrict__ topk_w,
-                                                        float* __restrict__ gap) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;
-  const float* zt = z + (size_t)t * m;
-  // order key of each logit; 0 marks "not eligible or already taken" (the
-  // one logit whose key is 0, a NaN, is nudged to 1)
-  uint32_t key[KPL];
-#pragma unroll
-  for (int q = 0; q < KPL; ++q) {
-    const int e = q * 64 + lane;
-    const bool ok = e < m && (keep_mask == nullptr || keep_mask[e] != 0);
-    key[q] = ok ? max(f32_order_key(zt[e]), 1u) : 0u;
-  }
+constexpr int kMaxSplit = 4;  // slices of H per logit tile
 
-  int my_id = -1;
-  float my_z = 0.f, zk = 0.f, zk1 = 0.f;
+// Order key of token t's logit for expert e: z = sum of the KS partials in
+// slice order, plus the bias; 0 marks an ineligible expert (the one logit
+// whose key is 0, a NaN, is nudged to 1).  All partial loads are issued
+// before the first add.
+__device__ __forceinline__ uint32_t logit_key(const float* __restrict__ part, int KS, int T,
+                                              int m, int t, int e, const float* __restrict__ bias,
+                                              const uint8_t* __restrict__ keep_mask) {
+  if (e >= m || (keep_mask != nullptr && keep_mask[e] == 0)) return 0u;
+  const float* p = part + (size_t)t * m + e;
+  const size_t plane = (size_t)T * m;
+  float zp[kMaxSplit];
+#pragma unroll
+  for (int ks = 0; ks < kMaxSplit; ++ks) zp[ks] = ks < KS ? p[ks * plane] : 0.f;
+  float z = zp[0];
+#pragma unroll
+  for (int ks = 1; ks < kMaxSplit; ++ks)
+    if (ks < KS) z += zp[ks];
+  if (bias != nullptr) z += bias[e];
+  return max(f32_order_key(z), 1u);
+}
+
+// Reductions inside one 16-lane row (quad swaps, then the half-row and row
+// mirrors): every lane of the row ends with the row's result.
+template <typename Op>
+__device__ __forceinline__ uint32_t row_reduce_u32(uint32_t v, uint32_t identity, Op op) {
+  v = op(v, dpp_mov<dpp::kXor1>(identity, v));
+  v = op(v, dpp_mov<dpp::kXor2>(identity, v));
+  v = op(v, dpp_mov<dpp::kHalfMirror>(identity, v));
+  v = op(v, dpp_mov<dpp::kMirror>(identity, v));
+  return v;
+}
+
+// Result of one token's selection, held by the lanes of its row or wave:
+// lane j < k holds slot j.
+struct Selection {
+  int id;        // expert id of this lane's slot, -1 if none
+  float z;       // its logit
+  float gate;    // renormalised gate (0 without an expert)
+  float gap;     // z_(k) - z_(k+1); +inf if only k eligible; NaN if fewer
+};
+
+// The k + 1 selection rounds and the softmax over the k selected logits.
+// Each round takes the largest remaining order key (a max reduction) and,
+// among the lanes holding it, the smallest expert id (a min reduction); the
+// (k+1)-th round only reads the runner-up for the gap.  The red_* functions
+// reduce over the lanes that hold this token's keys (a row or the whole wave);
+// `slot` is this lane's position among them.
+template <int KPL, typename MaxOp, typename MinOp, typename SumOp>
+__device__ __forceinline__ Selection select_topk(uint32_t (&key)[KPL], const int (&eid)[KPL],
+                                                 int k, int slot, MaxOp red_max, MinOp red_min,
+                                                 SumOp red_sum) {
+  Selection s{-1, 0.f, 0.f, 0.f};
+  float z_first = 0.f, zk = 0.f, zk1 = 0.f;
   bool complete = true, have_next = false;
   for (int j = 0; j <= k; ++j) {
     uint32_t lm = key[0];
 #pragma unroll
     for (int q = 1; q < KPL; ++q) lm = key[q] > lm ? key[q] : lm;
-    const uint32_t best = wave_max_u32(lm);
-    if (best == 0) {  // wave-uniform: no eligible expert left
-      if (j < k) complete = false;
-      break;
-    }
+    const uint32_t best = red_max(lm);
+    const bool found = best != 0;  // uniform over the reducing lanes
     const float ze = f32_from_order_key(best);
     if (j == k) {
-      zk1 = ze;
-      have_next = true;
+      if (found) {
+        zk1 = ze;
+        have_next = true;
+      }
       break;
     }
+    if (!found) complete = false;
     uint32_t cand = 0xffffffffu;
 #pragma unroll
-    for (int q = KPL - 1; q >= 0; --q) cand = key[q] == best ? (uint32_t)(q * 64 + lane) : cand;
-    const int e = (int)wave_min_u32(cand);
-    if (lane == j) {
-      my_id = e;
-      my_z = ze;
-    }
-    if (j == k - 1) zk = ze;
+    for (int q = KPL - 1; q >= 0; --q) cand = key[q] == best ? (uint32_t)eid[q] : cand;
+    const int e = (int)red_min(cand);
+    if (found) {
+      if (j == 0) z_first = ze;
+      if (slot == j) {
+        s.id = e;
+        s.z = ze;
+      }
+      if (j == k - 1) zk = ze;
 #pragma unroll
-    for (int q = 0; q < KPL; ++q)
-      if (q * 64 + lane == e) key[q] = 0u;
+      for (int q = 0; q < KPL; ++q)
+        if (eid[q] == e) key[q] = 0u;
+    }
   }
+  const float ex = (slot < k && s.id >= 0) ? expf(s.z - z_first) : 0.f;
+  const float sum = red_sum(ex);
+  s.gate = s.id >= 0 ? ex / sum : 0.f;
+  s.gap = !complete ? __builtin_nanf("") : (have_next ? zk - zk1 : __builtin_inff());
+  return s;
+}
 
-  const float z0 = __shfl(my_z, 0);
-  const float ex = (lane < k && my_id >= 0) ? expf(my_z - z0) : 0.f;
-  const float s = wave_sum_f32(ex);
-  if (lane < k) {
-    topk_ids[(size_t)t * k + lane] = my_id;
-    topk_w[(size_t)t * k + lane] = my_id >= 0 ? ex / s : 0.f;
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint32_t fadd_bits(uint32_t a, uint32_t b) {
+  return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+}
+
+// Top-k of one token per 16-lane row (four tokens per wave): lane r of the
+// row holds the keys of experts q * 16 + r.  Needs m <= 16 * KPL and k <= 16.
+// The softmax sum runs over the row with the same pairing as the wave
+// variant's first four steps; the other rows only add +0 there, so both
+// variants give identical gates.
+template <int KPL>
+__device__ __forceinline__ Selection select_row(const float* part, int KS, int T, int m, int k,
+                                                int t, const float* bias,
+                                                const uint8_t* keep_mask) {
+  const int r = threadIdx.x & 15;
+  uint32_t key[KPL];
+  int eid[KPL];
+#pragma unroll
+  for (int q = 0; q < KPL; ++q) {
+    eid[q] = q * 16 + r;
+    key[q] = t < T ? logit_key(part, KS, T, m, t, eid[q], bias, keep_mask) : 0u;
   }
-  if (gap != nullptr && lane == 0)
-    gap[t] = !complete ? __builtin_nanf("") : (have_next ? zk - zk1 : __builtin_inff());
+  return select_topk<KPL>(
+      key, eid, k, r, [](uint32_t v) { return row_reduce_u32(v, 0u, umax); },
+      [](uint32_t v) { return row_reduce_u32(v, 0xffffffffu, umin); },
+      [](float v) { return __uint_as_float(row_reduce_u32(__float_as_uint(v), 0u, fadd_bits)); });
+}
+
+// Top-k of one token per wave: lane l holds the keys of experts q * 64 + l.
+template <int KPL>
+__device__ __forceinline__ Selection select_wave(const float* part, int KS, int T, int m, int k,
+                                                 int t, const float* bias,
+                                                 const uint8_t* keep_mask) {
+  const int lane = threadIdx.x & 63;
+  uint32_t key[KPL];
+  int eid[KPL];
+#pragma unroll
+  for (int q = 0; q < KPL; ++q) {
+    eid[q] = q * 64 + lane;
+    key[q] = logit_key(part, KS, T, m, t, eid[q], bias, keep_mask);
+  }
+  return select_topk<KPL>(
+      key, eid, k, lane, [](uint32_t v) { return wave_max_u32(v); },
+      [](uint32_t v) { return wave_min_u32(v); }, [](float v) { return wave_sum_f32(v); });
+}
+
+__device__ __forceinline__ void store_selection(const Selection& s, int t, int k, int slot,
+                                                int* __restrict__ topk_ids,
+                                                float* __restrict__ topk_w,
+                                                float* __restrict__ gap) {
+  if (slot < k) {
+    topk_ids[(size_t)t * k + slot] = s.id;
+    topk_w[(size_t)t * k + slot] = s.gate;
+  }
+  if (gap != nullptr && slot == 0) gap[t] = s.gap;
+}
+
+// ROW: one token per 16-lane row (16 tokens per 256-thread block), else one
+// token per wave (4 per block).
+template <int KPL, bool ROW>
+__global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ part, int KS,
+                                                        const float* __restrict__ bias,
+                                                        const uint8_t* __restrict__ keep_mask,
+                                                        int T, int m, int k,
+                                                        int* __restrict__ topk_ids,
+                                                        float* __restrict__ topk_w,
+                                                        float* __restrict__ gap) {
+  if (ROW) {
+    const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
+    const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
+    if (t < T) store_selection(s, t, k, threadIdx.x & 15, topk_ids, topk_w, gap);
+  } else {
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;  // wave-uniform
+    const Selection s = select_wave<KPL>(part, KS, T, m, k, t, bias, keep_mask);
+    store_selection(s, t, k, threadIdx.x & 63, topk_ids, topk_w, gap);
+  }
+}
+
+// Route + dispatch of a small batch in one 1024-thread block: every 16-lane
+// row selects one token at a time (64 tokens per pass), the ids go to LDS as
+// well as to memory, and the block then builds the dispatch plan from them.
+constexpr int kFusedThreads = 1024;
+constexpr int kFusedMaxPool = 256;
+constexpr int kFusedMaxPairs = 4096;
+
+template <int KPL>
+__global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
+    const float* __restrict__ part, int KS, const float* __restrict__ bias,
+    const uint8_t* __restrict__ keep_mask, int T, int m, int k, int* __restrict__ topk_ids,
+    float* __restrict__ topk_w, float* __restrict__ gap, int* __restrict__ counts,
+    int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
+    int* __restrict__ n_active) {
+  __shared__ int ids_s[kFusedMaxPairs];
+  __shared__ int cursor[kFusedMaxPool];
+  __shared__ int wave_base[(kFusedThreads / kWave) * kFusedMaxPool];
+  __shared__ uint8_t wave_cnt[(kFusedThreads / kWave) * kFusedMaxPool];
+  __shared__ uint32_t scan_scratch[34];
+  __shared__ int bad;
+  const int row = threadIdx.x >> 4, r = threadIdx.x & 15;
+  for (int t0 = 0; t0 < T; t0 += kFusedThreads / 16) {
+    const int t = t0 + row;
+    const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
+    if (t < T) {
+      store_selection(s, t, k, r, topk_ids, topk_w, gap);
+      if (r < k) ids_s[t * k + r] = s.id;
+    }
+  }
+  __syncthreads();
+  const DispatchLds lds{cursor, wave_base, wave_cnt, scan_scratch, &bad};
+  dispatch_block(ids_s, T * k, m, lds, counts, offsets, perm, active, n_active);
+}
+
+// Split of the router contraction for T tokens and m experts: KW waves per
+// block, KS blocks per 16 x 16 output tile.  Few tiles (decode): 4 waves and
+// up to 4 slices of H, so that about 256 blocks share the router bytes; many
+// tiles (prefill): 2 waves and no split.
+struct LogitsSplit {
+  int kw, ks;
+};
+
+LogitsSplit logits_split(int T, int H, int m) {
+  const long tiles = (long)((T + 15) / 16) * ((m + 15) / 16);
+  if (tiles >= 1024) return {2, 1};
+  const int nsteps = (H + 31) / 32;
+  const int max_ks = std::min(kMaxSplit, std::max(1, nsteps / 16));  // waves keep >= 4 K steps
+  const long want = (256 + tiles - 1) / tiles;
+  return {4, (int)std::max<long>(1, std::min<long>(want, max_ks))};
+}
+
+hipError_t launch_logits(const uint16_t* x, int T, const float* wr, int H, int m, float* part,
+                         const LogitsSplit& sp, hipStream_t stream) {
+  const dim3 grid((T + 15) / 16, (m + 15) / 16, sp.ks);
+  if (sp.kw == 4)
+    route_logits_kernel<4><<<grid, 256, 0, stream>>>(x, wr, part, T, H, m);
+  else
+    route_logits_kernel<2><<<grid, 128, 0, stream>>>(x, wr, part, T, H, m);
+  return hipGetLastError();
+}
+
+template <int KPL, bool ROW>
+void launch_topk_t(const float* part, int KS, const float* bias, const uint8_t* keep_mask, int T,
+                   int m, int k, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
+  const int per_block = ROW ? 16 : 4;
+  route_topk_kernel<KPL, ROW><<<(T + per_block - 1) / per_block, 256, 0, stream>>>(
+      part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap);
+}
+
+void launch_topk(const float* part, int KS, const float* bias, const uint8_t* keep_mask, int T,
+                 int m, int k, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
+  if (k <= 16 && m <= 256) {
+    const int kpl = (m + 15) / 16;
+    if (kpl <= 4)
+      launch_topk_t<4, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    else if (kpl <= 8)
+      launch_topk_t<8, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    else
+      launch_topk_t<16, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    return;
+  }
+  const int kpl = (m + 63) / 64;
+  if (kpl <= 1)
+    launch_topk_t<1, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  else if (kpl <= 2)
+    launch_topk_t<2, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  else if (kpl <= 4)
+    launch_topk_t<4, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  else if (kpl <= 8)
+    launch_topk_t<8, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  else
+    launch_topk_t<16, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
 }
 
 }  // namespace
 
-size_t route_workspace_bytes(int T, int m) {
-  return T > 0 ? align_up((size_t)T * m * sizeof(float), 256) : 0;
-}
-
-template <int KPL>
-static void launch_topk_t(const float* z, const uint8_t* keep_mask, int T, int m, int k,
-                          int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
-  route_topk_kernel<KPL><<<(T + 3) / 4, 256, 0, stream>>>(z, keep_mask, T, m, k, topk_ids, topk_w,
-                                                          gap);
+size_t route_workspace_bytes(int T, int H, int m) {
+  if (T <= 0) return 0;
+  return align_up((size_t)logits_split(T, H, m).ks * T * m * sizeof(float), 256);
 }
 
 hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* bias,
                         const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                         float* topk_w, float* gap, void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  float* z = static_cast<float*>(workspace);
-  const dim3 grid((T + 15) / 16, (m + 15) / 16);
-  // few output tiles: spread H over 16 waves per tile (one load round trip
-  // per wave at H = 2048); many: 2 waves
-  if ((long)grid.x * grid.y < 1024)
-    route_logits_kernel<16><<<grid, 1024, 0, stream>>>(x, wr, bias, z, T, H, m);
-  else
-    route_logits_kernel<2><<<grid, 128, 0, stream>>>(x, wr, bias, z, T, H, m);
-  hipError_t err = hipGetLastError();
+  float* part = static_cast<float*>(workspace);
+  const LogitsSplit sp = logits_split(T, H, m);
+  hipError_t err = launch_logits(x, T, wr, H, m, part, sp, stream);
   if (err != hipSuccess) return err;
-  const int kpl = (m + 63) / 64;
-  if (kpl <= 1)
-    launch_topk_t<1>(z, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
-  else if (kpl <= 2)
-    launch_topk_t<2>(z, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
-  else if (kpl <= 4)
-    launch_topk_t<4>(z, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  launch_topk(part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+  return hipGetLastError();
+}
+
+bool fused_route_dispatch_supported(int T, int m, int k) {
+  return T > 0 && m <= kFusedMaxPool && k <= 16 && (long)T * k <= kFusedMaxPairs;
+}
+
+hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
+                                 const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
+                                 float* topk_w, float* gap, int* counts, int* offsets, int* perm,
+                                 int* active, int* n_active, void* workspace,
+                                 hipStream_t stream) {
+  if (!fused_route_dispatch_supported(T, m, k)) {
+    hipError_t err = launch_route(x, T, wr, bias, keep_mask, H, m, k, topk_ids, topk_w, gap,
+                                  workspace, stream);
+    if (err != hipSuccess) return err;
+    return launch_dispatch(topk_ids, T * k, m, counts, offsets, perm, active, n_active, stream);
+  }
+  float* part = static_cast<float*>(workspace);
+  const LogitsSplit sp = logits_split(T, H, m);
+  hipError_t err = launch_logits(x, T, wr, H, m, part, sp, stream);
+  if (err != hipSuccess) return err;
+  const int kpl = (m + 15) / 16;
+  if (kpl <= 4)
+    route_select_dispatch_kernel<4><<<1, kFusedThreads, 0, stream>>>(
+        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
+        active, n_active);
   else if (kpl <= 8)
-    launch_topk_t<8>(z, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    route_select_dispatch_kernel<8><<<1, kFusedThreads, 0, stream>>>(
+        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
+        active, n_active);
   else
-    launch_topk_t<16>(z, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    route_select_dispatch_kernel<16><<<1, kFusedThreads, 0, stream>>>(
+        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
+        active, n_active);
   return hipGetLastError();
 }
 

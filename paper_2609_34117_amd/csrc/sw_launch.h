@@ -15,7 +15,7 @@ __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a -
 constexpr int kMaxStreamH = 2048;
 constexpr int kMaxStreamI = 1024;
 
-size_t route_workspace_bytes(int T, int m);
+size_t route_workspace_bytes(int T, int H, int m);
 size_t forward_workspace_bytes(int T, int H, int I, int k);
 
 hipError_t launch_prune_select(const float* importance, int m, int n_keep, int32_t* kept,
@@ -31,6 +31,14 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
 
 hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts, int* offsets,
                            int* perm, int* active, int* n_active, hipStream_t stream);
+
+// Route, then dispatch of the selected ids; one select + dispatch block when
+// fused_route_dispatch_supported, else the separate kernels.
+bool fused_route_dispatch_supported(int T, int m, int k);
+hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
+                                 const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
+                                 float* topk_w, float* gap, int* counts, int* offsets, int* perm,
+                                 int* active, int* n_active, void* workspace, hipStream_t stream);
 
 // `tiled`: weights in the fragment-major layout of sw_moe_pack_experts.
 hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool tiled,

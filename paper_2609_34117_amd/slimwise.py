@@ -42,6 +42,8 @@ def _load() -> ctypes.CDLL:
         "sw_moe_route_workspace_bytes": ([D, I32], SZ),
         "sw_moe_route": ([D, P, I32, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_dispatch": ([D, P, I32, P, P, P, P, P, P], ctypes.c_int),
+        "sw_moe_route_dispatch": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
+                                  ctypes.c_int),
         "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
         "sw_moe_pack_experts": ([D, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward": ([D, P, I32, P, P, I32, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
@@ -58,7 +60,7 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 2
+ABI_VERSION = 3
 ROW_MAJOR, TILED = 0, 1
 if LIB.sw_abi_version() != ABI_VERSION:
     raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
@@ -209,6 +211,34 @@ def sw_moe_dispatch(topk_ids: torch.Tensor, n_experts: int, *, plan: Optional[Pl
     return plan
 
 
+def sw_moe_route_dispatch(x: torch.Tensor, wr: torch.Tensor, top_k: int, *, keep_mask=None,
+                          bias=None, want_gap=True, out=None, plan: Optional[Plan] = None, ws=None,
+                          stream=None):
+    """Section 3.1, Eq. 2 then Section 2.1, Eq. 1: ``sw_moe_route`` followed by
+    ``sw_moe_dispatch`` in one call (bitwise the same results).
+
+    Returns ``(topk_ids, topk_w, gap, plan)``."""
+    t, hidden = x.shape
+    m = wr.shape[0]
+    d = Dims(hidden, 8, m, top_k)
+    if out is None:
+        out = (_empty((t, top_k), torch.int32, x.device), _empty((t, top_k), torch.float32, x.device),
+               _empty(t, torch.float32, x.device) if want_gap else None)
+    ids, w, gap = out
+    if plan is None:
+        plan = alloc_plan(t, m, top_k, x.device)
+    nbytes = sw_moe_route_workspace_bytes(d, t)
+    if ws is None:
+        ws = workspace(nbytes, x.device)
+    st = LIB.sw_moe_route_dispatch(
+        ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
+        _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
+        _ptr(ids), _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+        _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "sw_moe_route_dispatch")
+    return ids, w, gap, plan
+
+
 def _fwd_dims(x_or_t, w13_or_w2, top_k, which="w13"):
     if which == "w13":
         m, two_i, hidden = w13_or_w2.shape
@@ -270,8 +300,9 @@ def sw_moe_forward_combine(topk_w, hidden, inter, n_experts, plan: Plan, out, ws
 
 def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, layout: int = ROW_MAJOR,
               stream=None) -> dict:
-    """Route, dispatch and forward of one layer (allocating convenience wrapper)."""
-    ids, w, gap = sw_moe_route(x, wr, top_k, keep_mask=keep_mask, bias=bias, stream=stream)
-    plan = sw_moe_dispatch(ids, wr.shape[0], stream=stream)
+    """Route + dispatch (one call) and forward of one layer (allocating
+    convenience wrapper)."""
+    ids, w, gap, plan = sw_moe_route_dispatch(x, wr, top_k, keep_mask=keep_mask, bias=bias,
+                                              stream=stream)
     out = sw_moe_forward(x, w13, w2, w, plan, layout=layout, stream=stream)
     return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)

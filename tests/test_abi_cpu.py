@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 2
+    assert lib.sw_abi_version() == 3
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -93,7 +93,11 @@ def test_workspace_queries(lib):
     f = lib.sw_moe_forward_workspace_bytes
     # h hi/lo (2 x T*k*I bf16) + y (T*k*H fp32)
     assert f(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 2 * 512 * 512 * 2 + 512 * 2048 * 4
-    assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 64 * 256 * 4
+    # router logits in up to 4 slices of H: a decode batch (few 16 x 16 tiles)
+    # keeps 4 partial planes, prefill (many tiles) one
+    assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 4 * 64 * 256 * 4
+    assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 4096) == 4096 * 256 * 4
+    assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(256, 128, 16, 2)), 8) == 8 * 16 * 4
 
 
 def test_prune_and_dispatch_validation(lib):
@@ -112,6 +116,31 @@ def test_prune_and_dispatch_validation(lib):
     assert dp(ctypes.byref(d), 16, 4, None, 16, 16, 16, 16, None) == SW_ERR_NULL
     assert dp(ctypes.byref(d), None, 4, 16, 16, 16, 16, 16, None) == SW_ERR_NULL
     assert dp(ctypes.byref(d), 16, 4, 18, 16, 16, 16, 16, None) == SW_ERR_ALIGN
+
+
+def test_route_dispatch_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.sw_moe_route_dispatch
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P, P, P, P, P, P, P,
+                  ctypes.c_size_t, P]
+    d = Dims(64, 32, 8, 2)
+    args = dict(x=16, wr=16, ids=16, w=16, c=16, o=16, p=16, a=16, na=16, ws=16)
+
+    def call(dims=d, t=4, nbytes=1 << 20, **kw):
+        a = dict(args, **kw)
+        return f(ctypes.byref(dims) if dims is not None else None, a["x"], t, a["wr"], None, None,
+                 a["ids"], a["w"], None, a["c"], a["o"], a["p"], a["a"], a["na"], a["ws"], nbytes, None)
+
+    assert call(dims=None) == SW_ERR_NULL
+    assert call(dims=Dims(64, 32, 8, 9)) == SW_ERR_SHAPE
+    assert call(t=-1) == SW_ERR_SHAPE
+    assert call(c=None) == SW_ERR_NULL
+    assert call(x=None) == SW_ERR_NULL
+    assert call(p=None) == SW_ERR_NULL
+    assert call(x=24) == SW_ERR_ALIGN
+    assert call(p=18) == SW_ERR_ALIGN
+    assert call(na=2) == SW_ERR_ALIGN
+    assert call(nbytes=16) == SW_ERR_WORKSPACE
 
 
 def test_forward_validation(lib):

@@ -354,3 +354,73 @@ def test_compacting_a_tiled_pool_equals_tiling_the_compacted_pool(sw):
     b = sw.sw_moe_prune_compact(D["importance"], n_keep, cfg.top_k, w13=D["w13"], w2=D["w2"], wr=D["wr"])
     bt13, bt2 = sw.sw_moe_pack_experts(b["w13"], b["w2"])
     assert torch.equal(a["w13"], bt13) and torch.equal(a["w2"], bt2)
+
+
+# --------------------------------------------------------------------------
+# fused route + dispatch: bitwise the separate calls
+
+def _route_then_dispatch(sw, x, wr, k, m, **kw):
+    ids, w, gap = sw.sw_moe_route(x, wr, k, **kw)
+    plan = sw.sw_moe_dispatch(ids, m)
+    return ids, w, gap, plan
+
+
+def _assert_same_route_dispatch(a, b):
+    ids_a, w_a, gap_a, pa = a
+    ids_b, w_b, gap_b, pb = b
+    assert torch.equal(ids_a, ids_b)
+    # gates and gaps bit for bit (NaN gaps compared as bits)
+    assert torch.equal(w_a.view(torch.int32), w_b.view(torch.int32))
+    assert torch.equal(gap_a.view(torch.int32), gap_b.view(torch.int32))
+    n = int(pa.n_active.item())
+    assert n == int(pb.n_active.item())
+    for f in ("counts", "offsets", "perm"):
+        assert torch.equal(getattr(pa, f), getattr(pb, f)), f
+    if n > 0:
+        assert torch.equal(pa.active[:n], pb.active[:n])
+
+
+@pytest.mark.parametrize("hidden,n_experts,top_k,tokens,masked,biased", [
+    (256, 16, 2, 8, False, False),        # tiny shape, one logit slice
+    (2048, 64, 8, 64, False, False),      # decode batch on a compacted 64-expert pool
+    (2048, 128, 8, 64, True, False),      # full pool under a 50% mask
+    (2048, 256, 8, 1, False, True),       # one token, 256 experts, with bias
+    (2048, 256, 8, 256, True, True),      # 256 tokens: four selection passes of the block
+    (2048, 256, 8, 512, False, False),    # T*k = 4096: largest fused batch
+    (2048, 256, 8, 600, False, False),    # T*k > 4096: separate kernels
+    (512, 300, 8, 40, False, False),      # m > 256: separate kernels, wave top-k
+    (256, 64, 17, 20, False, False),      # k > 16: separate kernels, wave top-k
+    (520, 12, 4, 70, True, False),        # ragged H
+])
+def test_route_dispatch_equals_route_then_dispatch(sw, hidden, n_experts, top_k, tokens, masked,
+                                                   biased):
+    cfg, L, D = small_layer(hidden, n_experts, top_k, 32, tokens, seed=3)
+    kw = {}
+    if masked:
+        kw["keep_mask"] = dev(oracle.prune_compact(L["importance"], n_experts // 2, top_k)[2])
+    if biased:
+        g = np.random.default_rng(11)
+        kw["bias"] = dev((0.5 * g.standard_normal(n_experts)).astype(np.float32))
+    a = _route_then_dispatch(sw, D["x"], D["wr"], top_k, n_experts, **kw)
+    b = sw.sw_moe_route_dispatch(D["x"], D["wr"], top_k, **kw)
+    _assert_same_route_dispatch(a, b)
+    # and the routing itself against the oracle
+    mask_np = host(kw["keep_mask"]) if masked else None
+    bias_np = host(kw["bias"]) if biased else None
+    ids_o, w_o, _, z_o = oracle.route(L["x"], L["wr"], top_k, keep_mask=mask_np, bias=bias_np,
+                                      want_logits=True)
+    compare_routing(host(b[0]), host(b[1]), ids_o, w_o, z_o, mask_np, top_k)
+
+
+def test_route_dispatch_in_band_errors_and_empty_batch(sw):
+    cfg, L, D = small_layer(64, 8, 3, 32, 2)
+    mask = np.zeros(8, np.uint8)
+    mask[[1, 6]] = 1
+    a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
+    b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
+    _assert_same_route_dispatch(a, b)
+    assert int(b[3].n_active.item()) == -1      # the missing third choice flags the batch
+    ids, w, gap, plan = sw.sw_moe_route_dispatch(D["x"][:0], D["wr"], 3)
+    assert ids.shape == (0, 3)
+    assert int(plan.n_active.item()) == 0
+    assert torch.all(plan.counts == 0) and torch.all(plan.offsets == 0)
