@@ -1,25 +1,33 @@
 """Benchmark of the batched-decode MoE layer (route -> dispatch -> expert FFNs
 -> combine) on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload decode_b64]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
 
-One step = one pass of the whole decode layer (route + dispatch in one call,
-then gate_up, down, combine) over one batch of synthetic tokens, with every
-input already resident in HBM.  The default workload is the batch-64 decode layer (H 2048, 128 experts, top-8, I 768) with a 50%
-pruned decoder (64 kept experts, compacted pool); the unpruned pool is timed
-in the same run for the speedup.  Batches rotate over 16 pre-generated token
-sets and the pool over 4 copies at distinct addresses, so the 256 MB
-Infinity Cache cannot serve expert bytes from one step to the next.
+One step = one pass of the whole layer (route + dispatch in one call, then
+gate_up, down, combine) over one batch of synthetic tokens, with every input
+already resident in HBM.  Batches rotate over pre-generated token sets and
+each pool over 4 copies at distinct addresses, so the 256 MB Infinity Cache
+cannot serve expert bytes from one step to the next.
+
+Workloads (the default line is decode_b64):
+  decode_b64    H 2048, 128 experts, top-8, I 768, batch 64: the 50% pruned
+                decoder (64 kept experts, compacted pool) and the unpruned
+                pool, for the speedup.
+  decode_sweep  H 2048, 256 experts, top-8, I 512: batches 1..256 at 0, 25,
+                50 and 75% pruning (unique expert bytes per step next to
+                Eq. 1's expectation); `value` is batch 64 at 50%.
+  prefill       the same layer shape, 4096 tokens through the full pool.
 
 Prints one JSON line.  `roofline` describes the dominant kernel (gate_up,
 which streams 2/3 of each active expert's bytes): algorithmic bytes per
 launch (the unique expert bytes n_active * 2 * I * H * 2) over its mean
 launch duration, measured with HIP events around back-to-back launches on the
-launch stream.  `traffic` is the HBM byte count of one such launch from the
-FETCH_SIZE / WRITE_SIZE hardware counters, scaled by what those counters read
-for plain device copies of known size; it is reported only while the kernel
-sources hash to the ones the counters were taken on.  `cpu_baseline` is the
-single-threaded C oracle timed on a bounded sample.
+launch stream (for prefill, also its flops against the bf16 MFMA peak).
+`traffic` is the HBM byte count of one such launch from the FETCH_SIZE /
+WRITE_SIZE hardware counters, scaled by what those counters read for plain
+device copies of known size; it is reported only for the workload and kernel
+sources the counters were taken on.  `cpu_baseline` is the single-threaded C
+oracle timed on a bounded sample of the same workload.
 """
 from __future__ import annotations
 
@@ -40,6 +48,7 @@ from paper_2609_34117_amd import inputs as I  # noqa: E402
 
 METRIC = "MoE decode-layer tokens/s + achieved HBM GB/s, batch 64, 0% vs 50% pruned"
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 N_X = 16
 N_COPIES = 4
 
@@ -63,7 +72,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="decode_b64", choices=["decode_b64", "decode_sweep"])
+    ap.add_argument("--workload", default="decode_b64",
+                    choices=["decode_b64", "decode_sweep", "prefill"])
+    ap.add_argument("--sweep-steps", type=int, default=50,
+                    help="timed steps per (batch, pruning) point of decode_sweep")
     ap.add_argument("--batch", type=int, default=None)
     ap.add_argument("--pruning", type=float, default=0.5)
     ap.add_argument("--layout", default="tiled", choices=["tiled", "row_major"])
@@ -127,28 +139,28 @@ class Runner:
 
 def time_runner(torch, r: Runner, xs, steps, warmup):
     for s in range(warmup):
-        r.step(xs[s % N_X], s % N_COPIES)
+        r.step(xs[s % len(xs)], s % N_COPIES)
     torch.cuda.synchronize()
     # (a) whole steps, nothing recorded between kernels
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for s in range(steps):
-        r.step(xs[s % N_X], s % N_COPIES)
+        r.step(xs[s % len(xs)], s % N_COPIES)
     e1.record()
     torch.cuda.synchronize()
     t_step = e0.elapsed_time(e1) / 1e3 / steps
     # (b) the same steps with events around each forward phase
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
     for s in range(steps):
-        r.step(xs[s % N_X], s % N_COPIES, ev=evs[s])
+        r.step(xs[s % len(xs)], s % N_COPIES, ev=evs[s])
     torch.cuda.synchronize()
     phase = np.array([[ev[i].elapsed_time(ev[i + 1]) / 1e3 for i in range(3)] for ev in evs])
     # n_active of every rotated batch (deterministic given the batch)
     n_act = []
-    for j in range(N_X):
+    for j in range(len(xs)):
         r.step(xs[j], 0)
         n_act.append(int(r.plan.n_active.item()))
-    n_act_steps = np.array([n_act[s % N_X] for s in range(steps)], float)
+    n_act_steps = np.array([n_act[s % len(xs)] for s in range(steps)], float)
     kern = time_kernels(torch, r, xs, steps)
     return t_step, phase, n_act_steps, n_act, kern
 
@@ -165,7 +177,7 @@ def time_kernels(torch, r: Runner, xs, steps):
     out = {}
     for name in ("gate_up", "down"):
         for s in range(4):
-            j, c = s % N_X, s % N_COPIES
+            j, c = s % len(xs), s % N_COPIES
             if name == "gate_up":
                 sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
             else:
@@ -173,7 +185,7 @@ def time_kernels(torch, r: Runner, xs, steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for s in range(steps):
-            j, c = s % N_X, s % N_COPIES
+            j, c = s % len(xs), s % N_COPIES
             if name == "gate_up":
                 sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
             else:
@@ -192,26 +204,213 @@ def sources_sha256():
     return h.hexdigest()
 
 
-def cpu_baseline(cfg, L, pruning, seconds):
-    """The C oracle (single-threaded) on the same decode layer: whole 64-token
-    batches through route + dispatch + forward until `seconds` have passed."""
+def cpu_baseline(cfg, L, pruning, seconds, tokens):
+    """The C oracle (single-threaded) on the same layer: whole batches of
+    `tokens` tokens through route + dispatch + forward until `seconds` have
+    passed."""
     import oracle
 
     k = cfg.top_k
-    n_keep = cfg.n_keep(pruning)
-    kept, remap, mask, w13c, w2c, wrc, _ = oracle.prune_compact(L["importance"], n_keep, k,
-                                                                w13=L["w13"], w2=L["w2"], wr=L["wr"])
-    tokens, elapsed, batches = 0, 0.0, 0
+    if pruning > 0:
+        n_keep = cfg.n_keep(pruning)
+        _, _, _, w13, w2, wr, _ = oracle.prune_compact(L["importance"], n_keep, k, w13=L["w13"],
+                                                       w2=L["w2"], wr=L["wr"])
+    else:
+        w13, w2, wr = L["w13"], L["w2"], L["wr"]
+    done, elapsed, batches = 0, 0.0, 0
     while elapsed < seconds and batches < N_X:
-        x = I.make_x(cfg, rep=batches)
+        x = I.make_x(cfg, tokens=tokens, rep=batches)
         t0 = time.perf_counter()
-        oracle.layer(x, wrc, w13c, w2c, k)
+        oracle.layer(x, wr, w13, w2, k)
         elapsed += time.perf_counter() - t0
-        tokens += x.shape[0]
+        done += x.shape[0]
         batches += 1
-    return dict(value=tokens / elapsed, unit="tokens/s", cores=1, kind="oracle",
-                sample=f"{batches} batch(es) of {cfg.tokens} tokens through the {int(pruning * 100)}% "
-                       f"pruned layer (route+dispatch+forward), {elapsed:.1f} s, 1 thread")
+    return dict(value=round(done / elapsed, 2), unit="tokens/s", cores=1, kind="oracle",
+                sample=f"{batches} batch(es) of {tokens} tokens through the {int(pruning * 100)}% "
+                       f"pruned {cfg.name} layer (route+dispatch+forward), {elapsed:.1f} s, 1 thread")
+
+
+def up(torch, dev, a):
+    a = np.ascontiguousarray(a)
+    return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
+
+
+def build_pools(sw, torch, cfg, L, prunings, layout, dev):
+    """pruning -> Pool: the full pool for 0, compacted pools otherwise (the
+    tiled layout is packed once, then the tiled pool is compacted)."""
+    w13, w2, wr, imp = (up(torch, dev, L[k]) for k in ("w13", "w2", "wr", "importance"))
+    if layout == sw.TILED:
+        w13, w2 = sw.sw_moe_pack_experts(w13, w2)
+    pools = {}
+    for p in prunings:
+        if p == 0:
+            pools[p] = Pool(w13, w2, wr, layout)
+        else:
+            c = sw.sw_moe_prune_compact(imp, cfg.n_keep(p), cfg.top_k, w13=w13, w2=w2, wr=wr)
+            pools[p] = Pool(c["w13"], c["w2"], c["wr"], layout)
+    torch.cuda.synchronize()
+    return pools
+
+
+def measure(sw, torch, pool, cfg, T, xs, steps, warmup, dev):
+    """Times one pool at batch T; returns the summary of its steps."""
+    r = Runner(sw, torch, pool, cfg, T, dev)
+    t_step, phase, nact_steps, _, kern = time_runner(torch, r, xs, steps, warmup)
+    H, Iw, k, m = cfg.hidden, cfg.inter, cfg.top_k, pool.m
+    t_gu, t_dn, t_cb = phase.mean(axis=0)
+    fwd = phase.sum(axis=1)
+    U = nact_steps * 3 * H * Iw * 2
+    n_mean = float(nact_steps.mean())
+    return dict(t_step_us=t_step * 1e6, tokens_per_s=T / t_step,
+                t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
+                n_active_mean=n_mean, eq1_expected=float(m * (1 - (1 - k / m) ** T)),
+                unique_MiB_per_step=float(U.mean() / 2 ** 20),
+                gate_up_launch_us=kern["gate_up"] * 1e6, down_launch_us=kern["down"] * 1e6,
+                gate_up_GBps=n_mean * 2 * H * Iw * 2 / kern["gate_up"] / 1e9,
+                down_GBps=n_mean * H * Iw * 2 / kern["down"] / 1e9,
+                fwd_GBps=float(U.sum() / fwd.sum() / 1e9),
+                layer_GBps=float(U.mean() / t_step / 1e9))
+
+
+def rounded(d):
+    return {k: round(v, 3) if isinstance(v, float) else v for k, v in d.items()}
+
+
+def base_line(args, cfg, T, value, t_step_us, steps):
+    return {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step_us / 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,0.02) bf16 experts, N(0,1) tokens, uniform importance)",
+    }
+
+
+def hbm_roofline(cfg, T, pruning, layout, s):
+    """The gate_up roofline object of one measured point."""
+    achieved = s["gate_up_GBps"]
+    traffic = None
+    if (GATE_UP_TRAFFIC["sources_sha256"] == sources_sha256()
+            and GATE_UP_TRAFFIC["workload"] == (cfg.name, T, pruning, layout)):
+        traffic = GATE_UP_TRAFFIC["bytes_per_launch"]
+    return {
+        "bound": "hbm", "kernel": "gate_up_wave_kernel",
+        "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+        "traffic_unit": "bytes/launch",
+        "algorithmic_bytes_per_launch": int(round(s["n_active_mean"] * 2 * cfg.hidden * cfg.inter * 2)),
+        "launch_us": round(s["gate_up_launch_us"], 3),
+    }
+
+
+def run_decode_b64(args, sw, torch, dev):
+    cfg = I.CONFIGS["decode_b64"]
+    T = args.batch or cfg.tokens
+    L = I.make_layer(cfg)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    pools = build_pools(sw, torch, cfg, L, (args.pruning, 0.0), layout, dev)
+    xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
+    sp = measure(sw, torch, pools[args.pruning], cfg, T, xs, args.steps, args.warmup, dev)
+    sf = measure(sw, torch, pools[0.0], cfg, T, xs, args.steps, args.warmup, dev)
+    n_keep = cfg.n_keep(args.pruning)
+    line = base_line(args, cfg, T, sp["tokens_per_s"], sp["t_step_us"], args.steps)
+    line["config"] = {
+        "workload": f"{cfg.name}: decode MoE layer H {cfg.hidden}, {cfg.n_experts} experts, "
+                    f"top-{cfg.top_k}, I {cfg.inter}, batch {T}, {int(args.pruning * 100)}% pruned "
+                    f"({n_keep} kept, compacted)",
+        "hidden": cfg.hidden, "n_experts": cfg.n_experts, "n_kept": n_keep, "top_k": cfg.top_k,
+        "inter": cfg.inter, "batch": T, "pruning": args.pruning, "weight_layout": args.layout,
+        "parallelism": "none (1 GPU)",
+    }
+    line["roofline"] = hbm_roofline(cfg, T, args.pruning, args.layout, sp)
+    line["detail"] = {
+        "pruned": rounded(sp), "full": rounded(sf),
+        "speedup_pruned_vs_full": round(sf["t_step_us"] / sp["t_step_us"], 3),
+        "ideal_byte_ratio": round(sf["n_active_mean"] / sp["n_active_mean"], 3),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, L, args.pruning, args.cpu_seconds, T)
+    return line
+
+
+def run_decode_sweep(args, sw, torch, dev):
+    cfg = I.CONFIGS["decode_sweep"]
+    L = I.make_layer(cfg)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    prunings = (0.0, 0.25, 0.5, 0.75)
+    pools = build_pools(sw, torch, cfg, L, prunings, layout, dev)
+    rows, at = [], {}
+    for T in I.SWEEP_BATCHES:
+        xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
+        for p in prunings:
+            s = measure(sw, torch, pools[p], cfg, T, xs, args.sweep_steps, args.warmup, dev)
+            at[(T, p)] = s
+            rows.append(dict(batch=T, pruning=p, m_pool=pools[p].m, **rounded(s)))
+            print(f"# batch {T:3d} pruning {p:.2f}: {s['tokens_per_s']:.0f} tokens/s, "
+                  f"step {s['t_step_us']:.1f} us, n_active {s['n_active_mean']:.1f} "
+                  f"(Eq. 1 {s['eq1_expected']:.1f}), fwd {s['fwd_GBps']:.0f} GB/s",
+                  file=sys.stderr, flush=True)
+    head = at[(64, 0.5)]
+    line = base_line(args, cfg, 64, head["tokens_per_s"], head["t_step_us"], args.sweep_steps)
+    line["config"] = {
+        "workload": f"{cfg.name}: decode MoE layer H {cfg.hidden}, {cfg.n_experts} experts, "
+                    f"top-{cfg.top_k}, I {cfg.inter}; value at batch 64, 50% pruned "
+                    f"({cfg.n_keep(0.5)} kept, compacted); batches {list(I.SWEEP_BATCHES)} x "
+                    f"pruning {list(prunings)} in detail",
+        "hidden": cfg.hidden, "n_experts": cfg.n_experts, "top_k": cfg.top_k, "inter": cfg.inter,
+        "batch": 64, "pruning": 0.5, "weight_layout": args.layout, "parallelism": "none (1 GPU)",
+    }
+    line["roofline"] = hbm_roofline(cfg, 64, 0.5, args.layout, head)
+    line["detail"] = {
+        "sweep": rows,
+        "speedup_vs_full_at_b64": {str(p): round(at[(64, 0.0)]["t_step_us"] / at[(64, p)]["t_step_us"], 3)
+                                   for p in prunings},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, L, 0.5, args.cpu_seconds, 64)
+    return line
+
+
+def run_prefill(args, sw, torch, dev):
+    cfg = I.CONFIGS["prefill"]
+    T = args.batch or cfg.tokens
+    L = I.make_layer(cfg)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    pools = build_pools(sw, torch, cfg, L, (0.0,), layout, dev)
+    xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(4)]
+    steps = min(args.steps, 20)
+    s = measure(sw, torch, pools[0.0], cfg, T, xs, steps, min(args.warmup, 5), dev)
+    H, Iw, k, m = cfg.hidden, cfg.inter, cfg.top_k, cfg.n_experts
+    flops_gate_up = 2.0 * T * k * 2 * Iw * H
+    flops = flops_gate_up + 2.0 * T * k * H * Iw + 2.0 * T * m * H
+    gu_tflops = flops_gate_up / (s["gate_up_launch_us"] * 1e-6) / 1e12
+    line = base_line(args, cfg, T, s["tokens_per_s"], s["t_step_us"], steps)
+    line["config"] = {
+        "workload": f"{cfg.name}: MoE layer H {H}, {m} experts, top-{k}, I {Iw}, {T} tokens, "
+                    f"full pool (prefill shape)",
+        "hidden": H, "n_experts": m, "top_k": k, "inter": Iw, "batch": T, "pruning": 0.0,
+        "weight_layout": args.layout, "parallelism": "none (1 GPU)",
+    }
+    line["roofline"] = {
+        "bound": "mfma", "kernel": "gate_up_wave_kernel",
+        "achieved": round(gu_tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+        "frac": round(gu_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+        "algorithmic_flops_per_launch": flops_gate_up,
+        "launch_us": round(s["gate_up_launch_us"], 3),
+        "hbm": hbm_roofline(cfg, T, 0.0, args.layout, s),
+    }
+    line["detail"] = {"full": rounded(s), "layer_flops": flops,
+                      "layer_TFLOPs": round(flops / (s["t_step_us"] * 1e-6) / 1e12, 2)}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, L, 0.0, args.cpu_seconds, 64)
+    return line
 
 
 def main():
@@ -225,98 +424,9 @@ def main():
     from paper_2609_34117_amd import slimwise as sw
 
     dev = torch.device("cuda:0")
-    base = I.CONFIGS[args.workload]
-    T = args.batch or base.tokens
-    cfg = base
-    L = I.make_layer(cfg)
-
-    def up(a):
-        a = np.ascontiguousarray(a)
-        return torch.from_numpy(a.view(np.int16) if a.dtype == np.uint16 else a).to(dev)
-
-    w13, w2, wr, imp = up(L["w13"]), up(L["w2"]), up(L["wr"]), up(L["importance"])
-    xs = [up(I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
-    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
-    if layout == sw.TILED:
-        # offline: re-lay the pool out for streaming, then compact the tiled pool
-        w13, w2 = sw.sw_moe_pack_experts(w13, w2)
-    full = Pool(w13, w2, wr, layout)
-    n_keep = cfg.n_keep(args.pruning)
-    comp = sw.sw_moe_prune_compact(imp, n_keep, cfg.top_k, w13=w13, w2=w2, wr=wr)
-    pruned = Pool(comp["w13"], comp["w2"], comp["wr"], layout)
-    torch.cuda.synchronize()
-
-    res = {}
-    for name, pool in (("pruned", pruned), ("full", full)):
-        r = Runner(sw, torch, pool, cfg, T, dev)
-        res[name] = time_runner(torch, r, xs, args.steps, args.warmup)
-
-    H, Iw = cfg.hidden, cfg.inter
-    expert_bytes = 3 * H * Iw * 2
-    gate_up_bytes = 2 * H * Iw * 2
-
-    def summary(name):
-        t_step, phase, nact_steps, nact, kern = res[name]
-        t_gu, t_dn, t_cb = phase.mean(axis=0)
-        fwd = phase.sum(axis=1)
-        U = nact_steps * expert_bytes
-        n_mean = float(nact_steps.mean())
-        return dict(t_step_us=t_step * 1e6, tokens_per_s=T / t_step,
-                    t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
-                    n_active_mean=n_mean,
-                    gate_up_launch_us=kern["gate_up"] * 1e6, down_launch_us=kern["down"] * 1e6,
-                    gate_up_GBps=n_mean * gate_up_bytes / kern["gate_up"] / 1e9,
-                    down_GBps=n_mean * H * Iw * 2 / kern["down"] / 1e9,
-                    fwd_GBps=float(U.sum() / fwd.sum() / 1e9),
-                    layer_GBps=float(U.mean() / t_step / 1e9),
-                    eq1_expected=float(pools[name] * (1 - (1 - cfg.top_k / pools[name]) ** T)))
-
-    pools = {"pruned": n_keep, "full": cfg.n_experts}
-    sp, sf = summary("pruned"), summary("full")
-    achieved = sp["gate_up_GBps"]
-    algo_bytes = sp["n_active_mean"] * gate_up_bytes
-    traffic = None
-    if (GATE_UP_TRAFFIC["sources_sha256"] == sources_sha256()
-            and GATE_UP_TRAFFIC["workload"] == (cfg.name, T, args.pruning, args.layout)):
-        traffic = GATE_UP_TRAFFIC["bytes_per_launch"]
-    line = {
-        "metric": METRIC,
-        "value": round(sp["tokens_per_s"], 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(sp["t_step_us"] / 1e3, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,0.02) bf16 experts, N(0,1) tokens, uniform importance)",
-        "config": {
-            "workload": f"{cfg.name}: decode MoE layer H {H}, {cfg.n_experts} experts, top-{cfg.top_k}, "
-                        f"I {Iw}, batch {T}, {int(args.pruning * 100)}% pruned ({n_keep} kept, compacted)",
-            "hidden": H, "n_experts": cfg.n_experts, "n_kept": n_keep, "top_k": cfg.top_k,
-            "inter": Iw, "batch": T, "pruning": args.pruning, "weight_layout": args.layout,
-            "parallelism": "none (1 GPU)",
-        },
-        "roofline": {
-            "bound": "hbm", "kernel": "gate_up_wave_kernel",
-            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "traffic_unit": "bytes/launch", "algorithmic_bytes_per_launch": int(round(algo_bytes)),
-            "launch_us": round(sp["gate_up_launch_us"], 3),
-        },
-        "detail": {
-            "pruned": {k: round(v, 3) for k, v in sp.items()},
-            "full": {k: round(v, 3) for k, v in sf.items()},
-            "speedup_pruned_vs_full": round(sf["t_step_us"] / sp["t_step_us"], 3),
-            "ideal_byte_ratio": round(sf["n_active_mean"] / sp["n_active_mean"], 3),
-        },
-    }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, L, args.pruning, args.cpu_seconds)
-        line["cpu_baseline"]["value"] = round(line["cpu_baseline"]["value"], 2)
-    print(json.dumps(line), flush=True)
+    run = {"decode_b64": run_decode_b64, "decode_sweep": run_decode_sweep,
+           "prefill": run_prefill}[args.workload]
+    print(json.dumps(run(args, sw, torch, dev)), flush=True)
 
 
 if __name__ == "__main__":
