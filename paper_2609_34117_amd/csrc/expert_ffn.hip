@@ -798,6 +798,9 @@ hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool ti
                           void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
+  if (prefill_supported(T, H, I, m, k))
+    return launch_gate_up_prefill(x, T, w13, tiled, counts, offsets, perm, active, n_active, H,
+                                  I, m, k, ws.h_hi, ws.h_lo, stream);
   // the tiled layout is only produced for shapes the wave kernels take
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_gate_up_wave(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m,
@@ -839,6 +842,9 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        hipStream_t stream) {
   if (T == 0) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
+  if (prefill_supported(T, H, I, m, k))
+    return launch_down_prefill(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                               ws.h_hi, ws.h_lo, ws.y, stream);
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_down_wave(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                             ws.h_hi, ws.h_lo, ws.y, stream);

@@ -1,0 +1,444 @@
+// Expert FFN kernels for prefill-sized batches on gfx950 (Section 2.1: with
+// many tokens per expert the layer reuses each weight across those tokens,
+// so the step turns from weight streaming toward MFMA work).
+//
+// The decode kernels keep an expert's tokens in LDS over the whole
+// contraction and stream each 16-row tile once per 32-token pass; with
+// ~128 tokens per expert that would re-stream every weight four times.
+// Here the loop order is inverted:
+//   - a unit is (active expert, group of 16 row tiles), two tiles per wave;
+//     a persistent grid of one 8-wave block per compute unit walks the units;
+//   - a pass covers up to 160 of the expert's tokens (10 MFMA column
+//     blocks), so a unit streams its weights once per pass, normally once;
+//   - the contraction runs in chunks of K: the activations of the pass are
+//     staged chunk by chunk through a double-buffered LDS ring (the loads of
+//     chunk c + 1 go out before chunk c is computed and land in LDS after),
+//     while the weight chunks stream through a register pipeline (two
+//     chunks deep for gate/up, three for down) in the same fragment-major
+//     layout as the decode kernels;
+//   - every B fragment read from LDS feeds the MFMAs of both of the wave's
+//     tiles, halving LDS traffic per MFMA.
+// Each output accumulates over K in the same order as the decode kernels.
+#include "sw_device.h"
+#include "sw_launch.h"
+
+namespace sw {
+namespace {
+
+constexpr int kWv = 8;                 // waves per block
+constexpr int kBlk = 64 * kWv;         // threads per block
+constexpr int kTpw = 2;                // 16-row tiles per wave per unit
+constexpr int kTpu = kWv * kTpw;       // tiles per unit
+constexpr int kNB = 10;                // 16-token column blocks per pass
+constexpr int kNT = 16 * kNB;          // tokens per pass
+constexpr int kPad = 8;                // bf16 padding per staged row
+
+// gate/up: chunk = 4 K steps (128 columns of x)
+constexpr int kGuKs = 4;
+constexpr int kGuKc = 32 * kGuKs;
+constexpr int kGuDepth = 2;            // weight chunks held in registers per wave
+constexpr int kGuRow = kGuKc + kPad;   // staged row stride (bf16)
+constexpr int kGuPieces = kNT * kGuKc / 8;                 // 16-byte pieces per chunk
+constexpr int kGuStage = (kGuPieces + kBlk - 1) / kBlk;    // per thread
+// down: chunk = 2 K steps (64 columns of h hi and of h lo)
+constexpr int kDnKs = 2;
+constexpr int kDnKc = 32 * kDnKs;
+constexpr int kDnDepth = 3;
+constexpr int kDnRow = kDnKc + kPad;
+constexpr int kDnPieces = kNT * kDnKc / 8;                 // per half (hi or lo)
+constexpr int kDnStage = (kDnPieces + kBlk - 1) / kBlk;
+
+// Unit u -> (active slot a, tile group grp); the expert and its pair range,
+// validated against the plan.
+struct Unit {
+  int e, cnt, base, grp;
+  bool ok;
+};
+
+__device__ __forceinline__ Unit unit_of(int u, int gpe, const int* active, const int* counts,
+                                        const int* offsets, int m, int n_pairs) {
+  Unit s;
+  const int a = u / gpe;
+  s.grp = u - a * gpe;
+  const int e = active[a];
+  s.ok = e >= 0 && e < m;
+  s.e = s.ok ? e : 0;
+  s.cnt = s.ok ? counts[s.e] : 0;
+  s.base = s.ok ? offsets[s.e] : 0;
+  s.ok = s.ok && s.cnt > 0 && s.base >= 0 && s.cnt <= n_pairs - s.base;
+  return s;
+}
+
+// Pair ids of one pass into LDS (-1 past the expert's count).
+__device__ __forceinline__ void load_pass_ids(const int* perm, int base, int p0, int cnt,
+                                              int n_pairs, int* pid) {
+  if ((int)threadIdx.x < kNT) {
+    const int slot = p0 + threadIdx.x;
+    const int p = slot < cnt ? perm[base + slot] : -1;
+    pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// gate/up + SwiGLU
+
+// Weight chunk c of the wave's tiles: kGuKs fragments of 1 KiB per tile.
+template <bool kTiled>
+__device__ __forceinline__ void gu_issue(__amdgpu_buffer_rsrc_t w, const int (&ib)[kTpw],
+                                         int c, int nchunks, int H, int I, int lane,
+                                         u32x4 (&A)[kTpw][kGuKs]) {
+  const int r = lane & 15, kg = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t) {
+    uint32_t row, stride;
+    if (kTiled) {
+      row = (uint32_t)ib[t] * 32u * H + (uint32_t)lane * 16u;
+      stride = 1024u;
+    } else {
+      const int wrow = r < 8 ? ib[t] * 8 + r : I + ib[t] * 8 + (r - 8);
+      row = (uint32_t)wrow * H * 2u + kg * 16u;
+      stride = 64u;
+    }
+    const bool ok = c < nchunks && ib[t] >= 0;
+#pragma unroll
+    for (int s = 0; s < kGuKs; ++s) {
+      const uint32_t off = ok ? row + (uint32_t)(c * kGuKs + s) * stride : kOutOfRange;
+      A[t][s] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
+    }
+  }
+}
+
+// x pieces of chunk c: thread piece i -> (row i / 16, 8 columns at 8 * (i % 16)).
+__device__ __forceinline__ void gu_stage_load(const uint16_t* __restrict__ x, const int* pid,
+                                              int c, int H, int k, u32x4 (&v)[kGuStage]) {
+#pragma unroll
+  for (int j = 0; j < kGuStage; ++j) {
+    const int i = (int)threadIdx.x + j * kBlk;
+    const int row = i >> 4, c8 = i & 15;
+    const int p = i < kGuPieces ? pid[row] : -1;
+    v[j] = p >= 0 ? ld128(x + (size_t)(p / k) * H + c * kGuKc + c8 * 8) : zero4();
+  }
+}
+
+__device__ __forceinline__ void gu_stage_store(uint16_t* buf, const u32x4 (&v)[kGuStage]) {
+#pragma unroll
+  for (int j = 0; j < kGuStage; ++j) {
+    const int i = (int)threadIdx.x + j * kBlk;
+    if (i < kGuPieces) *reinterpret_cast<u32x4*>(buf + (i >> 4) * kGuRow + (i & 15) * 8) = v[j];
+  }
+}
+
+template <bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
+    const int* __restrict__ counts, const int* __restrict__ offsets,
+    const int* __restrict__ perm, const int* __restrict__ active,
+    const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
+    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
+  __shared__ uint16_t xs[2][kNT * kGuRow];
+  __shared__ int pid[kNT];
+  const int n_act = *n_active_p;
+  if (n_act <= 0 || n_act > m) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, kg = lane >> 4;
+  const int tpe = I / 8;                      // tiles per expert
+  const int gpe = (tpe + kTpu - 1) / kTpu;    // units per expert
+  const int nchunks = H / kGuKc;
+
+  for (int u = blockIdx.x; u < n_act * gpe; u += gridDim.x) {
+    const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
+    if (!s.ok) continue;  // block-uniform
+    const auto w = make_rsrc(w13 + (size_t)s.e * 2 * I * H, 4u * (uint32_t)I * (uint32_t)H);
+    const uint32_t hbytes = 2u * (uint32_t)s.cnt * (uint32_t)I;
+    const auto hh = make_rsrc(h_hi + (size_t)s.base * I, hbytes);
+    const auto hl = make_rsrc(h_lo + (size_t)s.base * I, hbytes);
+    int ib[kTpw];
+#pragma unroll
+    for (int t = 0; t < kTpw; ++t) {
+      const int tile = s.grp * kTpu + wave * kTpw + t;
+      ib[t] = tile < tpe ? tile : -1;
+    }
+
+    for (int p0 = 0; p0 < s.cnt; p0 += kNT) {
+      const int nbn = (min(kNT, s.cnt - p0) + 15) >> 4;
+      __syncthreads();  // the previous pass's readers of pid and xs are done
+      load_pass_ids(perm, s.base, p0, s.cnt, n_pairs, pid);
+      __syncthreads();
+      u32x4 A[kGuDepth][kTpw][kGuKs];
+#pragma unroll
+      for (int d = 0; d < kGuDepth - 1; ++d) gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
+      {
+        u32x4 v[kGuStage];
+        gu_stage_load(x, pid, 0, H, k, v);
+        gu_stage_store(xs[0], v);
+      }
+      f32x4 acc[kTpw][kNB];
+#pragma unroll
+      for (int t = 0; t < kTpw; ++t)
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+      for (int c0 = 0; c0 < nchunks; c0 += kGuDepth) {
+#pragma unroll
+        for (int d = 0; d < kGuDepth; ++d) {
+          const int c = c0 + d;
+          if (c < nchunks) {  // block-uniform
+            __syncthreads();  // chunk c is in LDS; chunk c - 1's buffer is free
+            u32x4 v[kGuStage];
+            const bool next = c + 1 < nchunks;
+            if (next) gu_stage_load(x, pid, c + 1, H, k, v);
+            gu_issue<kTiled>(w, ib, c + kGuDepth - 1, nchunks, H, I, lane,
+                             A[(d + kGuDepth - 1) % kGuDepth]);
+            const uint16_t* buf = xs[c & 1];
+#pragma unroll
+            for (int st = 0; st < kGuKs; ++st) {
+#pragma unroll
+              for (int nb = 0; nb < kNB; ++nb) {
+                if (nb < nbn) {
+                  const u32x4 b = *reinterpret_cast<const u32x4*>(
+                      buf + (nb * 16 + r) * kGuRow + st * 32 + kg * 8);
+#pragma unroll
+                  for (int t = 0; t < kTpw; ++t) acc[t][nb] = mfma_16x16x32(A[d][t][st], b, acc[t][nb]);
+                }
+              }
+            }
+            if (next) gu_stage_store(xs[(c + 1) & 1], v);
+          }
+        }
+      }
+
+      // SwiGLU of each tile's 8 (gate, up) row pairs; lanes 0-31 own the results
+#pragma unroll
+      for (int t = 0; t < kTpw; ++t) {
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) {
+          if (nb < nbn) {
+            const f32x4 g4 = acc[t][nb];
+            f32x4 u4;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
+            uint16_t hb[4], lb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float gt = g4[i];
+              const float hv = (gt / (1.0f + expf(-gt))) * u4[i];
+              hb[i] = f32_to_bf16(hv);
+              lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
+            }
+            const u32x2 hw = {(uint32_t)hb[0] | ((uint32_t)hb[1] << 16),
+                              (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
+            const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
+                              (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+            const int slot = p0 + nb * 16 + r;
+            uint32_t off = kOutOfRange;
+            if (lane < 32 && ib[t] >= 0 && slot < s.cnt)
+              off = ((uint32_t)slot * I + (uint32_t)(ib[t] * 8 + kg * 4)) * 2u;
+            __builtin_amdgcn_raw_buffer_store_b64(hw, hh, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b64(lw, hl, off, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down projection
+
+template <bool kTiled>
+__device__ __forceinline__ void dn_issue(__amdgpu_buffer_rsrc_t w, const int (&ob)[kTpw], int c,
+                                         int nchunks, int H, int I, int lane,
+                                         u32x4 (&A)[kTpw][kDnKs]) {
+  const int r = lane & 15, kg = lane >> 4;
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t) {
+    uint32_t row, stride;
+    if (kTiled) {
+      row = (uint32_t)ob[t] * 32u * I + (uint32_t)lane * 16u;
+      stride = 1024u;
+    } else {
+      row = (uint32_t)(ob[t] * 16 + r) * I * 2u + kg * 16u;
+      stride = 64u;
+    }
+    const bool ok = c < nchunks && ob[t] >= 0;
+#pragma unroll
+    for (int s = 0; s < kDnKs; ++s) {
+      const uint32_t off = ok ? row + (uint32_t)(c * kDnKs + s) * stride : kOutOfRange;
+      A[t][s] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
+    }
+  }
+}
+
+// h pieces of chunk c (hi then lo): rows are the pass's dispatch slots,
+// contiguous from base + p0.
+__device__ __forceinline__ void dn_stage_load(const uint16_t* __restrict__ h_hi,
+                                              const uint16_t* __restrict__ h_lo, int base,
+                                              int p0, int cnt, int c, int I,
+                                              u32x4 (&v)[2 * kDnStage]) {
+#pragma unroll
+  for (int j = 0; j < kDnStage; ++j) {
+    const int i = (int)threadIdx.x + j * kBlk;
+    const int row = i >> 3, c8 = i & 7;
+    const bool ok = i < kDnPieces && p0 + row < cnt;
+    const size_t off = (size_t)(base + p0 + row) * I + c * kDnKc + c8 * 8;
+    v[j] = ok ? ld128(h_hi + off) : zero4();
+    v[kDnStage + j] = ok ? ld128(h_lo + off) : zero4();
+  }
+}
+
+__device__ __forceinline__ void dn_stage_store(uint16_t* buf, const u32x4 (&v)[2 * kDnStage]) {
+#pragma unroll
+  for (int j = 0; j < kDnStage; ++j) {
+    const int i = (int)threadIdx.x + j * kBlk;
+    if (i < kDnPieces) {
+      uint16_t* dst = buf + (i >> 3) * kDnRow + (i & 7) * 8;
+      *reinterpret_cast<u32x4*>(dst) = v[j];
+      *reinterpret_cast<u32x4*>(dst + kNT * kDnRow) = v[kDnStage + j];
+    }
+  }
+}
+
+template <bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
+    const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
+    const uint16_t* __restrict__ w2, const int* __restrict__ counts,
+    const int* __restrict__ offsets, const int* __restrict__ perm,
+    const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
+    int H, int I, int m, int n_pairs) {
+  __shared__ uint16_t hs[2][2 * kNT * kDnRow];  // [buffer][hi rows, then lo rows]
+  __shared__ int pid[kNT];
+  const int n_act = *n_active_p;
+  if (n_act <= 0 || n_act > m) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, kg = lane >> 4;
+  const int tpe = H / 16;
+  const int gpe = (tpe + kTpu - 1) / kTpu;
+  const int nchunks = I / kDnKc;
+  const auto yr = make_rsrc(y, 4u * (uint32_t)n_pairs * (uint32_t)H);
+
+  for (int u = blockIdx.x; u < n_act * gpe; u += gridDim.x) {
+    const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
+    if (!s.ok) continue;
+    const auto w = make_rsrc(w2 + (size_t)s.e * H * I, 2u * (uint32_t)H * (uint32_t)I);
+    int ob[kTpw];
+#pragma unroll
+    for (int t = 0; t < kTpw; ++t) {
+      const int tile = s.grp * kTpu + wave * kTpw + t;
+      ob[t] = tile < tpe ? tile : -1;
+    }
+
+    for (int p0 = 0; p0 < s.cnt; p0 += kNT) {
+      const int nbn = (min(kNT, s.cnt - p0) + 15) >> 4;
+      __syncthreads();
+      load_pass_ids(perm, s.base, p0, s.cnt, n_pairs, pid);
+      u32x4 A[kDnDepth][kTpw][kDnKs];
+#pragma unroll
+      for (int d = 0; d < kDnDepth - 1; ++d) dn_issue<kTiled>(w, ob, d, nchunks, H, I, lane, A[d]);
+      {
+        u32x4 v[2 * kDnStage];
+        dn_stage_load(h_hi, h_lo, s.base, p0, s.cnt, 0, I, v);
+        dn_stage_store(hs[0], v);
+      }
+      f32x4 acc[kTpw][kNB];
+#pragma unroll
+      for (int t = 0; t < kTpw; ++t)
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+      for (int c0 = 0; c0 < nchunks; c0 += kDnDepth) {
+#pragma unroll
+        for (int d = 0; d < kDnDepth; ++d) {
+          const int c = c0 + d;
+          if (c < nchunks) {
+            __syncthreads();
+            u32x4 v[2 * kDnStage];
+            const bool next = c + 1 < nchunks;
+            if (next) dn_stage_load(h_hi, h_lo, s.base, p0, s.cnt, c + 1, I, v);
+            dn_issue<kTiled>(w, ob, c + kDnDepth - 1, nchunks, H, I, lane,
+                             A[(d + kDnDepth - 1) % kDnDepth]);
+            const uint16_t* buf = hs[c & 1];
+#pragma unroll
+            for (int st = 0; st < kDnKs; ++st) {
+#pragma unroll
+              for (int nb = 0; nb < kNB; ++nb) {
+                if (nb < nbn) {
+                  const uint16_t* row = buf + (nb * 16 + r) * kDnRow + st * 32 + kg * 8;
+                  const u32x4 bh = *reinterpret_cast<const u32x4*>(row);
+                  const u32x4 bl = *reinterpret_cast<const u32x4*>(row + kNT * kDnRow);
+#pragma unroll
+                  for (int t = 0; t < kTpw; ++t) {
+                    acc[t][nb] = mfma_16x16x32(A[d][t][st], bh, acc[t][nb]);
+                    acc[t][nb] = mfma_16x16x32(A[d][t][st], bl, acc[t][nb]);
+                  }
+                }
+              }
+            }
+            if (next) dn_stage_store(hs[(c + 1) & 1], v);
+          }
+        }
+      }
+
+      // y rows of the pass's pairs: lane (r, kg) holds output rows
+      // ob * 16 + 4 kg .. + 3 of pair pid[nb * 16 + r]
+#pragma unroll
+      for (int t = 0; t < kTpw; ++t) {
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) {
+          if (nb < nbn) {
+            const int p = pid[nb * 16 + r];
+            const int o = ob[t] * 16 + kg * 4;
+            uint32_t off = kOutOfRange;
+            if (ob[t] >= 0 && p >= 0) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[t][nb]), yr, off,
+                                                   0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+int prefill_grid() {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  return cus;
+}
+
+}  // namespace
+
+bool prefill_supported(int T, int H, int I, int m, int k) {
+  // about 48 or more tokens per expert, whole K chunks, and 32-bit offsets
+  return (int64_t)T * k >= (int64_t)48 * m && H % kGuKc == 0 && I % kDnKc == 0 &&
+         H <= 32768 && 4 * (int64_t)T * k * H < ((int64_t)1 << 31);
+}
+
+hipError_t launch_gate_up_prefill(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                  const int* counts, const int* offsets, const int* perm,
+                                  const int* active, const int* n_active, int H, int I, int m,
+                                  int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+  if (tiled)
+    gate_up_prefill_kernel<true><<<prefill_grid(), kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
+  else
+    gate_up_prefill_kernel<false><<<prefill_grid(), kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
+  return hipGetLastError();
+}
+
+hipError_t launch_down_prefill(int T, const uint16_t* w2, bool tiled, const int* counts,
+                               const int* offsets, const int* perm, const int* active,
+                               const int* n_active, int H, int I, int m, int k,
+                               const uint16_t* h_hi, const uint16_t* h_lo, float* y,
+                               hipStream_t stream) {
+  if (tiled)
+    down_prefill_kernel<true><<<prefill_grid(), kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
+  else
+    down_prefill_kernel<false><<<prefill_grid(), kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
+  return hipGetLastError();
+}
+
+}  // namespace sw

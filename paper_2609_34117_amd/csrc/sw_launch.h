@@ -58,6 +58,18 @@ hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* co
                             const int* offsets, const int* perm, const int* active,
                             const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
                             const uint16_t* h_lo, float* y, hipStream_t stream);
+// Prefill-sized batches (about 48 or more tokens per expert): each weight
+// tile is streamed once per 160-token pass (expert_prefill.hip).
+bool prefill_supported(int T, int H, int I, int m, int k);
+hipError_t launch_gate_up_prefill(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                  const int* counts, const int* offsets, const int* perm,
+                                  const int* active, const int* n_active, int H, int I, int m,
+                                  int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
+hipError_t launch_down_prefill(int T, const uint16_t* w2, bool tiled, const int* counts,
+                               const int* offsets, const int* perm, const int* active,
+                               const int* n_active, int H, int I, int m, int k,
+                               const uint16_t* h_hi, const uint16_t* h_lo, float* y,
+                               hipStream_t stream);
 hipError_t launch_pack_experts(const uint16_t* w13, const uint16_t* w2, uint16_t* w13_t,
                                uint16_t* w2_t, int H, int I, int m, hipStream_t stream);
 hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,

@@ -125,6 +125,65 @@ def test_prefill_shape_parity(sw):
 
 
 # --------------------------------------------------------------------------
+# the prefill-sized path (about 48 or more tokens per expert)
+
+def _layer_in_batches(sw, D, k, nb, layout, mask=None, bias=None):
+    """The layer over the tokens in batches of nb (small enough for the
+    decode kernels), concatenated."""
+    outs = []
+    for t0 in range(0, D["x"].shape[0], nb):
+        g = sw.moe_layer(D["x"][t0:t0 + nb], D["wr"], D["w13"], D["w2"], k, keep_mask=mask,
+                         bias=bias, layout=layout)
+        outs.append(g["out"])
+    return torch.cat(outs)
+
+
+@pytest.mark.parametrize("tiled", [False, True])
+@pytest.mark.parametrize("masked", [False, True])
+def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked):
+    # 512 tokens, 16 experts, top-4: ~128 tokens per expert, the prefill kernels
+    cfg, L, D = small_layer(256, 16, 4, 128, 512, seed=7)
+    mask = mask_for(cfg, L, 0.25) if masked else None
+    layout = sw.ROW_MAJOR
+    if tiled:
+        D = dict(D)
+        D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+        layout = sw.TILED
+    keep = None if mask is None else dev(mask)
+    g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], cfg.top_k, keep_mask=keep, layout=layout)
+    g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
+    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], cfg.top_k, keep_mask=mask, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, cfg.top_k)
+    o_out = oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w)
+    compare_out(host(g["out"]), o_out)
+    # each output accumulates in the same order on both paths: bit for bit
+    small = _layer_in_batches(sw, D, cfg.top_k, 16, layout, mask=keep)
+    assert torch.equal(g["out"], small)
+
+
+@pytest.mark.parametrize("tiled", [False, True])
+def test_prefill_path_expert_with_several_passes(sw, tiled):
+    # a bias makes expert 3 every token's first choice: 400 pairs on one
+    # expert (passes of 160, 160 and 80 tokens)
+    cfg, L, D = small_layer(256, 8, 2, 128, 400, seed=8)
+    bias = np.zeros(8, np.float32)
+    bias[3] = 50.0
+    layout = sw.ROW_MAJOR
+    if tiled:
+        D = dict(D)
+        D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+        layout = sw.TILED
+    g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], 2, bias=dev(bias), layout=layout)
+    assert int(host(g["plan"].counts)[3]) == 400
+    g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
+    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], 2, bias=bias, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 2)
+    compare_out(host(g["out"]), oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w))
+    small = _layer_in_batches(sw, D, 2, 16, layout, bias=dev(bias))
+    assert torch.equal(g["out"], small)
+
+
+# --------------------------------------------------------------------------
 # pruning: masked full pool == compacted pool, 0% == full, GPU compaction
 
 @pytest.mark.parametrize("name,pruning", [("tiny", 0.5), ("decode_b64", 0.5), ("decode_sweep", 0.25)])
