@@ -17,6 +17,10 @@ Workloads (the default line is decode_b64):
                 50 and 75% pruning (unique expert bytes per step next to
                 Eq. 1's expectation); `value` is batch 64 at 50%.
   prefill       the same layer shape, 4096 tokens through the full pool.
+  skewed_stack  40 such layers at batch 256 with a Zipf(1.1) router bias per
+                layer (60 GiB of experts, drawn on the device), the full
+                stack and the 50% pruned one (top 128 experts by
+                popularity); one step = the 40 layers back to back.
 
 Prints one JSON line.  `roofline` describes the dominant kernel (gate_up,
 which streams 2/3 of each active expert's bytes): algorithmic bytes per
@@ -73,7 +77,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="decode_b64",
-                    choices=["decode_b64", "decode_sweep", "prefill"])
+                    choices=["decode_b64", "decode_sweep", "prefill", "skewed_stack"])
     ap.add_argument("--sweep-steps", type=int, default=50,
                     help="timed steps per (batch, pruning) point of decode_sweep")
     ap.add_argument("--batch", type=int, default=None)
@@ -413,6 +417,130 @@ def run_prefill(args, sw, torch, dev):
     return line
 
 
+def run_skewed_stack(args, sw, torch, dev):
+    import oracle
+    from paper_2609_34117_amd import gen
+
+    cfg = I.CONFIGS["skewed_stack"]
+    T, H, Iw, m, k = cfg.tokens, cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k
+    n_keep = cfg.n_keep(0.5)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    layers = []
+    for li in range(cfg.n_layers):
+        w13 = torch.empty((m, 2 * Iw, H), dtype=torch.int16, device=dev)
+        w2 = torch.empty((m, H, Iw), dtype=torch.int16, device=dev)
+        gen.philox_normal_bf16(w13, I.philox_key(cfg.config_id, li, I.W13), 0, cfg.w_std)
+        gen.philox_normal_bf16(w2, I.philox_key(cfg.config_id, li, I.W2), 0, cfg.w_std)
+        if layout == sw.TILED:
+            w13, w2 = sw.sw_moe_pack_experts(w13, w2)
+        L = I.make_layer(cfg, layer=li, experts=False)
+        wr, bias, imp = (up(torch, dev, L[n]) for n in ("wr", "bias", "importance"))
+        c = sw.sw_moe_prune_compact(imp, n_keep, k, w13=w13, w2=w2, wr=wr, bias=bias)
+        xs = [up(torch, dev, I.make_x(cfg, layer=li, rep=r)) for r in range(2)]
+        x64 = up(torch, dev, I.make_x(cfg, tokens=64, layer=li, rep=7))
+        layers.append(dict(full=(w13, w2, wr, bias, m), pruned=(c["w13"], c["w2"], c["wr"], c["bias"], n_keep),
+                           xs=xs, x64=x64))
+        torch.cuda.synchronize()
+        print(f"# layer {li} drawn and packed", file=sys.stderr, flush=True)
+
+    d_full, d_pr = sw.dims(H, Iw, m, k), sw.dims(H, Iw, n_keep, k)
+    rws = sw.workspace(max(sw.sw_moe_route_workspace_bytes(d_full, T),
+                           sw.sw_moe_route_workspace_bytes(d_pr, T)), dev)
+    fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(d_full, T), dev)
+    ids = torch.empty((T, k), dtype=torch.int32, device=dev)
+    w = torch.empty((T, k), dtype=torch.float32, device=dev)
+    gap = torch.empty(T, dtype=torch.float32, device=dev)
+    out = torch.empty((T, H), dtype=torch.float32, device=dev)
+    plans = {"full": [sw.alloc_plan(T, m, k, dev) for _ in layers],
+             "pruned": [sw.alloc_plan(T, n_keep, k, dev) for _ in layers]}
+
+    def step(which, r):
+        for li, Lr in enumerate(layers):
+            w13, w2, wr, bias, mp = Lr[which]
+            x = Lr["xs"][r % 2]
+            sw.sw_moe_route_dispatch(x, wr, k, bias=bias, out=(ids, w, gap), plan=plans[which][li],
+                                     ws=rws)
+            sw.sw_moe_forward(x, w13, w2, w, plans[which][li], layout=layout, out=out, ws=fws)
+
+    steps = max(2, min(args.steps, 10))
+    res = {}
+    for which in ("pruned", "full"):
+        for r in range(2):
+            step(which, r)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for r in range(steps):
+            step(which, r)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3 / steps
+        n_act = np.array([int(p.n_active.item()) for p in plans[which]])  # of the last step
+        vol = []
+        for Lr in layers:  # pool fraction a batch of 64 touches
+            w13, w2, wr, bias, mp = Lr[which]
+            _, _, _, pl = sw.sw_moe_route_dispatch(Lr["x64"], wr, k, bias=bias)
+            vol.append(int(pl.n_active.item()) / mp)
+        U = n_act.sum() * 3 * H * Iw * 2
+        res[which] = dict(t_step_us=t * 1e6, tokens_per_s=T / t, n_active_mean=float(n_act.mean()),
+                          pool_fraction_b256=float(n_act.mean() / (m if which == "full" else n_keep)),
+                          pool_fraction_b64=float(np.mean(vol)),
+                          unique_GiB_per_step=float(U / 2 ** 30), fwd_layer_GBps=float(U / t / 1e9))
+        print(f"# {which}: {res[which]}", file=sys.stderr, flush=True)
+    sp, sf = res["pruned"], res["full"]
+    line = base_line(args, cfg, T, sp["tokens_per_s"], sp["t_step_us"], steps)
+    line["config"] = {
+        "workload": f"{cfg.name}: {cfg.n_layers} MoE layers H {H}, {m} experts, top-{k}, I {Iw}, "
+                    f"batch {T}, Zipf({cfg.zipf_s}) router bias (beta {cfg.zipf_beta}), 50% pruned "
+                    f"({n_keep} kept by popularity, compacted); step = all {cfg.n_layers} layers",
+        "hidden": H, "n_experts": m, "n_kept": n_keep, "top_k": k, "inter": Iw, "batch": T,
+        "layers": cfg.n_layers, "pruning": 0.5, "weight_layout": args.layout,
+        "parallelism": "none (1 GPU)",
+    }
+    line["data"] = ("synthetic: experts drawn on the device from a counter-based stream "
+                    "(Philox4x64-10, ~N(0,0.02) bf16), routers and tokens seeded on the host")
+    # roofline: the stack's unique expert bytes over its step time
+    ach = sp["fwd_layer_GBps"]
+    line["roofline"] = {"bound": "hbm", "kernel": "whole step (40 layers)", "achieved": round(ach, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+                        "traffic": None}
+    line["detail"] = {"pruned": rounded(sp), "full": rounded(sf),
+                      "speedup_pruned_vs_full": round(sf["t_step_us"] / sp["t_step_us"], 3)}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = stack_cpu_baseline(cfg, n_keep, args.cpu_seconds)
+    return line
+
+
+def stack_cpu_baseline(cfg, n_keep, seconds):
+    """The C oracle on layer 0 of the pruned stack (route + dispatch +
+    forward) for batches of 8 tokens, extrapolated to the 40 layers; only the
+    experts the batch selects are drawn on the host."""
+    import oracle
+
+    L = I.make_layer(cfg, layer=0, experts=False)
+    kept, remap, mask, *_ = oracle.prune_compact(L["importance"], n_keep, cfg.top_k)
+    done, elapsed, batches = 0, 0.0, 0
+    while elapsed < seconds and batches < 8:
+        x = I.make_x(cfg, tokens=8, layer=0, rep=100 + batches)
+        ids, w, _ = oracle.route(x, L["wr"], cfg.top_k, keep_mask=mask, bias=L["bias"])
+        used = np.unique(ids)
+        w13 = I.philox_expert_slice(cfg, 0, "w13", used)
+        w2 = I.philox_expert_slice(cfg, 0, "w2", used)
+        local = np.searchsorted(used, ids).astype(np.int32)
+        t0 = time.perf_counter()
+        oracle.route(x, L["wr"], cfg.top_k, keep_mask=mask, bias=L["bias"])
+        oracle.dispatch(ids, cfg.n_experts)
+        oracle.forward(x, w13, w2, local, w)
+        elapsed += time.perf_counter() - t0
+        done += x.shape[0]
+        batches += 1
+    per_layer = done / elapsed
+    return dict(value=round(per_layer / cfg.n_layers, 3), unit="tokens/s", cores=1, kind="oracle",
+                sample=f"{batches} batch(es) of 8 tokens through layer 0 of the pruned stack "
+                       f"(route+dispatch+forward, {elapsed:.1f} s, 1 thread), extrapolated to "
+                       f"{cfg.n_layers} layers")
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -425,7 +553,7 @@ def main():
 
     dev = torch.device("cuda:0")
     run = {"decode_b64": run_decode_b64, "decode_sweep": run_decode_sweep,
-           "prefill": run_prefill}[args.workload]
+           "prefill": run_prefill, "skewed_stack": run_skewed_stack}[args.workload]
     print(json.dumps(run(args, sw, torch, dev)), flush=True)
 
 

@@ -12,6 +12,14 @@ seeded random subset.
 
 Seeding: ``numpy.random.default_rng([config_id, layer, tensor_id, rep])`` with
 tensor ids x=0, router=1, W13=2, W2=3, importance=4, popularity=5.
+
+Expert pools too large to draw on the host (the 40-layer, 60 GiB stack) use a
+counter-based stream instead, so any element range can be drawn anywhere:
+element i of a tensor is a function of (key, i) alone.  The stream is
+Philox4x64-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers: as
+easy as 1, 2, 3", SC 2011); here numpy's implementation of it draws the host
+side, and the HIP library of synthetic inputs implements it independently
+for the device.  See ``philox_normal_bf16``.
 """
 from __future__ import annotations
 
@@ -155,3 +163,53 @@ def make_layer(cfg: MoEConfig, layer: int = 0, tokens: Optional[int] = None, rep
 def small_config(hidden=64, n_experts=8, top_k=2, inter=32, tokens=5, name="custom") -> MoEConfig:
     """An ad-hoc shape for edge-case tests (config id 100)."""
     return MoEConfig(name, 100, hidden=hidden, n_experts=n_experts, top_k=top_k, inter=inter, tokens=tokens)
+
+
+# ---------------------------------------------------------------------------
+# counter-based normal draws (Philox4x64-10 + Irwin-Hall)
+
+IRWIN_HALL_MEAN = 12 * 65535 // 2  # 393210: mean of a sum of 12 uniform 16-bit integers
+
+
+def philox_key(config_id: int, layer: int, tensor_id: int) -> np.ndarray:
+    """Philox key of one tensor: (config_id << 32 | layer, tensor_id)."""
+    return np.array([(config_id << 32) | layer, tensor_id], dtype=np.uint64)
+
+
+def philox_normal_bf16(key: np.ndarray, start: int, n: int, std: float) -> np.ndarray:
+    """Elements start .. start + n - 1 of a tensor ~N(0, std), as bf16 bits.
+
+    Element i takes the Philox4x64-10 block of counter (i + 1, 0, 0, 0) under
+    `key`; the twelve 16-bit halves of the block's first three 64-bit words
+    (low half first) are summed, S, and the value is
+    float32(S - 393210) * float32(std / 65536), rounded to bf16 (ties to
+    even).  The sum of 12 uniform integers on [0, 65535] has mean 393210 and
+    standard deviation ~65536 (Irwin-Hall), so the value is ~N(0, std)
+    truncated at +-6 std.  Both products are exact or correctly rounded fp32
+    operations, so any IEEE implementation gives the same bits."""
+    out = np.empty(n, np.uint16)
+    scale = np.float32(np.float32(std) / np.float32(65536.0))
+    chunk = 1 << 22
+    for s0 in range(0, n, chunk):
+        m = min(chunk, n - s0)
+        # numpy's Philox advances the counter before each block: starting
+        # from counter start + s0, the first block uses start + s0 + 1
+        bg = np.random.Philox(key=key, counter=np.array([start + s0, 0, 0, 0], dtype=np.uint64))
+        words = np.ascontiguousarray(bg.random_raw(4 * m).reshape(m, 4)[:, :3])
+        sums = words.view("<u2").reshape(m, 12).sum(axis=1, dtype=np.int64)
+        v = (sums - IRWIN_HALL_MEAN).astype(np.float32) * scale
+        out[s0:s0 + m] = to_bf16_bits(v)
+    return out
+
+
+def philox_expert_slice(cfg: MoEConfig, layer: int, which: str, experts) -> np.ndarray:
+    """Host copy of the counter-drawn W13 or W2 rows of the given experts
+    (the same bits the device draws for the whole pool)."""
+    if which == "w13":
+        tid, per, shape = W13, 2 * cfg.inter * cfg.hidden, (2 * cfg.inter, cfg.hidden)
+    else:
+        tid, per, shape = W2, cfg.hidden * cfg.inter, (cfg.hidden, cfg.inter)
+    key = philox_key(cfg.config_id, layer, tid)
+    return np.stack([philox_normal_bf16(key, int(e) * per, per, cfg.w_std).reshape(shape)
+                     for e in experts])
+

@@ -1,6 +1,6 @@
-"""CPU checks of the C ABI: the library loads, exports every symbol the header
-declares, and rejects bad arguments before touching the device (so these
-calls need no GPU and launch nothing)."""
+"""CPU checks of the C ABI: the libraries load, export every symbol their
+headers declare, and reject bad arguments before touching the device (so
+these calls need no GPU and launch nothing)."""
 import ctypes
 import os
 import re
@@ -181,11 +181,11 @@ def test_pack_validation(lib):
     assert f(ctypes.byref(Dims(64, 32, 4, 2)), 16, None, 24, None, None) == SW_ERR_ALIGN
 
 
-def _prototypes():
+def _prototypes(header=HEADER, prefix="sw_"):
     """name -> list of parameter declarations, parsed from the header."""
-    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    text = re.sub(r"/\*.*?\*/", "", open(header).read(), flags=re.S)
     protos = {}
-    for m in re.finditer(r"\b(sw_\w+)\s*\(([^;{]*?)\)\s*;", text, flags=re.S):
+    for m in re.finditer(r"\b(" + prefix + r"\w+)\s*\(([^;{]*?)\)\s*;", text, flags=re.S):
         params = [p.strip() for p in m.group(2).split(",") if p.strip() and p.strip() != "void"]
         protos[m.group(1)] = params
     return protos
@@ -213,3 +213,35 @@ def test_binding_signatures_match_the_header():
                 assert a is ctypes.c_int, (name, decl, a)
             else:
                 raise AssertionError(f"unhandled parameter {decl} of {name}")
+
+
+GEN_HEADER = os.path.join(ROOT, "include", "swgen.h")
+GEN_LIB_PATH = os.path.join(ROOT, "paper_2609_34117_amd", "libswgen.so")
+
+
+def test_input_draw_library_exports_and_binding_match_its_header():
+    from paper_2609_34117_amd import gen
+
+    protos = _prototypes(GEN_HEADER, "swg_")
+    assert protos, "no declarations parsed"
+    out = subprocess.run(["nm", "-D", "--defined-only", GEN_LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(line.split()[-1] for line in out.splitlines() if line.strip())
+    assert set(protos) <= exported
+    assert set(gen.LIB.signatures) == set(protos)
+    for name, (args, _res) in gen.LIB.signatures.items():
+        params = protos[name]
+        assert len(args) == len(params), (name, len(args), len(params))
+        for a, decl in zip(args, params):
+            if "*" in decl:
+                assert a is ctypes.c_void_p, (name, decl, a)
+            elif decl.startswith("uint64_t"):
+                assert a is ctypes.c_uint64, (name, decl, a)
+            elif decl.startswith("float"):
+                assert a is ctypes.c_float, (name, decl, a)
+            else:
+                raise AssertionError(f"unhandled parameter {decl} of {name}")
+    # no work and a NULL destination: validated without a launch
+    assert gen.LIB.swg_philox_normal_bf16(None, 0, 1, 2, 0, 0.02, None) == 0
+    assert gen.LIB.swg_philox_normal_bf16(None, 5, 1, 2, 0, 0.02, None) == 1
+
