@@ -74,7 +74,7 @@ typedef struct {
 const char* sw_status_str(int status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 3
+#define SW_ABI_VERSION 4
 int32_t sw_abi_version(void);
 
 /*
@@ -234,6 +234,32 @@ sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint
 sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
                                  const int32_t* n_active, float* out, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/* Workspace bytes sw_moe_shared_expert needs for T tokens (0 if T == 0). */
+size_t sw_moe_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
+
+/*
+ * The always-on shared expert of the distilled pruned decoder (Section 3.3:
+ * the frozen shared expert SE1 and the added SE2, whose down projection
+ * starts at zero, share one sigmoid gate and are exported as one expert of
+ * twice the intermediate width), added onto the layer output:
+ *   out[t] += sigmoid(gate_w . x[t]) * W2s (silu(W1s x[t]) * W3s x[t]).
+ *
+ *   d          hidden = H, inter = the shared expert's width I_s,
+ *              n_experts = 1, top_k = 1
+ *   x          bf16 [T, H]
+ *   w13, w2    bf16 [2 I_s, H] (gate rows, then up rows) and [H, I_s], in
+ *              `layout` (SW_LAYOUT_TILED: packed by sw_moe_pack_experts with
+ *              n_experts = 1)
+ *   gate_w     fp32 [H], 16-byte aligned
+ *   out        fp32 [T, H], read and written (the routed layer output)
+ *   workspace  >= sw_moe_shared_workspace_bytes(d, T) bytes, 16-byte aligned
+ * Calls that share `out` or `workspace` must be ordered on one stream.
+ */
+sw_status sw_moe_shared_expert(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                               const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                               const float* gate_w, float* out, void* workspace,
+                               size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

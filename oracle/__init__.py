@@ -12,4 +12,5 @@ from .oracle import (  # noqa: F401
     lib_path,
     prune_compact,
     route,
+    shared_expert,
 )

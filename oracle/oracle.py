@@ -48,6 +48,7 @@ def _load():
         lib.swo_dispatch.argtypes = [I, I, P, I, P, P, P, P, P]
         lib.swo_forward.argtypes = [I, I, I, I, P, I, P, P, P, P, P]
         lib.swo_forward_f64.argtypes = [I, I, I, I, P, I, P, P, P, P, P]
+        lib.swo_shared_expert.argtypes = [I, I, P, I, P, P, P, P]
         for f in (lib.swo_prune_compact, lib.swo_route, lib.swo_dispatch,
                   lib.swo_forward, lib.swo_forward_f64):
             f.restype = ctypes.c_int
@@ -173,6 +174,22 @@ def forward(x, w13, w2, topk_ids, topk_w):
 def forward_f64(x, w13, w2, topk_ids, topk_w):
     """The same computation accumulated in fp64 (error shadow)."""
     return _forward(_load().swo_forward_f64, np.float64, x, w13, w2, topk_ids, topk_w)
+
+
+def shared_expert(x, w13s, w2s, gate_w, out=None):
+    """Section 3.3: out + sigmoid(gate_w . x) * SwiGLU_s(x) per token (out
+    defaults to zeros); returns the new output."""
+    lib = _load()
+    x = _c(x, np.uint16)
+    w13s = _c(w13s, np.uint16)
+    w2s = _c(w2s, np.uint16)
+    gate_w = _c(gate_w, np.float32)
+    t, hidden = x.shape
+    inter = w2s.shape[-1]
+    res = np.zeros((t, hidden), np.float32) if out is None else np.array(out, np.float32, copy=True)
+    rc = lib.swo_shared_expert(hidden, inter, _p(x), t, _p(w13s), _p(w2s), _p(gate_w), _p(res))
+    _check(rc, "shared_expert")
+    return res
 
 
 def layer(x, wr, w13, w2, top_k, keep_mask=None, bias=None):

@@ -278,3 +278,45 @@ int swo_forward_f64(int hidden, int inter, int n_experts, int top_k,
   }
   return 0;
 }
+
+/* Section 3.3 (the distilled pruned decoder keeps an always-on shared expert
+ * behind a sigmoid gate; the frozen expert SE1 and the added SE2, whose down
+ * projection starts at zero, share that gate, so their concatenation is one
+ * expert of twice the intermediate width).  For every token,
+ *   out[t] += sigmoid(gate_w . x[t]) * W2s (silu(W1s x[t]) * W3s x[t]),
+ * with W13s = [W1s; W3s] ([2I, H], gate rows first) and W2s = [H, I].  The
+ * gate's dot product and every contraction accumulate in ascending index
+ * order in fp32; the shared term is added to out after the routed sum. */
+int swo_shared_expert(int hidden, int inter, const uint16_t* x, int n_tokens,
+                      const uint16_t* w13, const uint16_t* w2, const float* gate_w,
+                      float* out) {
+  if (hidden <= 0 || inter <= 0 || n_tokens < 0) return -1;
+  if (n_tokens > 0 && (!x || !w13 || !w2 || !gate_w || !out)) return -1;
+  const size_t H = (size_t)hidden, I = (size_t)inter;
+  const uint16_t* gate = w13;
+  const uint16_t* up = w13 + I * H;
+  float a[inter];
+  for (int t = 0; t < n_tokens; ++t) {
+    const uint16_t* xt = x + (size_t)t * H;
+    float* ot = out + (size_t)t * H;
+    float z = 0.0f;
+    for (size_t h = 0; h < H; ++h) z += gate_w[h] * widen_bf16(xt[h]);
+    const float s = 1.0f / (1.0f + expf(-z));
+    for (size_t i = 0; i < I; ++i) {
+      float g = 0.0f, u = 0.0f;
+      for (size_t h = 0; h < H; ++h) {
+        const float xv = widen_bf16(xt[h]);
+        g += widen_bf16(gate[i * H + h]) * xv;
+        u += widen_bf16(up[i * H + h]) * xv;
+      }
+      a[i] = swiglu_f32(g, u);
+    }
+    for (size_t o = 0; o < H; ++o) {
+      float y = 0.0f;
+      for (size_t i = 0; i < I; ++i) y += widen_bf16(w2[o * I + i]) * a[i];
+      ot[o] += s * y;
+    }
+  }
+  return 0;
+}
+

@@ -80,6 +80,14 @@ int swo_forward_f64(int hidden, int inter, int n_experts, int top_k,
                     const uint16_t* w2, const int32_t* topk_ids,
                     const float* topk_w, double* out);
 
+/* Section 3.3: the always-on shared expert behind a sigmoid gate, added to
+ * the layer output: for every token,
+ *   out[t] += sigmoid(gate_w . x_t) * W2s (silu(W1s x_t) * W3s x_t),
+ * W13s = [2I, H] (gate rows first), W2s = [H, I], gate_w fp32 [H]. */
+int swo_shared_expert(int hidden, int inter, const uint16_t* x, int n_tokens,
+                      const uint16_t* w13, const uint16_t* w2, const float* gate_w,
+                      float* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -260,6 +260,32 @@ sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const f
                                      d->n_experts, d->top_k, workspace, as_stream(stream)));
 }
 
+size_t sw_moe_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
+  if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
+  return sw::shared_workspace_bytes(n_tokens, d->hidden, d->inter);
+}
+
+sw_status sw_moe_shared_expert(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                               const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                               const float* gate_w, float* out, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  SW_TRY(check_dims(d));
+  if (d->n_experts != 1 || d->top_k != 1) return SW_ERR_SHAPE;
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0) return SW_OK;
+  SW_TRY(check_layout(d, n_tokens, layout));
+  if (!x || !w13 || !w2 || !gate_w || !out || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(gate_w) ||
+      !aligned16(out) || !aligned16(workspace))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::shared_workspace_bytes(n_tokens, d->hidden, d->inter))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_shared_expert(x, n_tokens, w13, w2, layout == SW_LAYOUT_TILED, gate_w,
+                                           out, d->hidden, d->inter, workspace,
+                                           as_stream(stream)));
+}
+
 sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
                          const uint16_t* w13, const uint16_t* w2, int32_t layout,
                          const float* topk_w, const int32_t* counts, const int32_t* offsets,

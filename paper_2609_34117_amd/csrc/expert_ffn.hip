@@ -776,6 +776,10 @@ int round8(long v) { return (int)align_up((size_t)v, 8); }
 
 }  // namespace
 
+const float* forward_y(const void* workspace, int T, int H, int I, int k) {
+  return carve(const_cast<void*>(workspace), T * k, H, I).y;
+}
+
 size_t forward_workspace_bytes(int T, int H, int I, int k) {
   if (T <= 0) return 0;
   const int n_pairs = T * k;

@@ -409,8 +409,9 @@ int prefill_grid() {
 }  // namespace
 
 bool prefill_supported(int T, int H, int I, int m, int k) {
-  // about 48 or more tokens per expert, whole K chunks, and 32-bit offsets
-  return (int64_t)T * k >= (int64_t)48 * m && H % kGuKc == 0 && I % kDnKc == 0 &&
+  // about 48 or more tokens per expert over a pool large enough to spread
+  // its units over the chip, whole K chunks, and 32-bit offsets
+  return m >= 16 && (int64_t)T * k >= (int64_t)48 * m && H % kGuKc == 0 && I % kDnKc == 0 &&
          H <= 32768 && 4 * (int64_t)T * k * H < ((int64_t)1 << 31);
 }
 

@@ -17,6 +17,12 @@ constexpr int kMaxStreamI = 1024;
 
 size_t route_workspace_bytes(int T, int H, int m);
 size_t forward_workspace_bytes(int T, int H, int I, int k);
+// y [T*k, H] fp32 inside a forward workspace
+const float* forward_y(const void* workspace, int T, int H, int I, int k = 1);
+size_t shared_workspace_bytes(int T, int H, int I);
+hipError_t launch_shared_expert(const uint16_t* x, int T, const uint16_t* w13, const uint16_t* w2,
+                                bool tiled, const float* gate_w, float* out, int H, int I,
+                                void* workspace, hipStream_t stream);
 
 hipError_t launch_prune_select(const float* importance, int m, int n_keep, int32_t* kept,
                                int32_t* remap, uint8_t* keep_mask, hipStream_t stream);

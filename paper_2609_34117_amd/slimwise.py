@@ -50,6 +50,8 @@ def _load() -> ctypes.CDLL:
         "sw_moe_forward_gate_up": ([D, P, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_down": ([D, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_shared_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_shared_expert": ([D, P, I32, P, P, I32, P, P, P, SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -60,7 +62,7 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 3
+ABI_VERSION = 4
 ROW_MAJOR, TILED = 0, 1
 if LIB.sw_abi_version() != ABI_VERSION:
     raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
@@ -296,6 +298,28 @@ def sw_moe_forward_combine(topk_w, hidden, inter, n_experts, plan: Plan, out, ws
                                     _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
                                     _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "sw_moe_forward_combine")
+
+
+def sw_moe_shared_workspace_bytes(d: Dims, n_tokens: int) -> int:
+    return LIB.sw_moe_shared_workspace_bytes(ctypes.byref(d), n_tokens)
+
+
+def sw_moe_shared_expert(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+                         gate_w: torch.Tensor, out: torch.Tensor, *, layout: int = ROW_MAJOR,
+                         ws=None, stream=None) -> torch.Tensor:
+    """Section 3.3: out += sigmoid(gate_w . x) * SwiGLU_s(x) (in place)."""
+    t, hidden = x.shape
+    two_i = w13.shape[-2]
+    d = Dims(hidden, two_i // 2, 1, 1)
+    if ws is None:
+        ws = workspace(sw_moe_shared_workspace_bytes(d, t), x.device)
+    st = LIB.sw_moe_shared_expert(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
+                                  _ptr(w2, _BF16, "w2"), layout,
+                                  _ptr(gate_w, (torch.float32,), "gate_w"),
+                                  _ptr(out, (torch.float32,), "out"), _ptr(ws), ws.numel(),
+                                  _stream(stream))
+    _check(st, "sw_moe_shared_expert")
+    return out
 
 
 def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, layout: int = ROW_MAJOR,

@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 3
+    assert lib.sw_abi_version() == 4
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -84,7 +84,8 @@ def test_route_validation_precedes_any_launch(lib):
 
 def test_workspace_queries(lib):
     P = ctypes.POINTER(Dims)
-    for name in ("sw_moe_route_workspace_bytes", "sw_moe_forward_workspace_bytes"):
+    for name in ("sw_moe_route_workspace_bytes", "sw_moe_forward_workspace_bytes",
+                 "sw_moe_shared_workspace_bytes"):
         f = getattr(lib, name)
         f.argtypes = [P, ctypes.c_int32]
         f.restype = ctypes.c_size_t
@@ -141,6 +142,32 @@ def test_route_dispatch_validation(lib):
     assert call(p=18) == SW_ERR_ALIGN
     assert call(na=2) == SW_ERR_ALIGN
     assert call(nbytes=16) == SW_ERR_WORKSPACE
+
+
+def test_shared_expert_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.sw_moe_shared_expert
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P,
+                  ctypes.c_size_t, P]
+    d = Dims(64, 32, 1, 1)
+    q = lib.sw_moe_shared_workspace_bytes
+    q.argtypes = [ctypes.POINTER(Dims), ctypes.c_int32]
+    q.restype = ctypes.c_size_t
+    need = q(ctypes.byref(d), 4)
+    assert need > 0
+
+    def call(dims=d, nbytes=need, lay=0, **kw):
+        a = dict(dict(x=16, w13=16, w2=16, g=16, out=16, ws=16), **kw)
+        return f(ctypes.byref(dims), a["x"], 4, a["w13"], a["w2"], lay, a["g"], a["out"], a["ws"],
+                 nbytes, None)
+
+    assert call(dims=Dims(64, 32, 2, 1)) == SW_ERR_SHAPE   # one expert, top-1
+    assert call(dims=Dims(64, 32, 1, 2)) == SW_ERR_SHAPE
+    assert call(g=None) == SW_ERR_NULL
+    assert call(out=None) == SW_ERR_NULL
+    assert call(g=24) == SW_ERR_ALIGN
+    assert call(nbytes=need - 1) == SW_ERR_WORKSPACE
+    assert call(lay=3) == SW_ERR_SHAPE
 
 
 def test_forward_validation(lib):

@@ -483,3 +483,45 @@ def test_route_dispatch_in_band_errors_and_empty_batch(sw):
     assert ids.shape == (0, 3)
     assert int(plan.n_active.item()) == 0
     assert torch.all(plan.counts == 0) and torch.all(plan.offsets == 0)
+
+
+# --------------------------------------------------------------------------
+# the shared expert (Section 3.3)
+
+def _shared_inputs(hidden, inter, tokens, seed):
+    g = np.random.default_rng([301, seed])
+    x = I.to_bf16_bits(g.standard_normal((tokens, hidden), dtype=np.float32))
+    w13 = I.to_bf16_bits(0.02 * g.standard_normal((2 * inter, hidden), dtype=np.float32))
+    w2 = I.to_bf16_bits(0.02 * g.standard_normal((hidden, inter), dtype=np.float32))
+    gate = (0.05 * g.standard_normal(hidden)).astype(np.float32)
+    base = g.standard_normal((tokens, hidden)).astype(np.float32)
+    return x, w13, w2, gate, base
+
+
+@pytest.mark.parametrize("hidden,inter,tokens", [(256, 128, 8), (2048, 1024, 64), (2048, 1024, 1),
+                                                 (512, 256, 200)])
+def test_shared_expert_parity(sw, hidden, inter, tokens):
+    x, w13, w2, gate, base = _shared_inputs(hidden, inter, tokens, hidden + tokens)
+    out = dev(base)
+    sw.sw_moe_shared_expert(dev(x), dev(w13[None]), dev(w2[None]), dev(gate), out)
+    want = oracle.shared_expert(x, w13, w2, gate, out=base)
+    err, rel = compare_out(host(out) - base, want - base, "shared expert term")
+    print(f"shared H={hidden} I_s={inter} T={tokens}: max|err|={err:.3g} rel={rel:.3g}")
+    if hidden <= 2048 and inter <= 1024:
+        t13, t2 = sw.sw_moe_pack_experts(dev(w13[None]), dev(w2[None]))
+        out_t = dev(base)
+        sw.sw_moe_shared_expert(dev(x), t13, t2, dev(gate), out_t, layout=sw.TILED)
+        assert torch.equal(out_t, out)
+
+
+def test_shared_expert_zero_initialised_se2_is_se1_bit_for_bit(sw):
+    x, w13a, w2a, gate, base = _shared_inputs(512, 128, 16, 5)
+    _, w13b, _, _, _ = _shared_inputs(512, 128, 16, 6)
+    i = 128
+    w13 = np.concatenate([w13a[:i], w13b[:i], w13a[i:], w13b[i:]])
+    w2 = np.concatenate([w2a, np.zeros_like(w2a)], axis=1)
+    one = dev(base)
+    sw.sw_moe_shared_expert(dev(x), dev(w13a[None]), dev(w2a[None]), dev(gate), one)
+    merged = dev(base)
+    sw.sw_moe_shared_expert(dev(x), dev(w13[None]), dev(w2[None]), dev(gate), merged)
+    assert torch.equal(one, merged)

@@ -15,7 +15,7 @@ import oracle.oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PIN_TESTS = ["tests/test_oracle_route.py", "tests/test_oracle_dispatch_prune.py",
-             "tests/test_oracle_forward.py"]
+             "tests/test_oracle_forward.py", "tests/test_oracle_shared.py"]
 
 # (name, original text, mutated text); every occurrence is replaced.
 MUTANTS = [
@@ -51,6 +51,10 @@ MUTANTS = [
     ("compact_wrong_rows", "memcpy(w13_c + ci * 2 * in * h, w13 + e * 2 * in * h",
      "memcpy(w13_c + ci * 2 * in * h, w13 + ci * 2 * in * h"),
     ("bf16_widen_wrong_shift", "((uint32_t)bits) << 16", "((uint32_t)bits) << 15"),
+    ("shared_gate_sign", "const float s = 1.0f / (1.0f + expf(-z));",
+     "const float s = 1.0f / (1.0f + expf(z));"),
+    ("shared_overwrites", "ot[o] += s * y;", "ot[o] = s * y;"),
+    ("shared_up_is_gate", "const uint16_t* up = w13 + I * H;", "const uint16_t* up = w13;"),
 ]
 
 
