@@ -17,6 +17,13 @@ Workloads (the default line is decode_b64):
                 50 and 75% pruning (unique expert bytes per step next to
                 Eq. 1's expectation); `value` is batch 64 at 50%.
   prefill       the same layer shape, 4096 tokens through the full pool.
+  decode_shared the decode sweep's layer at batch 64 with the shared expert of
+                the distilled pruned decoder (width 2 I, sigmoid gate), 0 and
+                50% pruning, each with and without the shared expert.
+  colocated     one resident full pool (the decode sweep's layer): an
+                unmasked 4096-token prefill forward, and batch-64 decode with
+                the 50% router mask, next to decode on the compacted pool
+                (the mask's cost).
   skewed_stack  40 such layers at batch 256 with a Zipf(1.1) router bias per
                 layer (60 GiB of experts, drawn on the device), the full
                 stack and the 50% pruned one (top 128 experts by
@@ -77,7 +84,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="decode_b64",
-                    choices=["decode_b64", "decode_sweep", "prefill", "skewed_stack"])
+                    choices=["decode_b64", "decode_sweep", "prefill", "skewed_stack",
+                             "decode_shared", "colocated"])
     ap.add_argument("--sweep-steps", type=int, default=50,
                     help="timed steps per (batch, pruning) point of decode_sweep")
     ap.add_argument("--batch", type=int, default=None)
@@ -91,13 +99,15 @@ def parse():
 class Pool:
     """One expert pool (full or compacted) resident on the device, N_COPIES times."""
 
-    def __init__(self, w13, w2, wr, layout, bias=None):
+    def __init__(self, w13, w2, wr, layout, bias=None, shared=None):
         self.w13 = [w13] + [w13.clone() for _ in range(N_COPIES - 1)]
         self.w2 = [w2] + [w2.clone() for _ in range(N_COPIES - 1)]
         self.wr = wr
         self.bias = bias
         self.layout = layout
         self.m = wr.shape[0]
+        self.shared = shared  # (w13_s, w2_s, gate_w) of the shared expert, or None
+        self.keep_mask = None  # router mask over this pool (colocated decode), or None
 
 
 class Runner:
@@ -114,22 +124,28 @@ class Runner:
         d = sw.dims(H, Iw, pool.m, k)
         self.rws = sw.workspace(sw.sw_moe_route_workspace_bytes(d, T), dev)
         self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(d, T), dev)
+        self.sws = None
+        if pool.shared is not None:
+            ds = sw.dims(H, pool.shared[1].shape[-1], 1, 1)
+            self.sws = sw.workspace(sw.sw_moe_shared_workspace_bytes(ds, T), dev)
 
     def plan_for(self, x):
         """A dispatch plan of its own for batch `x` (route + dispatch)."""
         sw, p = self.sw, self.pool
         plan = sw.alloc_plan(self.T, p.m, self.cfg.top_k, x.device)
-        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias,
+        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
                                  out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
         return plan
 
     def step(self, x, c, ev=None):
         sw, p = self.sw, self.pool
-        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias,
+        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
                                  out=(self.ids, self.w, self.gap), plan=self.plan, ws=self.rws)
         if ev is None:
             sw.sw_moe_forward(x, p.w13[c], p.w2[c], self.w, self.plan, layout=p.layout,
                               out=self.out, ws=self.fws)
+            if p.shared is not None:
+                sw.sw_moe_shared_expert(x, *p.shared, self.out, layout=p.layout, ws=self.sws)
             return
         ev[0].record()
         sw.sw_moe_forward_gate_up(x, p.w13[c], self.cfg.top_k, self.plan, self.fws, layout=p.layout)
@@ -417,6 +433,95 @@ def run_prefill(args, sw, torch, dev):
     return line
 
 
+def run_decode_shared(args, sw, torch, dev):
+    import copy
+
+    cfg = I.CONFIGS["decode_sweep"]
+    T, H, Iw = 64, cfg.hidden, cfg.inter
+    Is = 2 * Iw  # the distilled decoder's shared expert: twice the original width
+    L = I.make_layer(cfg)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    pools = build_pools(sw, torch, cfg, L, (0.5, 0.0), layout, dev)
+    g = np.random.default_rng([cfg.config_id, 0, 6])
+    w13s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((1, 2 * Is, H), dtype=np.float32))
+    w2s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((1, H, Is), dtype=np.float32))
+    gate_w = (cfg.wr_std * g.standard_normal(H)).astype(np.float32)
+    w13s_d, w2s_d = up(torch, dev, w13s), up(torch, dev, w2s)
+    if layout == sw.TILED:
+        w13s_d, w2s_d = sw.sw_moe_pack_experts(w13s_d, w2s_d)
+    shared = (w13s_d, w2s_d, up(torch, dev, gate_w))
+    xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
+    res = {}
+    for p in (0.5, 0.0):
+        res[(p, False)] = measure(sw, torch, pools[p], cfg, T, xs, args.steps, args.warmup, dev)
+        with_se = copy.copy(pools[p])
+        with_se.shared = shared
+        res[(p, True)] = measure(sw, torch, with_se, cfg, T, xs, args.steps, args.warmup, dev)
+    head = res[(0.5, True)]
+    line = base_line(args, cfg, T, head["tokens_per_s"], head["t_step_us"], args.steps)
+    line["config"] = {
+        "workload": f"decode_shared: decode MoE layer H {H}, {cfg.n_experts} experts, top-{cfg.top_k}, "
+                    f"I {Iw}, batch {T}, 50% pruned ({cfg.n_keep(0.5)} kept, compacted) plus a shared "
+                    f"expert of width {Is} behind a sigmoid gate",
+        "hidden": H, "n_experts": cfg.n_experts, "n_kept": cfg.n_keep(0.5), "top_k": cfg.top_k,
+        "inter": Iw, "shared_inter": Is, "batch": T, "pruning": 0.5, "weight_layout": args.layout,
+        "parallelism": "none (1 GPU)",
+    }
+    line["roofline"] = hbm_roofline(cfg, T, 0.5, args.layout, res[(0.5, True)])
+    shared_bytes = 3 * H * Is * 2
+    line["detail"] = {
+        f"{int(p * 100)}%{' + shared' if s else ''}": rounded(v) for (p, s), v in res.items()}
+    line["detail"]["shared_expert_us"] = {
+        f"{int(p * 100)}%": round(res[(p, True)]["t_step_us"] - res[(p, False)]["t_step_us"], 3)
+        for p in (0.5, 0.0)}
+    line["detail"]["shared_expert_MiB"] = shared_bytes / 2 ** 20
+    line["detail"]["speedup_pruned_vs_full_with_shared"] = round(
+        res[(0.0, True)]["t_step_us"] / res[(0.5, True)]["t_step_us"], 3)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, L, 0.5, args.cpu_seconds, T)
+    return line
+
+
+def run_colocated(args, sw, torch, dev):
+    import copy
+
+    cfg = I.CONFIGS["decode_sweep"]
+    T, H, Iw, m, k = 64, cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k
+    L = I.make_layer(cfg)
+    layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
+    pools = build_pools(sw, torch, cfg, L, (0.5, 0.0), layout, dev)
+    n_keep = cfg.n_keep(0.5)
+    mask = sw.sw_moe_prune_compact(up(torch, dev, L["importance"]), n_keep, k, hidden=H,
+                                   compact=False)["keep_mask"]
+    masked = copy.copy(pools[0.0])
+    masked.keep_mask = mask
+    xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
+    sm = measure(sw, torch, masked, cfg, T, xs, args.steps, args.warmup, dev)
+    sc = measure(sw, torch, pools[0.5], cfg, T, xs, args.steps, args.warmup, dev)
+    sf = measure(sw, torch, pools[0.0], cfg, T, xs, args.steps, args.warmup, dev)
+    # the prefill phase on the same resident pool, no mask
+    xp = [up(torch, dev, I.make_x(I.CONFIGS["prefill"], rep=r)) for r in range(2)]
+    sp = measure(sw, torch, pools[0.0], cfg, 4096, xp, 10, 2, dev)
+    line = base_line(args, cfg, T, sm["tokens_per_s"], sm["t_step_us"], args.steps)
+    line["config"] = {
+        "workload": f"colocated: one resident pool of {m} experts (H {H}, top-{k}, I {Iw}); decode "
+                    f"batch {T} with the 50% router mask ({n_keep} eligible), prefill 4096 tokens "
+                    f"unmasked",
+        "hidden": H, "n_experts": m, "n_kept": n_keep, "top_k": k, "inter": Iw, "batch": T,
+        "pruning": 0.5, "weight_layout": args.layout, "parallelism": "none (1 GPU)",
+    }
+    line["roofline"] = hbm_roofline(cfg, T, 0.5, args.layout, sm)
+    line["detail"] = {
+        "masked_full_pool": rounded(sm), "compacted_pool": rounded(sc), "unmasked_full_pool": rounded(sf),
+        "prefill_unmasked_4096": rounded(sp),
+        "mask_overhead_us_per_layer": round(sm["t_step_us"] - sc["t_step_us"], 3),
+        "speedup_masked_vs_full": round(sf["t_step_us"] / sm["t_step_us"], 3),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, L, 0.5, args.cpu_seconds, T)
+    return line
+
+
 def run_skewed_stack(args, sw, torch, dev):
     import oracle
     from paper_2609_34117_amd import gen
@@ -553,7 +658,8 @@ def main():
 
     dev = torch.device("cuda:0")
     run = {"decode_b64": run_decode_b64, "decode_sweep": run_decode_sweep,
-           "prefill": run_prefill, "skewed_stack": run_skewed_stack}[args.workload]
+           "prefill": run_prefill, "skewed_stack": run_skewed_stack,
+           "decode_shared": run_decode_shared, "colocated": run_colocated}[args.workload]
     print(json.dumps(run(args, sw, torch, dev)), flush=True)
 
 
