@@ -74,7 +74,7 @@ typedef struct {
 const char* sw_status_str(int status);
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 4
+#define SW_ABI_VERSION 5
 int32_t sw_abi_version(void);
 
 /*
@@ -234,6 +234,35 @@ sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint
 sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
                                  const int32_t* n_active, float* out, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/* Workspace bytes sw_moe_routing_mass needs for T tokens (0 if T == 0). */
+size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
+
+/*
+ * Routing-mass statistics of a batch of calibration tokens (Section 2.3:
+ * the routing-mass importance criterion aggregates the router's gate
+ * probabilities), accumulated into the caller's arrays:
+ *   mass_softmax[e] += sum_t softmax(z_t)[e], over the eligible experts'
+ *                      logits z_t = wr . x_t (+ bias);
+ *   mass_topk[e]    += sum of the renormalised gates e receives as one of a
+ *                      token's top-k (sw_moe_route's selection).
+ * Pruning then keeps the experts with the largest mass (pass it as the
+ * importance of sw_moe_prune_compact).  Masked experts receive nothing.
+ *
+ *   d                hidden, n_experts = m, top_k (inter is not used)
+ *   x, wr, bias,     as for sw_moe_route
+ *   keep_mask
+ *   mass_softmax,    nullable fp32 [m] each, read and written
+ *   mass_topk
+ *   workspace        >= sw_moe_routing_mass_workspace_bytes(d, T) bytes,
+ *                    16-byte aligned
+ * In-band error: if fewer than k experts are eligible, mass_topk is left
+ * unchanged (mass_softmax is still accumulated).
+ */
+sw_status sw_moe_routing_mass(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                              const float* wr, const float* bias, const uint8_t* keep_mask,
+                              float* mass_softmax, float* mass_topk, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* Workspace bytes sw_moe_shared_expert needs for T tokens (0 if T == 0). */
 size_t sw_moe_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);

@@ -12,5 +12,6 @@ from .oracle import (  # noqa: F401
     lib_path,
     prune_compact,
     route,
+    routing_mass,
     shared_expert,
 )

@@ -49,6 +49,7 @@ def _load():
         lib.swo_forward.argtypes = [I, I, I, I, P, I, P, P, P, P, P]
         lib.swo_forward_f64.argtypes = [I, I, I, I, P, I, P, P, P, P, P]
         lib.swo_shared_expert.argtypes = [I, I, P, I, P, P, P, P]
+        lib.swo_routing_mass.argtypes = [I, I, I, P, I, P, P, P, P, P]
         for f in (lib.swo_prune_compact, lib.swo_route, lib.swo_dispatch,
                   lib.swo_forward, lib.swo_forward_f64):
             f.restype = ctypes.c_int
@@ -190,6 +191,24 @@ def shared_expert(x, w13s, w2s, gate_w, out=None):
     rc = lib.swo_shared_expert(hidden, inter, _p(x), t, _p(w13s), _p(w2s), _p(gate_w), _p(res))
     _check(rc, "shared_expert")
     return res
+
+
+def routing_mass(x, wr, top_k, keep_mask=None, bias=None, mass=None):
+    """Section 2.3: (mass_softmax, mass_topk) accumulated over the tokens of
+    x, onto `mass` (a pair of [m] arrays) if given."""
+    lib = _load()
+    x = _c(x, np.uint16)
+    wr = _c(wr, np.float32)
+    t, hidden = x.shape
+    m = wr.shape[0]
+    keep_mask = _c(keep_mask, np.uint8)
+    bias = _c(bias, np.float32)
+    ms, mt = ((np.zeros(m, np.float32), np.zeros(m, np.float32)) if mass is None else
+              (np.array(mass[0], np.float32, copy=True), np.array(mass[1], np.float32, copy=True)))
+    rc = lib.swo_routing_mass(hidden, m, top_k, _p(x), t, _p(wr), _p(bias), _p(keep_mask),
+                              _p(ms), _p(mt))
+    _check(rc, "routing_mass")
+    return ms, mt
 
 
 def layer(x, wr, w13, w2, top_k, keep_mask=None, bias=None):

@@ -24,6 +24,7 @@
 
 #include <math.h>
 #include <stddef.h>
+#include <stdlib.h>
 #include <string.h>
 
 /* A bf16 value is the top 16 bits of an IEEE fp32 value: widening is exact. */
@@ -318,5 +319,49 @@ int swo_shared_expert(int hidden, int inter, const uint16_t* x, int n_tokens,
     }
   }
   return 0;
+}
+
+/* Section 2.3 (importance criteria computed from calibration tokens; the
+ * routing-mass criterion aggregates the router's gate probabilities).  Two
+ * aggregates are accumulated into the caller's arrays, token by token in
+ * ascending order:
+ *   mass_softmax[e] += softmax(z_t)[e], the softmax over the eligible
+ *                      experts' logits (masked experts receive nothing);
+ *   mass_topk[e]    += the renormalised gate expert e receives among the
+ *                      token's top-k (slot order), as routed by swo_route.
+ * Either may be NULL. */
+int swo_routing_mass(int hidden, int n_experts, int top_k, const uint16_t* x, int n_tokens,
+                     const float* wr, const float* bias, const uint8_t* keep_mask,
+                     float* mass_softmax, float* mass_topk) {
+  if (hidden <= 0 || n_experts <= 0 || top_k <= 0 || n_tokens < 0) return -1;
+  if (n_tokens == 0) return 0;
+  const size_t T = (size_t)n_tokens, m = (size_t)n_experts, k = (size_t)top_k;
+  float* z = (float*)malloc(T * m * sizeof(float));
+  int32_t* ids = (int32_t*)malloc(T * k * sizeof(int32_t));
+  float* w = (float*)malloc(T * k * sizeof(float));
+  int rc = (z && ids && w) ? 0 : -1;
+  if (rc == 0)
+    rc = swo_route(hidden, n_experts, top_k, x, n_tokens, wr, bias, keep_mask, ids, w, NULL, z);
+  if (rc == 0) {
+    for (size_t t = 0; t < T; ++t) {
+      const float* zt = z + t * m;
+      if (mass_softmax) {
+        float zmax = -INFINITY;
+        for (size_t e = 0; e < m; ++e)
+          if ((!keep_mask || keep_mask[e]) && zt[e] > zmax) zmax = zt[e];
+        float denom = 0.0f;
+        for (size_t e = 0; e < m; ++e)
+          if (!keep_mask || keep_mask[e]) denom += expf(zt[e] - zmax);
+        for (size_t e = 0; e < m; ++e)
+          if (!keep_mask || keep_mask[e]) mass_softmax[e] += expf(zt[e] - zmax) / denom;
+      }
+      if (mass_topk)
+        for (size_t j = 0; j < k; ++j) mass_topk[ids[t * k + j]] += w[t * k + j];
+    }
+  }
+  free(z);
+  free(ids);
+  free(w);
+  return rc;
 }
 

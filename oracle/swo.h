@@ -88,6 +88,14 @@ int swo_shared_expert(int hidden, int inter, const uint16_t* x, int n_tokens,
                       const uint16_t* w13, const uint16_t* w2, const float* gate_w,
                       float* out);
 
+/* Section 2.3: the routing-mass statistics of a batch of calibration
+ * tokens, accumulated into mass_softmax[m] (softmax over the eligible
+ * experts' logits) and mass_topk[m] (renormalised top-k gates); either may
+ * be NULL. */
+int swo_routing_mass(int hidden, int n_experts, int top_k, const uint16_t* x, int n_tokens,
+                     const float* wr, const float* bias, const uint8_t* keep_mask,
+                     float* mass_softmax, float* mass_topk);
+
 #ifdef __cplusplus
 }
 #endif

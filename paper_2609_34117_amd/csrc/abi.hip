@@ -260,6 +260,31 @@ sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const f
                                      d->n_experts, d->top_k, workspace, as_stream(stream)));
 }
 
+size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
+  if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
+  return sw::routing_mass_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k);
+}
+
+sw_status sw_moe_routing_mass(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                              const float* wr, const float* bias, const uint8_t* keep_mask,
+                              float* mass_softmax, float* mass_topk, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0 || (!mass_softmax && !mass_topk)) return SW_OK;
+  if (!x || !wr || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || (bias && !aligned4(bias)) ||
+      (mass_softmax && !aligned4(mass_softmax)) || (mass_topk && !aligned4(mass_topk)))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes <
+      sw::routing_mass_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_routing_mass(x, n_tokens, wr, bias, keep_mask, d->hidden,
+                                          d->n_experts, d->top_k, mass_softmax, mass_topk,
+                                          workspace, as_stream(stream)));
+}
+
 size_t sw_moe_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
   if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
   return sw::shared_workspace_bytes(n_tokens, d->hidden, d->inter);

@@ -363,7 +363,123 @@ void launch_topk(const float* part, int KS, const float* bias, const uint8_t* ke
     launch_topk_t<16, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Routing-mass statistics (Section 2.3: an importance criterion aggregating
+// the router's gate probabilities over calibration tokens).
+
+// Token t's logit for expert e: the KS partials in slice order, plus bias.
+__device__ __forceinline__ float logit_value(const float* __restrict__ part, int KS, int T, int m,
+                                             int t, int e, const float* __restrict__ bias) {
+  const float* p = part + (size_t)t * m + e;
+  const size_t plane = (size_t)T * m;
+  float z = p[0];
+  for (int ks = 1; ks < KS; ++ks) z += p[ks * plane];
+  if (bias != nullptr) z += bias[e];
+  return z;
+}
+
+// One wave per token: the largest eligible logit and the softmax
+// denominator over the eligible experts.
+__global__ __launch_bounds__(256) void mass_token_stats_kernel(
+    const float* __restrict__ part, int KS, const float* __restrict__ bias,
+    const uint8_t* __restrict__ keep_mask, int T, int m, float* __restrict__ zmax,
+    float* __restrict__ denom) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= T) return;  // wave-uniform
+  uint32_t best = 0u;  // order key; 0 = no eligible expert on this lane
+  for (int e = lane; e < m; e += kWave)
+    if (keep_mask == nullptr || keep_mask[e] != 0)
+      best = max(best, max(f32_order_key(logit_value(part, KS, T, m, t, e, bias)), 1u));
+  best = wave_max_u32(best);
+  const float zm = f32_from_order_key(best);
+  float s = 0.f;
+  for (int e = lane; e < m; e += kWave)
+    if (keep_mask == nullptr || keep_mask[e] != 0)
+      s += expf(logit_value(part, KS, T, m, t, e, bias) - zm);
+  s = wave_sum_f32(s);
+  if (lane == 0) {
+    zmax[t] = zm;
+    denom[t] = s;
+  }
+}
+
+// One thread per expert: the token-ordered sum of its softmax share and of
+// the gates it received (its dispatch slots in order), added to the masses.
+__global__ __launch_bounds__(256) void mass_accumulate_kernel(
+    const float* __restrict__ part, int KS, const float* __restrict__ bias,
+    const uint8_t* __restrict__ keep_mask, int T, int m, const float* __restrict__ zmax,
+    const float* __restrict__ denom, const float* __restrict__ topk_w,
+    const int* __restrict__ counts, const int* __restrict__ offsets,
+    const int* __restrict__ perm, const int* __restrict__ n_active, int n_pairs,
+    float* __restrict__ mass_softmax, float* __restrict__ mass_topk) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= m) return;
+  if (mass_softmax != nullptr && (keep_mask == nullptr || keep_mask[e] != 0)) {
+    float acc = 0.f;
+    for (int t = 0; t < T; ++t)
+      acc += expf(logit_value(part, KS, T, m, t, e, bias) - zmax[t]) / denom[t];
+    mass_softmax[e] += acc;
+  }
+  if (mass_topk != nullptr && *n_active >= 0) {
+    const int b = offsets[e], c = counts[e];
+    float acc = 0.f;
+    if (b >= 0 && c >= 0 && c <= n_pairs - b)
+      for (int i = 0; i < c; ++i) {
+        const int p = perm[b + i];
+        if (p >= 0 && p < n_pairs) acc += topk_w[p];
+      }
+    mass_topk[e] += acc;
+  }
+}
+
 }  // namespace
+
+size_t routing_mass_workspace_bytes(int T, int H, int m, int k) {
+  if (T <= 0) return 0;
+  const size_t P = (size_t)T * k;
+  return route_workspace_bytes(T, H, m) + 3 * align_up(P * 4, 256) +
+         3 * align_up((size_t)(m + 1) * 4, 256) + 256 + 2 * align_up((size_t)T * 4, 256);
+}
+
+hipError_t launch_routing_mass(const uint16_t* x, int T, const float* wr, const float* bias,
+                               const uint8_t* keep_mask, int H, int m, int k, float* mass_softmax,
+                               float* mass_topk, void* workspace, hipStream_t stream) {
+  if (T == 0) return hipSuccess;
+  char* p = static_cast<char*>(workspace);
+  const size_t P = (size_t)T * k;
+  float* part = reinterpret_cast<float*>(p);
+  p += route_workspace_bytes(T, H, m);
+  int* ids = reinterpret_cast<int*>(p);
+  p += align_up(P * 4, 256);
+  float* w = reinterpret_cast<float*>(p);
+  p += align_up(P * 4, 256);
+  int* perm = reinterpret_cast<int*>(p);
+  p += align_up(P * 4, 256);
+  int* counts = reinterpret_cast<int*>(p);
+  p += align_up((size_t)(m + 1) * 4, 256);
+  int* offsets = reinterpret_cast<int*>(p);
+  p += align_up((size_t)(m + 1) * 4, 256);
+  int* active = reinterpret_cast<int*>(p);
+  p += align_up((size_t)(m + 1) * 4, 256);
+  int* n_active = reinterpret_cast<int*>(p);
+  p += 256;
+  float* zmax = reinterpret_cast<float*>(p);
+  p += align_up((size_t)T * 4, 256);
+  float* denom = reinterpret_cast<float*>(p);
+  hipError_t err = launch_route_dispatch(x, T, wr, bias, keep_mask, H, m, k, ids, w, nullptr,
+                                         counts, offsets, perm, active, n_active, part, stream);
+  if (err != hipSuccess) return err;
+  const int KS = logits_split(T, H, m).ks;
+  mass_token_stats_kernel<<<(T + 3) / 4, 256, 0, stream>>>(part, KS, bias, keep_mask, T, m, zmax,
+                                                           denom);
+  err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  mass_accumulate_kernel<<<(m + 255) / 256, 256, 0, stream>>>(
+      part, KS, bias, keep_mask, T, m, zmax, denom, w, counts, offsets, perm, n_active,
+      (int)P, mass_softmax, mass_topk);
+  return hipGetLastError();
+}
 
 size_t route_workspace_bytes(int T, int H, int m) {
   if (T <= 0) return 0;

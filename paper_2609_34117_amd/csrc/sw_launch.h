@@ -20,6 +20,10 @@ size_t forward_workspace_bytes(int T, int H, int I, int k);
 // y [T*k, H] fp32 inside a forward workspace
 const float* forward_y(const void* workspace, int T, int H, int I, int k = 1);
 size_t shared_workspace_bytes(int T, int H, int I);
+size_t routing_mass_workspace_bytes(int T, int H, int m, int k);
+hipError_t launch_routing_mass(const uint16_t* x, int T, const float* wr, const float* bias,
+                               const uint8_t* keep_mask, int H, int m, int k, float* mass_softmax,
+                               float* mass_topk, void* workspace, hipStream_t stream);
 hipError_t launch_shared_expert(const uint16_t* x, int T, const uint16_t* w13, const uint16_t* w2,
                                 bool tiled, const float* gate_w, float* out, int H, int I,
                                 void* workspace, hipStream_t stream);

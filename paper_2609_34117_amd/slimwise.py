@@ -51,6 +51,8 @@ def _load() -> ctypes.CDLL:
         "sw_moe_forward_down": ([D, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_shared_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_routing_mass_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_routing_mass": ([D, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_shared_expert": ([D, P, I32, P, P, I32, P, P, P, SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -62,7 +64,7 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 4
+ABI_VERSION = 5
 ROW_MAJOR, TILED = 0, 1
 if LIB.sw_abi_version() != ABI_VERSION:
     raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
@@ -298,6 +300,29 @@ def sw_moe_forward_combine(topk_w, hidden, inter, n_experts, plan: Plan, out, ws
                                     _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
                                     _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "sw_moe_forward_combine")
+
+
+def sw_moe_routing_mass(x: torch.Tensor, wr: torch.Tensor, top_k: int, *, keep_mask=None,
+                        bias=None, mass=None, ws=None, stream=None):
+    """Section 2.3: routing-mass statistics of the tokens of x, accumulated
+    onto `mass` = (mass_softmax, mass_topk) (fp32 [m] device tensors, created
+    as zeros if None); returns the pair."""
+    t, hidden = x.shape
+    m = wr.shape[0]
+    d = Dims(hidden, 8, m, top_k)
+    if mass is None:
+        mass = (torch.zeros(m, dtype=torch.float32, device=x.device),
+                torch.zeros(m, dtype=torch.float32, device=x.device))
+    if ws is None:
+        ws = workspace(LIB.sw_moe_routing_mass_workspace_bytes(ctypes.byref(d), t), x.device)
+    st = LIB.sw_moe_routing_mass(ctypes.byref(d), _ptr(x, _BF16, "x"), t,
+                                 _ptr(wr, (torch.float32,), "wr"), _ptr(bias, (torch.float32,), "bias"),
+                                 _ptr(keep_mask, (torch.uint8,), "keep_mask"),
+                                 _ptr(mass[0], (torch.float32,), "mass_softmax"),
+                                 _ptr(mass[1], (torch.float32,), "mass_topk"), _ptr(ws), ws.numel(),
+                                 _stream(stream))
+    _check(st, "sw_moe_routing_mass")
+    return mass
 
 
 def sw_moe_shared_workspace_bytes(d: Dims, n_tokens: int) -> int:

@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 4
+    assert lib.sw_abi_version() == 5
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -85,7 +85,7 @@ def test_route_validation_precedes_any_launch(lib):
 def test_workspace_queries(lib):
     P = ctypes.POINTER(Dims)
     for name in ("sw_moe_route_workspace_bytes", "sw_moe_forward_workspace_bytes",
-                 "sw_moe_shared_workspace_bytes"):
+                 "sw_moe_shared_workspace_bytes", "sw_moe_routing_mass_workspace_bytes"):
         f = getattr(lib, name)
         f.argtypes = [P, ctypes.c_int32]
         f.restype = ctypes.c_size_t
@@ -141,6 +141,25 @@ def test_route_dispatch_validation(lib):
     assert call(x=24) == SW_ERR_ALIGN
     assert call(p=18) == SW_ERR_ALIGN
     assert call(na=2) == SW_ERR_ALIGN
+    assert call(nbytes=16) == SW_ERR_WORKSPACE
+
+
+def test_routing_mass_validation(lib):
+    P = ctypes.c_void_p
+    f = lib.sw_moe_routing_mass
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, P, P, P, P, ctypes.c_size_t, P]
+    d = Dims(64, 8, 8, 2)
+
+    def call(dims=d, t=4, nbytes=1 << 20, **kw):
+        a = dict(dict(x=16, wr=16, ms=16, mt=16, ws=16), **kw)
+        return f(ctypes.byref(dims), a["x"], t, a["wr"], None, None, a["ms"], a["mt"], a["ws"],
+                 nbytes, None)
+
+    assert call(dims=Dims(64, 8, 8, 9)) == SW_ERR_SHAPE
+    assert call(ms=None, mt=None, x=None) == SW_OK      # nothing to accumulate
+    assert call(x=None) == SW_ERR_NULL
+    assert call(wr=24) == SW_ERR_ALIGN
+    assert call(mt=18) == SW_ERR_ALIGN
     assert call(nbytes=16) == SW_ERR_WORKSPACE
 
 

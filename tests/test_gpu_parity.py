@@ -525,3 +525,32 @@ def test_shared_expert_zero_initialised_se2_is_se1_bit_for_bit(sw):
     merged = dev(base)
     sw.sw_moe_shared_expert(dev(x), dev(w13[None]), dev(w2[None]), dev(gate), merged)
     assert torch.equal(one, merged)
+
+
+# --------------------------------------------------------------------------
+# routing-mass statistics (Section 2.3)
+
+@pytest.mark.parametrize("hidden,m,k,tokens,masked,biased", [
+    (256, 16, 2, 8, False, False),
+    (2048, 64, 8, 64, False, False),
+    (2048, 256, 8, 256, True, True),
+    (512, 300, 8, 40, False, True),     # separate route + dispatch kernels
+    (2048, 256, 8, 1024, False, False),
+])
+def test_routing_mass_parity(sw, hidden, m, k, tokens, masked, biased):
+    cfg, L, D = small_layer(hidden, m, k, 32, tokens, seed=11)
+    mask = mask_for(cfg, L, 0.5) if masked else None
+    bias = (0.3 * np.random.default_rng(12).standard_normal(m)).astype(np.float32) if biased else None
+    kw = dict(keep_mask=None if mask is None else dev(mask), bias=None if bias is None else dev(bias))
+    ms, mt = sw.sw_moe_routing_mass(D["x"], D["wr"], k, **kw)
+    o_ms, o_mt = oracle.routing_mass(L["x"], L["wr"], k, keep_mask=mask, bias=bias)
+    np.testing.assert_allclose(host(ms), o_ms, rtol=1e-4, atol=1e-5)
+    # near-tie tokens may route their k-th slot differently: allow their gates
+    _, _, _, o_z = oracle.route(L["x"], L["wr"], k, keep_mask=mask, bias=bias, want_logits=True)
+    from parity import near_tie_tokens
+    n_near = int(near_tie_tokens(o_z, mask, k).sum())
+    assert np.abs(host(mt) - o_mt).max() <= 1e-4 + n_near * 1.0
+    assert abs(float(host(mt).sum()) - tokens) < 1e-3 * tokens
+    # accumulation over a second batch
+    sw.sw_moe_routing_mass(D["x"], D["wr"], k, mass=(ms, mt), **kw)
+    np.testing.assert_allclose(host(ms), 2 * o_ms, rtol=2e-4, atol=2e-5)

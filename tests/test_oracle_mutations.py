@@ -15,7 +15,8 @@ import oracle.oracle as O
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PIN_TESTS = ["tests/test_oracle_route.py", "tests/test_oracle_dispatch_prune.py",
-             "tests/test_oracle_forward.py", "tests/test_oracle_shared.py"]
+             "tests/test_oracle_forward.py", "tests/test_oracle_shared.py",
+             "tests/test_oracle_mass.py"]
 
 # (name, original text, mutated text); every occurrence is replaced.
 MUTANTS = [
@@ -55,6 +56,11 @@ MUTANTS = [
      "const float s = 1.0f / (1.0f + expf(z));"),
     ("shared_overwrites", "ot[o] += s * y;", "ot[o] = s * y;"),
     ("shared_up_is_gate", "const uint16_t* up = w13 + I * H;", "const uint16_t* up = w13;"),
+    ("mass_no_shift", "denom += expf(zt[e] - zmax);", "denom += expf(zt[e]);"),
+    ("mass_ignores_mask", "if ((!keep_mask || keep_mask[e]) && zt[e] > zmax) zmax = zt[e];",
+     "if (zt[e] > zmax) zmax = zt[e];"),
+    ("mass_topk_unweighted", "mass_topk[ids[t * k + j]] += w[t * k + j];",
+     "mass_topk[ids[t * k + j]] += 1.0f;"),
 ]
 
 
