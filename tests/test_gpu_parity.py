@@ -554,3 +554,16 @@ def test_routing_mass_parity(sw, hidden, m, k, tokens, masked, biased):
     # accumulation over a second batch
     sw.sw_moe_routing_mass(D["x"], D["wr"], k, mass=(ms, mt), **kw)
     np.testing.assert_allclose(host(ms), 2 * o_ms, rtol=2e-4, atol=2e-5)
+
+
+def test_gpu_kept_sets_nest_and_match_the_oracle(sw):
+    cfg, L, D = layer_inputs("decode_sweep")
+    prev = None
+    for p in (0.75, 0.5, 0.25):
+        g = sw.sw_moe_prune_compact(D["importance"], cfg.n_keep(p), cfg.top_k, compact=False,
+                                    hidden=cfg.hidden)
+        kept = set(host(g["kept"]).tolist())
+        assert kept == set(oracle.prune_compact(L["importance"], cfg.n_keep(p), cfg.top_k)[0].tolist())
+        if prev is not None:
+            assert prev < kept
+        prev = kept

@@ -116,3 +116,15 @@ def test_pool_shape_matches_the_paper_60gib():
         cfg = I.CONFIGS[name]
         assert 40 * cfg.n_experts * cfg.expert_bytes() == 60 * 2 ** 30
     assert I.CONFIGS["skewed_stack"].n_layers == 40
+
+
+def test_kept_sets_nest_across_pruning_ratios():
+    # one importance ranking gives nested kept sets: K'(64) in K'(128) in
+    # K'(192), as the paper's 25/50/75% sweeps use (Section 4, Fig. 2)
+    cfg = I.CONFIGS["decode_sweep"]
+    imp = I.make_importance(cfg)
+    sets = [set(oracle.prune_compact(imp, cfg.n_keep(p), cfg.top_k)[0].tolist())
+            for p in (0.75, 0.5, 0.25, 0.0)]
+    for small, big in zip(sets, sets[1:]):
+        assert small < big
+    assert sets[-1] == set(range(cfg.n_experts))
