@@ -182,7 +182,38 @@ def time_runner(torch, r: Runner, xs, steps, warmup):
         n_act.append(int(r.plan.n_active.item()))
     n_act_steps = np.array([n_act[s % len(xs)] for s in range(steps)], float)
     kern = time_kernels(torch, r, xs, steps)
+    kern["graph_step"], kern["graph_same"] = time_graph(torch, r, xs, max(4, steps // len(xs)))
     return t_step, phase, n_act_steps, n_act, kern
+
+
+def time_graph(torch, r: Runner, xs, reps):
+    """Mean step time with the host out of the loop: len(xs) steps (rotating
+    the batches and the pool copies) captured once in a HIP graph and
+    replayed `reps` times.  Returns (seconds per step, whether the graph's
+    last output equals the eager step's bit for bit)."""
+    G = len(xs)
+    r.step(xs[G - 1], (G - 1) % N_COPIES)
+    torch.cuda.synchronize()
+    ref = r.out.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for j in range(G):
+            r.step(xs[j], j % N_COPIES)
+    torch.cuda.synchronize()
+    same = True
+    for _ in range(2):
+        r.out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        same = same and bool(torch.equal(r.out, ref))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) / 1e3 / (reps * G), same
 
 
 def time_kernels(torch, r: Runner, xs, steps):
@@ -281,7 +312,10 @@ def measure(sw, torch, pool, cfg, T, xs, steps, warmup, dev):
     fwd = phase.sum(axis=1)
     U = nact_steps * 3 * H * Iw * 2
     n_mean = float(nact_steps.mean())
+    if not kern["graph_same"]:
+        raise RuntimeError("graph replay differs from the eager step")
     return dict(t_step_us=t_step * 1e6, tokens_per_s=T / t_step,
+                t_step_graph_us=kern["graph_step"] * 1e6, tokens_per_s_graph=T / kern["graph_step"],
                 t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
                 n_active_mean=n_mean, eq1_expected=float(m * (1 - (1 - k / m) ** T)),
                 unique_MiB_per_step=float(U.mean() / 2 ** 20),
@@ -374,7 +408,7 @@ def run_decode_sweep(args, sw, torch, dev):
             at[(T, p)] = s
             rows.append(dict(batch=T, pruning=p, m_pool=pools[p].m, **rounded(s)))
             print(f"# batch {T:3d} pruning {p:.2f}: {s['tokens_per_s']:.0f} tokens/s, "
-                  f"step {s['t_step_us']:.1f} us, n_active {s['n_active_mean']:.1f} "
+                  f"step {s['t_step_us']:.1f} us (graph {s['t_step_graph_us']:.1f} us), n_active {s['n_active_mean']:.1f} "
                   f"(Eq. 1 {s['eq1_expected']:.1f}), fwd {s['fwd_GBps']:.0f} GB/s",
                   file=sys.stderr, flush=True)
     head = at[(64, 0.5)]

@@ -99,9 +99,11 @@ __device__ __forceinline__ void dispatch_block(const int* ids, int n_pairs, int 
     const int rank = __popcll(peers & lt_mask);
     if (valid && rank == 0) s.wave_cnt[wave * m + e] = static_cast<uint8_t>(__popcll(peers));
     __syncthreads();
+    // only the waves holding pairs of this chunk have runs
+    const int used = min(nwaves, (n_pairs - c0 + 63) >> 6);
     for (int ee = tid; ee < m; ee += nthr) {
       int run = s.cursor[ee];
-      for (int w = 0; w < nwaves; ++w) {
+      for (int w = 0; w < used; ++w) {
         s.wave_base[w * m + ee] = run;
         run += s.wave_cnt[w * m + ee];
         s.wave_cnt[w * m + ee] = 0;

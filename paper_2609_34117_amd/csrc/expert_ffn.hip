@@ -805,6 +805,9 @@ hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool ti
   if (prefill_supported(T, H, I, m, k))
     return launch_gate_up_prefill(x, T, w13, tiled, counts, offsets, perm, active, n_active, H,
                                   I, m, k, ws.h_hi, ws.h_lo, stream);
+  if (skinny_gate_up_supported(T, H, I, m, k))
+    return launch_gate_up_skinny(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I,
+                                 m, k, ws.h_hi, ws.h_lo, stream);
   // the tiled layout is only produced for shapes the wave kernels take
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_gate_up_wave(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m,
@@ -849,6 +852,9 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
   if (prefill_supported(T, H, I, m, k))
     return launch_down_prefill(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                                ws.h_hi, ws.h_lo, ws.y, stream);
+  if (skinny_down_supported(T, H, I, m, k))
+    return launch_down_skinny(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                              ws.h_hi, ws.h_lo, ws.y, stream);
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_down_wave(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                             ws.h_hi, ws.h_lo, ws.y, stream);

@@ -1,0 +1,430 @@
+// Split-K expert kernels for calls with few tiles on gfx950: a decode batch
+// of one or two tokens (Section 2.1, Eq. 1: a batch of B tokens reads about
+// B * k distinct experts), or the single always-on shared expert (Section
+// 3.3).
+//
+// With far fewer 16-row tiles than the chip has waves, giving each wave
+// whole tiles leaves most waves idle and the step waits on one long stream
+// per wave.  Here the contraction of a tile is split over S waves of a
+// block (S = 8, 4, 2 or 1, chosen so that every wave still reads at least
+// six 1 KiB K steps): wave w of the block works on tile slot w / S and K
+// slice w % S.  A wave streams its slice of the tile's weights with all of
+// its loads in flight at once and multiplies it with the matching slice of
+// the tokens' activations, read straight from L2 (no LDS staging: every
+// activation element is used by one wave only).  The S partial tiles meet
+// in LDS, the slot's first wave adds them in slice order and runs the usual
+// epilogue (SwiGLU into h for gate/up; y rows for down).
+//
+// A pass covers 16 * NB tokens of a tile's expert; the host picks NB from
+// the batch size (an expert receives at most one pair per token), and the
+// pass count of a block is the largest of its tiles', the same in every
+// wave, so the barriers stay block-uniform.
+#include "sw_device.h"
+#include "sw_launch.h"
+
+namespace sw {
+namespace {
+
+constexpr int kWv = 8;         // waves per block
+constexpr int kBlk = 64 * kWv;
+constexpr int kKS = 8;         // K steps (32 wide) loaded per round per wave
+
+// The expert of tile `tile` as the active list holds it, read without
+// waiting for n_active (any entry below m is safe to read): the first
+// weight loads of a group go out before the plan is validated.  -1 when the
+// slot is outside the list's storage.
+__device__ __forceinline__ int speculative_expert(int tile, int tpe, const int* active, int m) {
+  const int a = tile / tpe;
+  return a < m ? active[a] : -1;
+}
+
+// Token count and first dispatch slot of tile `tile` with expert e; an
+// out-of-range tile, a bad expert id or a pair range outside [0, n_pairs)
+// has no tokens.
+__device__ __forceinline__ void tile_tokens(int tile, int n_tiles, int e, const int* counts,
+                                            const int* offsets, int m, int n_pairs, int* cnt,
+                                            int* base) {
+  *cnt = 0;
+  *base = 0;
+  if (tile >= n_tiles || e < 0 || e >= m) return;
+  const int c = counts[e], b = offsets[e];
+  if (c <= 0 || b < 0 || c > n_pairs - b) return;
+  *cnt = c;
+  *base = b;
+}
+
+// Largest token count over the block's tile slots: the block's pass count
+// follows from it, identically in every wave.
+__device__ __forceinline__ int group_max_count(int grp, int tps, int n_tiles, int tpe,
+                                               const int* active, const int* counts,
+                                               const int* offsets, int m, int n_pairs) {
+  int mx = 0;
+  for (int s = 0; s < tps; ++s) {
+    const int tile = grp * tps + s;
+    if (tile >= n_tiles) break;
+    int c, b;
+    tile_tokens(tile, n_tiles, active[tile / tpe], counts, offsets, m, n_pairs, &c, &b);
+    mx = max(mx, c);
+  }
+  return mx;
+}
+
+// ---------------------------------------------------------------------------
+// gate/up + SwiGLU
+
+template <int NB, bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void gate_up_skinny_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
+    const int* __restrict__ counts, const int* __restrict__ offsets,
+    const int* __restrict__ perm, const int* __restrict__ active,
+    const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
+    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs, int S) {
+  constexpr int kNT = 16 * NB;
+  __shared__ f32x4 red[kWv][NB][kWave];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, kg = lane >> 4;
+  const int tps = kWv / S, slot = wave / S, slice = wave - slot * S;
+  const int tpe = I / 8, nsteps = H / 32;
+  const int s_lo = (slice * nsteps) / S, s_hi = ((slice + 1) * nsteps) / S;
+  const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
+  const int n_act = *n_active_p;
+  bool first = true;
+
+  for (int grp = blockIdx.x;; grp += gridDim.x) {
+    const int tile = grp * tps + slot;
+    const int e = speculative_expert(tile, tpe, active, m);
+    const bool e_ok = e >= 0 && e < m;
+    const int ib = tile - (tile / tpe) * tpe;
+    const auto w = make_rsrc(w13 + (size_t)(e_ok ? e : 0) * 2 * I * H,
+                             e_ok ? 4u * (uint32_t)I * H : 0u);
+    uint32_t row, stride;
+    if (kTiled) {
+      row = (uint32_t)ib * 32u * H + (uint32_t)lane * 16u;
+      stride = 1024u;
+    } else {
+      const int wrow = r < 8 ? ib * 8 + r : I + ib * 8 + (r - 8);
+      row = (uint32_t)wrow * H * 2u + kg * 16u;
+      stride = 64u;
+    }
+    auto issue = [&](u32x4 (&A)[kKS], int sb) {
+#pragma unroll
+      for (int j = 0; j < kKS; ++j) {
+        const uint32_t off = sb + j < s_hi ? row + (uint32_t)(sb + j) * stride : kOutOfRange;
+        A[j] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
+      }
+    };
+    u32x4 A[kKS];
+    issue(A, s_lo);
+    if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
+    const int n_tiles = n_act * tpe;
+    if (grp * tps >= n_tiles) break;
+    int cnt, base;
+    tile_tokens(tile, n_tiles, e, counts, offsets, m, n_pairs, &cnt, &base);
+    const int maxcnt =
+        tps == 1 ? cnt : group_max_count(grp, tps, n_tiles, tpe, active, counts, offsets, m, n_pairs);
+    const uint32_t hbytes = 2u * (uint32_t)cnt * (uint32_t)I;
+    const auto hh = make_rsrc(h_hi + (size_t)base * I, hbytes);
+    const auto hl = make_rsrc(h_lo + (size_t)base * I, hbytes);
+
+    for (int p0 = 0; p0 < maxcnt; p0 += kNT) {
+      if (!first) __syncthreads();  // the previous pass's readers of red are done
+      first = false;
+      const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
+      // activation row of column r of each 16-token block: x[pair / k].  The
+      // pair ids are read with wave-uniform (scalar) loads, which do not
+      // wait behind the weight loads already in flight; the index is clamped
+      // into the array and the value used only for slots below cnt.
+      uint32_t xrow[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        int p = -1;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int v = perm[min(base + p0 + nb * 16 + j, n_pairs - 1)];
+          p = r == j ? v : p;
+        }
+        const int sl = p0 + nb * 16 + r;
+        xrow[nb] = (nb < nbn && sl < cnt && p >= 0 && p < n_pairs)
+                       ? (uint32_t)(p / k) * H * 2u + kg * 16u : kOutOfRange;
+      }
+      f32x4 acc[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int sb = s_lo; sb < s_hi; sb += kKS) {
+        if (sb != s_lo || p0 != 0) issue(A, sb);
+        u32x4 B[NB][kKS];
+#pragma unroll
+        for (int j = 0; j < kKS; ++j)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            B[nb][j] = buf_ld128(xr, (sb + j < s_hi && xrow[nb] != kOutOfRange)
+                                         ? xrow[nb] + (uint32_t)(sb + j) * 64u : kOutOfRange);
+        // keep every load of the round ahead of the first MFMA
+        __builtin_amdgcn_sched_barrier(0);
+        // (columns past the pass's tokens multiply zeros and are not stored)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int j = 0; j < kKS; ++j) acc[nb] = mfma_16x16x32(A[j], B[nb][j], acc[nb]);
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
+      __syncthreads();
+      if (slice == 0 && nbn > 0) {
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          if (nb < nbn) {
+            f32x4 g4 = red[wave][nb][lane];
+            for (int q = 1; q < S; ++q) g4 += red[wave + q][nb][lane];
+            f32x4 u4;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
+            uint16_t hb[4], lb[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float gt = g4[i];
+              const float hv = (gt / (1.0f + expf(-gt))) * u4[i];
+              hb[i] = f32_to_bf16(hv);
+              lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
+            }
+            const u32x2 hw = {(uint32_t)hb[0] | ((uint32_t)hb[1] << 16),
+                              (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
+            const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
+                              (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+            const int sl = p0 + nb * 16 + r;
+            uint32_t off = kOutOfRange;
+            if (lane < 32 && sl < cnt) off = ((uint32_t)sl * I + (uint32_t)(ib * 8 + kg * 4)) * 2u;
+            __builtin_amdgcn_raw_buffer_store_b64(hw, hh, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b64(lw, hl, off, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// down projection
+
+template <int NB, bool kTiled>
+__global__ __launch_bounds__(kBlk, 1) void down_skinny_kernel(
+    const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
+    const uint16_t* __restrict__ w2, const int* __restrict__ counts,
+    const int* __restrict__ offsets, const int* __restrict__ perm,
+    const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
+    int H, int I, int m, int n_pairs, int S) {
+  constexpr int kNT = 16 * NB;
+  constexpr int kHS = kKS / 2;  // two MFMAs (hi, lo) per weight load
+  __shared__ f32x4 red[kWv][NB][kWave];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = lane & 15, kg = lane >> 4;
+  const int tps = kWv / S, slot = wave / S, slice = wave - slot * S;
+  const int tpe = H / 16, nsteps = I / 32;
+  const int s_lo = (slice * nsteps) / S, s_hi = ((slice + 1) * nsteps) / S;
+  const uint32_t hbytes_all = 2u * (uint32_t)n_pairs * (uint32_t)I;
+  const auto hhr = make_rsrc(h_hi, hbytes_all);
+  const auto hlr = make_rsrc(h_lo, hbytes_all);
+  const auto yr = make_rsrc(y, 4u * (uint32_t)n_pairs * (uint32_t)H);
+  const int n_act = *n_active_p;
+  bool first = true;
+
+  for (int grp = blockIdx.x;; grp += gridDim.x) {
+    const int tile = grp * tps + slot;
+    const int e = speculative_expert(tile, tpe, active, m);
+    const bool e_ok = e >= 0 && e < m;
+    const int ib = tile - (tile / tpe) * tpe;
+    const auto w = make_rsrc(w2 + (size_t)(e_ok ? e : 0) * H * I, e_ok ? 2u * (uint32_t)H * I : 0u);
+    uint32_t row, stride;
+    if (kTiled) {
+      row = (uint32_t)ib * 32u * I + (uint32_t)lane * 16u;
+      stride = 1024u;
+    } else {
+      row = (uint32_t)(ib * 16 + r) * I * 2u + kg * 16u;
+      stride = 64u;
+    }
+    auto issue = [&](u32x4 (&A)[kHS], int sb) {
+#pragma unroll
+      for (int j = 0; j < kHS; ++j) {
+        const uint32_t off = sb + j < s_hi ? row + (uint32_t)(sb + j) * stride : kOutOfRange;
+        A[j] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
+      }
+    };
+    u32x4 A[kHS];
+    issue(A, s_lo);
+    if (n_act <= 0 || n_act > m) return;
+    const int n_tiles = n_act * tpe;
+    if (grp * tps >= n_tiles) break;
+    int cnt, base;
+    tile_tokens(tile, n_tiles, e, counts, offsets, m, n_pairs, &cnt, &base);
+    const int maxcnt =
+        tps == 1 ? cnt : group_max_count(grp, tps, n_tiles, tpe, active, counts, offsets, m, n_pairs);
+
+    for (int p0 = 0; p0 < maxcnt; p0 += kNT) {
+      if (!first) __syncthreads();
+      first = false;
+      const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
+      // h rows of the pass are the dispatch slots base + p0 + nb * 16 + r;
+      // the pair ids (y rows) are loaded now and used by the epilogue
+      uint32_t hrow[NB];
+      int pid[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int sl = p0 + nb * 16 + r;
+        const bool in = nb < nbn && sl < cnt;
+        hrow[nb] = in ? (uint32_t)(base + sl) * I * 2u + kg * 16u : kOutOfRange;
+        pid[nb] = in ? perm[base + sl] : -1;
+      }
+      f32x4 acc[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int sb = s_lo; sb < s_hi; sb += kHS) {
+        if (sb != s_lo || p0 != 0) issue(A, sb);
+        u32x4 BH[NB][kHS], BL[NB][kHS];
+#pragma unroll
+        for (int j = 0; j < kHS; ++j)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const uint32_t ho = (sb + j < s_hi && hrow[nb] != kOutOfRange)
+                                    ? hrow[nb] + (uint32_t)(sb + j) * 64u : kOutOfRange;
+            BH[nb][j] = buf_ld128(hhr, ho);
+            BL[nb][j] = buf_ld128(hlr, ho);
+          }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+            for (int j = 0; j < kHS; ++j) {
+              acc[nb] = mfma_16x16x32(A[j], BH[nb][j], acc[nb]);
+              acc[nb] = mfma_16x16x32(A[j], BL[nb][j], acc[nb]);
+            }
+      }
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
+      __syncthreads();
+      if (slice == 0 && nbn > 0) {
+        const int o = ib * 16 + kg * 4;
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+          if (nb < nbn) {
+            f32x4 c = red[wave][nb][lane];
+            for (int q = 1; q < S; ++q) c += red[wave + q][nb][lane];
+            const int p = pid[nb];
+            uint32_t off = kOutOfRange;
+            if (p >= 0 && p < n_pairs) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
+            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, c), yr, off, 0, 0);
+          }
+        }
+      }
+    }
+  }
+}
+
+// K split: the largest S in {8, 4, 2, 1} that leaves every wave at least six
+// K steps.
+int split_factor(int nsteps) {
+  int s = 8;
+  while (s > 1 && nsteps / s < 6) s >>= 1;
+  return s;
+}
+
+// Token blocks per pass: an expert receives at most one pair per token.
+int token_blocks(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : 4; }
+
+// Upper bound of the active experts of a call.
+int64_t max_active(int T, int m, int k) { return std::min<int64_t>(m, (int64_t)T * k); }
+
+int skinny_grid(int64_t tiles, int S) {
+  const int64_t groups = (tiles + kWv / S - 1) / (kWv / S);
+  return (int)std::max<int64_t>(1, std::min<int64_t>(groups, 4096));
+}
+
+constexpr int kMaxSkinnyTiles = 2048;
+
+}  // namespace
+
+bool skinny_gate_up_supported(int T, int H, int I, int m, int k) {
+  return T >= 1 && H >= 1024 && H % 32 == 0 && I % 8 == 0 &&
+         max_active(T, m, k) * (I / 8) <= kMaxSkinnyTiles &&
+         2 * (int64_t)T * H < ((int64_t)1 << 31) && 2 * (int64_t)T * k * I < ((int64_t)1 << 31);
+}
+
+bool skinny_down_supported(int T, int H, int I, int m, int k) {
+  return T >= 1 && I >= 256 && I % 32 == 0 && H % 16 == 0 &&
+         max_active(T, m, k) * (H / 16) <= kMaxSkinnyTiles &&
+         4 * (int64_t)T * k * H < ((int64_t)1 << 31) && 2 * (int64_t)T * k * I < ((int64_t)1 << 31);
+}
+
+template <int NB>
+static void gate_up_skinny(int grid, const uint16_t* x, const uint16_t* w13, bool tiled,
+                           const int* counts, const int* offsets, const int* perm,
+                           const int* active, const int* n_active, int H, int I, int m, int k,
+                           int n_pairs, int S, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+  if (tiled)
+    gate_up_skinny_kernel<NB, true><<<grid, kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, n_pairs, S);
+  else
+    gate_up_skinny_kernel<NB, false><<<grid, kBlk, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, n_pairs, S);
+}
+
+hipError_t launch_gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                 const int* counts, const int* offsets, const int* perm,
+                                 const int* active, const int* n_active, int H, int I, int m,
+                                 int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+  const int S = split_factor(H / 32);
+  const int grid = skinny_grid(max_active(T, m, k) * (I / 8), S);
+  switch (token_blocks(T)) {
+    case 1:
+      gate_up_skinny<1>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        T * k, S, h_hi, h_lo, stream);
+      break;
+    case 2:
+      gate_up_skinny<2>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        T * k, S, h_hi, h_lo, stream);
+      break;
+    default:
+      gate_up_skinny<4>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        T * k, S, h_hi, h_lo, stream);
+  }
+  return hipGetLastError();
+}
+
+template <int NB>
+static void down_skinny(int grid, const uint16_t* w2, bool tiled, const int* counts,
+                        const int* offsets, const int* perm, const int* active,
+                        const int* n_active, int H, int I, int m, int n_pairs, int S,
+                        const uint16_t* h_hi, const uint16_t* h_lo, float* y, hipStream_t stream) {
+  if (tiled)
+    down_skinny_kernel<NB, true><<<grid, kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, n_pairs, S);
+  else
+    down_skinny_kernel<NB, false><<<grid, kBlk, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, n_pairs, S);
+}
+
+hipError_t launch_down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
+                              const int* offsets, const int* perm, const int* active,
+                              const int* n_active, int H, int I, int m, int k,
+                              const uint16_t* h_hi, const uint16_t* h_lo, float* y,
+                              hipStream_t stream) {
+  const int S = split_factor(I / 32);
+  const int grid = skinny_grid(max_active(T, m, k) * (H / 16), S);
+  switch (token_blocks(T)) {
+    case 1:
+      down_skinny<1>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
+                     h_hi, h_lo, y, stream);
+      break;
+    case 2:
+      down_skinny<2>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
+                     h_hi, h_lo, y, stream);
+      break;
+    default:
+      down_skinny<4>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
+                     h_hi, h_lo, y, stream);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace sw

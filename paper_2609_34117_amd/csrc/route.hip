@@ -269,12 +269,16 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
   }
 }
 
-// Route + dispatch of a small batch in one 1024-thread block: every 16-lane
-// row selects one token at a time (64 tokens per pass), the ids go to LDS as
-// well as to memory, and the block then builds the dispatch plan from them.
+// Route + dispatch of a small batch in one 1024-thread block: 16-lane row
+// i selects token i (four tokens per wave; waves without a token skip the
+// selection, so the busy waves have a SIMD each up to 16 tokens), the ids go
+// to LDS as well as to memory, and the block then builds the dispatch plan
+// from them.  Larger batches take the multi-block top-k kernel and the
+// dispatch kernel: one block's SIMDs would serialise their selections.
 constexpr int kFusedThreads = 1024;
 constexpr int kFusedMaxPool = 256;
-constexpr int kFusedMaxPairs = 4096;
+constexpr int kFusedMaxTokens = 32;
+constexpr int kFusedMaxK = 16;
 
 template <int KPL>
 __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
@@ -283,15 +287,14 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
     float* __restrict__ topk_w, float* __restrict__ gap, int* __restrict__ counts,
     int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
     int* __restrict__ n_active) {
-  __shared__ int ids_s[kFusedMaxPairs];
+  __shared__ int ids_s[kFusedMaxTokens * kFusedMaxK];
   __shared__ int cursor[kFusedMaxPool];
   __shared__ int wave_base[(kFusedThreads / kWave) * kFusedMaxPool];
   __shared__ uint8_t wave_cnt[(kFusedThreads / kWave) * kFusedMaxPool];
   __shared__ uint32_t scan_scratch[34];
   __shared__ int bad;
-  const int row = threadIdx.x >> 4, r = threadIdx.x & 15;
-  for (int t0 = 0; t0 < T; t0 += kFusedThreads / 16) {
-    const int t = t0 + row;
+  const int t = threadIdx.x >> 4, r = threadIdx.x & 15;
+  if ((threadIdx.x >> 6) * 4 < T) {  // wave-uniform
     const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
     if (t < T) {
       store_selection(s, t, k, r, topk_ids, topk_w, gap);
@@ -499,7 +502,7 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
 }
 
 bool fused_route_dispatch_supported(int T, int m, int k) {
-  return T > 0 && m <= kFusedMaxPool && k <= 16 && (long)T * k <= kFusedMaxPairs;
+  return T > 0 && T <= kFusedMaxTokens && m <= kFusedMaxPool && k <= kFusedMaxK;
 }
 
 hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,

@@ -80,6 +80,19 @@ hipError_t launch_down_prefill(int T, const uint16_t* w2, bool tiled, const int*
                                const int* n_active, int H, int I, int m, int k,
                                const uint16_t* h_hi, const uint16_t* h_lo, float* y,
                                hipStream_t stream);
+// Few tiles (a decode batch of one or two tokens, the shared expert): each
+// tile's K is split over the waves of a block (expert_skinny.hip).
+bool skinny_gate_up_supported(int T, int H, int I, int m, int k);
+bool skinny_down_supported(int T, int H, int I, int m, int k);
+hipError_t launch_gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                 const int* counts, const int* offsets, const int* perm,
+                                 const int* active, const int* n_active, int H, int I, int m,
+                                 int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
+hipError_t launch_down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
+                              const int* offsets, const int* perm, const int* active,
+                              const int* n_active, int H, int I, int m, int k,
+                              const uint16_t* h_hi, const uint16_t* h_lo, float* y,
+                              hipStream_t stream);
 hipError_t launch_pack_experts(const uint16_t* w13, const uint16_t* w2, uint16_t* w13_t,
                                uint16_t* w2_t, int H, int I, int m, hipStream_t stream);
 hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,

@@ -248,6 +248,42 @@ def test_edge_shapes(sw, hidden, n_experts, top_k, inter, tokens):
         assert np.all(host(s["gpu"]["topk_w"]) == 1.0)
 
 
+# the split-K path (few tiles: each tile's K spread over the waves of a block)
+
+@pytest.mark.parametrize("name,batch,pruning", [("decode_sweep", 1, 0.0), ("decode_sweep", 2, 0.5),
+                                                ("decode_sweep", 3, 0.25), ("decode_b64", 1, 0.0),
+                                                ("decode_b64", 2, 0.5)])
+def test_split_k_decode_parity_and_layouts_agree(sw, name, batch, pruning):
+    cfg, L, D = layer_inputs(name)
+    mask = mask_for(cfg, L, pruning)
+    x = I.make_x(cfg, tokens=batch, rep=100 + batch)
+    s = check_layer(sw, cfg, dict(L, x=x), dict(D, x=dev(x)), mask)
+    assert s["n_active"] <= batch * cfg.top_k
+    t13, t2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    keep = None if mask is None else dev(mask)
+    tl = sw.moe_layer(dev(x), D["wr"], t13, t2, cfg.top_k, keep_mask=keep, layout=sw.TILED)
+    assert torch.equal(tl["out"], s["gpu"]["out"])
+    print(f"split-K {name} B={batch} p={pruning}: n_active={s['n_active']} "
+          f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
+    (1056, 24, 2, 296, 5, False),   # 37 gate/up tiles per expert: tile pairs span two experts
+    (1056, 24, 3, 288, 7, False),   # 66 down tiles per expert, 8 per block: groups span experts
+    (1024, 30, 4, 288, 20, True),   # 20 tokens on expert 0: two 16-token blocks in its pass;
+                                    # down on one wave per tile over 9 K steps
+])
+def test_split_k_ragged_shapes(sw, hidden, n_experts, top_k, inter, tokens, popular):
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=11)
+    bias = None
+    if popular:
+        bias = np.zeros(n_experts, np.float32)
+        bias[0] = 50.0
+    s = check_layer(sw, cfg, L, D, None, bias=bias)
+    if popular:
+        assert int(host(s["gpu"]["plan"].counts)[0]) == tokens
+
+
 def test_popular_expert_spans_several_token_passes(sw):
     # a bias makes expert 3 every token's first choice: 200 pairs on one
     # expert (4 passes of 64 tokens over its weights)
@@ -441,12 +477,12 @@ def _assert_same_route_dispatch(a, b):
 
 @pytest.mark.parametrize("hidden,n_experts,top_k,tokens,masked,biased", [
     (256, 16, 2, 8, False, False),        # tiny shape, one logit slice
-    (2048, 64, 8, 64, False, False),      # decode batch on a compacted 64-expert pool
-    (2048, 128, 8, 64, True, False),      # full pool under a 50% mask
+    (2048, 64, 8, 32, False, False),      # largest fused batch, compacted 64-expert pool
+    (2048, 128, 8, 21, True, False),      # full pool under a 50% mask, ragged last wave
     (2048, 256, 8, 1, False, True),       # one token, 256 experts, with bias
-    (2048, 256, 8, 256, True, True),      # 256 tokens: four selection passes of the block
-    (2048, 256, 8, 512, False, False),    # T*k = 4096: largest fused batch
-    (2048, 256, 8, 600, False, False),    # T*k > 4096: separate kernels
+    (2048, 256, 16, 32, True, True),      # largest fused k
+    (2048, 128, 8, 64, False, False),     # 64 tokens: multi-block top-k, then dispatch
+    (2048, 256, 8, 600, False, False),    # 4800 pairs: several dispatch chunks
     (512, 300, 8, 40, False, False),      # m > 256: separate kernels, wave top-k
     (256, 64, 17, 20, False, False),      # k > 16: separate kernels, wave top-k
     (520, 12, 4, 70, True, False),        # ragged H
@@ -499,7 +535,8 @@ def _shared_inputs(hidden, inter, tokens, seed):
 
 
 @pytest.mark.parametrize("hidden,inter,tokens", [(256, 128, 8), (2048, 1024, 64), (2048, 1024, 1),
-                                                 (512, 256, 200)])
+                                                 (512, 256, 200), (2048, 1024, 17),
+                                                 (2048, 1536, 100), (1024, 512, 300)])
 def test_shared_expert_parity(sw, hidden, inter, tokens):
     x, w13, w2, gate, base = _shared_inputs(hidden, inter, tokens, hidden + tokens)
     out = dev(base)
