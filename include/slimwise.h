@@ -102,7 +102,9 @@ sw_status sw_moe_prune_compact(const sw_moe_dims* full, const float* importance,
                                uint16_t* w13_c, uint16_t* w2_c, float* wr_c, float* bias_c,
                                void* stream);
 
-/* Workspace bytes sw_moe_route needs for T tokens (0 if T == 0). */
+/* Workspace bytes sw_moe_route and sw_moe_route_dispatch need for T tokens
+ * (0 if T == 0): the logit partials, plus, for batches of more than 2048
+ * pairs, the scratch of the chunked multi-block dispatch. */
 size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
 
 /*
@@ -153,9 +155,11 @@ sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t
  * Route, then dispatch, in one call (Section 3.1, Eq. 2; Section 2.1, Eq. 1):
  * every output is bit for bit what sw_moe_route followed by sw_moe_dispatch
  * of its topk_ids would write, with the same arguments, workspace
- * (sw_moe_route_workspace_bytes) and in-band errors.  For decode-sized
- * batches (m <= 256, k <= 16, T*k <= 4096) the selection and the dispatch
- * plan are built by one block, which saves two kernel launches per step.
+ * (sw_moe_route_workspace_bytes) and in-band errors.  For small decode
+ * batches (T <= 32, m <= 256, k <= 16) the selection and the dispatch plan
+ * are built by one block, which saves a kernel launch per step; above 2048
+ * pairs the dispatch runs as chunked multi-block kernels whose scratch is in
+ * the workspace (sw_moe_dispatch, which has no workspace, keeps one block).
  * T = 0 writes the empty plan (counts and offsets 0, *n_active = 0).
  */
 sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,

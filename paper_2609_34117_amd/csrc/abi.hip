@@ -137,7 +137,7 @@ sw_status sw_moe_pack_experts(const sw_moe_dims* d, const uint16_t* w13, const u
 
 size_t sw_moe_route_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
   if (check_dims(d) != SW_OK || n_tokens <= 0) return 0;
-  return sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts);
+  return sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k);
 }
 
 sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
@@ -151,7 +151,7 @@ sw_status sw_moe_route(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
   if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
       !aligned4(topk_w) || (gap && !aligned4(gap)) || (bias && !aligned4(bias)))
     return SW_ERR_ALIGN;
-  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts))
+  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k))
     return SW_ERR_WORKSPACE;
   (void)hipGetLastError();
   return launched(sw::launch_route(x, n_tokens, wr, bias, keep_mask, d->hidden, d->n_experts,
@@ -195,7 +195,7 @@ sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t
       !aligned4(topk_w) || !aligned4(perm) || (gap && !aligned4(gap)) ||
       (bias && !aligned4(bias)))
     return SW_ERR_ALIGN;
-  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts))
+  if (workspace_bytes < sw::route_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k))
     return SW_ERR_WORKSPACE;
   (void)hipGetLastError();
   return launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, d->hidden,

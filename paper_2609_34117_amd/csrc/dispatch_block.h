@@ -34,6 +34,47 @@ __device__ __forceinline__ uint64_t match_peers(int key, bool valid, int nbits) 
   return peers;
 }
 
+// Bits needed for an expert id below m.
+__device__ __forceinline__ int id_bits(int m) {
+  int nbits = 0;
+  while ((1 << nbits) < m) ++nbits;
+  return nbits;
+}
+
+// Stable scatter of the pairs c0 .. c0 + blockDim.x - 1 (those below
+// n_pairs) into perm: s.cursor[e] holds the first free slot of expert e and
+// is advanced past this chunk's pairs.  Within a wave a pair's rank among
+// equal ids comes from a ballot match; across waves the per-expert runs are
+// placed in wave order by a column scan over the waves that hold pairs.
+// Every thread of the block calls it (it contains barriers); s.wave_cnt must
+// be zero on entry and is left zero.
+__device__ __forceinline__ void scatter_chunk(const int* ids, int c0, int n_pairs, int m,
+                                              int nbits, const DispatchLds& s,
+                                              int* __restrict__ perm) {
+  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6;
+  const int nwaves = nthr >> 6;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  const int p = c0 + tid;
+  const bool valid = p < n_pairs;
+  const int e = valid ? ids[p] : 0;
+  const uint64_t peers = match_peers(e, valid, nbits);
+  const int rank = __popcll(peers & lt_mask);
+  if (valid && rank == 0) s.wave_cnt[wave * m + e] = static_cast<uint8_t>(__popcll(peers));
+  __syncthreads();
+  const int used = min(nwaves, (n_pairs - c0 + 63) >> 6);
+  for (int ee = tid; ee < m; ee += nthr) {
+    int run = s.cursor[ee];
+    for (int w = 0; w < used; ++w) {
+      s.wave_base[w * m + ee] = run;
+      run += s.wave_cnt[w * m + ee];
+      s.wave_cnt[w * m + ee] = 0;
+    }
+    s.cursor[ee] = run;
+  }
+  __syncthreads();
+  if (valid) perm[s.wave_base[wave * m + e] + rank] = p;
+}
+
 // Must be called by every thread of the block.  `ids` may live in global
 // memory or in LDS (written before a barrier that precedes the call).
 __device__ __forceinline__ void dispatch_block(const int* ids, int n_pairs, int m,
@@ -41,8 +82,7 @@ __device__ __forceinline__ void dispatch_block(const int* ids, int n_pairs, int 
                                                int* __restrict__ offsets, int* __restrict__ perm,
                                                int* __restrict__ active,
                                                int* __restrict__ n_active) {
-  const int tid = threadIdx.x, nthr = blockDim.x, lane = tid & 63, wave = tid >> 6;
-  const int nwaves = nthr >> 6;
+  const int tid = threadIdx.x, nthr = blockDim.x, nwaves = nthr >> 6;
   if (tid == 0) *s.bad = 0;
   for (int e = tid; e < m; e += nthr) s.cursor[e] = 0;
   for (int i = tid; i < nwaves * m; i += nthr) s.wave_cnt[i] = 0;
@@ -85,34 +125,9 @@ __device__ __forceinline__ void dispatch_block(const int* ids, int n_pairs, int 
   }
   __syncthreads();
 
-  // stable scatter, nthr pairs per chunk in pair order: within a wave a
-  // pair's rank among equal ids comes from a ballot match; across waves the
-  // per-expert runs are placed in wave order by a column scan
-  int nbits = 0;
-  while ((1 << nbits) < m) ++nbits;
-  const uint64_t lt_mask = (1ull << lane) - 1ull;
-  for (int c0 = 0; c0 < n_pairs; c0 += nthr) {
-    const int p = c0 + tid;
-    const bool valid = p < n_pairs;
-    const int e = valid ? ids[p] : 0;
-    const uint64_t peers = match_peers(e, valid, nbits);
-    const int rank = __popcll(peers & lt_mask);
-    if (valid && rank == 0) s.wave_cnt[wave * m + e] = static_cast<uint8_t>(__popcll(peers));
-    __syncthreads();
-    // only the waves holding pairs of this chunk have runs
-    const int used = min(nwaves, (n_pairs - c0 + 63) >> 6);
-    for (int ee = tid; ee < m; ee += nthr) {
-      int run = s.cursor[ee];
-      for (int w = 0; w < used; ++w) {
-        s.wave_base[w * m + ee] = run;
-        run += s.wave_cnt[w * m + ee];
-        s.wave_cnt[w * m + ee] = 0;
-      }
-      s.cursor[ee] = run;
-    }
-    __syncthreads();
-    if (valid) perm[s.wave_base[wave * m + e] + rank] = p;
-  }
+  // stable scatter, nthr pairs per chunk in pair order
+  const int nbits = id_bits(m);
+  for (int c0 = 0; c0 < n_pairs; c0 += nthr) scatter_chunk(ids, c0, n_pairs, m, nbits, s, perm);
 }
 
 }  // namespace sw

@@ -7,7 +7,9 @@
 // ~128 tokens per expert that would re-stream every weight four times.
 // Here the loop order is inverted:
 //   - a unit is (active expert, group of 16 row tiles), two tiles per wave;
-//     a persistent grid of one 8-wave block per compute unit walks the units;
+//     a persistent grid of one 8-wave block per compute unit walks the units,
+//     each XCD taking a contiguous run of every round's units (an expert's
+//     units then share one L2 for its gathered activations);
 //   - a pass covers up to 160 of the expert's tokens (10 MFMA column
 //     blocks), so a unit streams its weights once per pass, normally once;
 //   - the contraction runs in chunks of K: the activations of the pass are
@@ -67,6 +69,16 @@ __device__ __forceinline__ Unit unit_of(int u, int gpe, const int* active, const
   s.base = s.ok ? offsets[s.e] : 0;
   s.ok = s.ok && s.cnt > 0 && s.base >= 0 && s.cnt <= n_pairs - s.base;
   return s;
+}
+
+// Slot of block b in each round of gridDim.x units.  Blocks are dispatched
+// round-robin over the eight XCDs (block b runs on XCD b % 8); giving each
+// XCD a contiguous run of the round's units puts the units of one expert
+// (consecutive in the list) on one XCD at the same time, so they share that
+// XCD's L2 for the expert's gathered activations.
+__device__ __forceinline__ int unit_slot() {
+  const int b = blockIdx.x, g = gridDim.x;
+  return (g & 7) ? b : (b & 7) * (g >> 3) + (b >> 3);
 }
 
 // Pair ids of one pass into LDS (-1 past the expert's count).
@@ -145,7 +157,7 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
   const int gpe = (tpe + kTpu - 1) / kTpu;    // units per expert
   const int nchunks = H / kGuKc;
 
-  for (int u = blockIdx.x; u < n_act * gpe; u += gridDim.x) {
+  for (int u = unit_slot(); u < n_act * gpe; u += gridDim.x) {
     const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
     if (!s.ok) continue;  // block-uniform
     const auto w = make_rsrc(w13 + (size_t)s.e * 2 * I * H, 4u * (uint32_t)I * (uint32_t)H);
@@ -316,7 +328,7 @@ __global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
   const int nchunks = I / kDnKc;
   const auto yr = make_rsrc(y, 4u * (uint32_t)n_pairs * (uint32_t)H);
 
-  for (int u = blockIdx.x; u < n_act * gpe; u += gridDim.x) {
+  for (int u = unit_slot(); u < n_act * gpe; u += gridDim.x) {
     const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
     if (!s.ok) continue;
     const auto w = make_rsrc(w2 + (size_t)s.e * H * I, 2u * (uint32_t)H * (uint32_t)I);

@@ -95,6 +95,114 @@ __global__ __launch_bounds__(64 * KW) void route_logits_kernel(const uint16_t* _
   }
 }
 
+// Router logits of prefill-sized batches: a block of 4 waves computes a
+// 64-token x 64-expert tile over slice blockIdx.z of H (KS = gridDim.z
+// slices of whole 128-column chunks, so that several blocks share a compute
+// unit and hide each other's load latency).  The tile's x
+// rows are staged in LDS one 128-column chunk at a time (double-buffered),
+// so each token row is read once per 64 experts instead of once per 16, and
+// wave w reads the router rows of experts e0 + 16 w .. e0 + 16 w + 15
+// directly: every router fragment, split into its three bf16 pieces once,
+// feeds the 4 token blocks of the tile.  Same exact three-piece products as
+// route_logits_kernel, accumulated over H in ascending order.
+constexpr int kWideT = 64, kWideE = 64, kWideKc = 128, kWideRow = kWideKc + 8;
+
+__global__ __launch_bounds__(256) void route_logits_wide_kernel(const uint16_t* __restrict__ x,
+                                                               const float* __restrict__ wr,
+                                                               float* __restrict__ part, int T,
+                                                               int H, int m) {
+  __shared__ uint16_t xs[2][kWideT * kWideRow];
+  const int t0 = blockIdx.x * kWideT, e0 = blockIdx.y * kWideE;
+  const int ks = blockIdx.z, KS = gridDim.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r = lane & 15, kg = lane >> 4;
+  const auto w_rsrc = make_rsrc(wr, 4u * (uint32_t)m * (uint32_t)H);
+  const auto x_rsrc = make_rsrc(x, 2u * (uint32_t)T * (uint32_t)H);
+  const int e = e0 + wave * 16 + r;
+  const uint32_t w_row = (uint32_t)e * H * 4u;
+  const int all = H / kWideKc;
+  const int c_lo = (ks * all) / KS, c_hi = ((ks + 1) * all) / KS;
+
+  // chunk c of the tile's x: 64 rows x 16 pieces of 8 columns, 4 per thread
+  auto stage_load = [&](int c, u32x4 (&v)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = (int)threadIdx.x + j * 256, row = i >> 4, c8 = i & 15;
+      const int t = t0 + row;
+      v[j] = buf_ld128(x_rsrc, t < T ? ((uint32_t)t * H + (uint32_t)(c * kWideKc + c8 * 8)) * 2u
+                                     : kOutOfRange);
+    }
+  };
+  auto stage_store = [&](uint16_t* buf, const u32x4 (&v)[4]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = (int)threadIdx.x + j * 256;
+      *reinterpret_cast<u32x4*>(buf + (i >> 4) * kWideRow + (i & 15) * 8) = v[j];
+    }
+  };
+  auto w_issue = [&](int c, u32x4 (&wa)[4], u32x4 (&wb)[4]) {
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const uint32_t off =
+          e < m ? w_row + (uint32_t)(c * kWideKc + st * 32 + kg * 8) * 4u : kOutOfRange;
+      wa[st] = buf_ld128(w_rsrc, off);
+      wb[st] = buf_ld128(w_rsrc, off == kOutOfRange ? kOutOfRange : off + 16u);
+    }
+  };
+
+  f32x4 acc[4];
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  u32x4 v[4], wa[4], wb[4], na[4], nbw[4];
+  stage_load(c_lo, v);
+  w_issue(c_lo, wa, wb);
+  stage_store(xs[c_lo & 1], v);
+  for (int c = c_lo; c < c_hi; ++c) {
+    __syncthreads();  // chunk c is in LDS; the other buffer is free
+    const bool more = c + 1 < c_hi;
+    if (more) {
+      stage_load(c + 1, v);
+      w_issue(c + 1, na, nbw);
+    }
+    const uint16_t* buf = xs[c & 1];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      u32x4 hi, mid, lo;
+      split3_bf16x8(__builtin_bit_cast(float4, wa[st]), __builtin_bit_cast(float4, wb[st]), hi, mid,
+                    lo);
+#pragma unroll
+      for (int nb = 0; nb < 4; ++nb) {
+        const u32x4 b = *reinterpret_cast<const u32x4*>(buf + (nb * 16 + r) * kWideRow + st * 32 +
+                                                        kg * 8);
+        acc[nb] = mfma_16x16x32(hi, b, acc[nb]);
+        acc[nb] = mfma_16x16x32(mid, b, acc[nb]);
+        acc[nb] = mfma_16x16x32(lo, b, acc[nb]);
+      }
+    }
+    if (more) {
+      stage_store(xs[(c + 1) & 1], v);
+#pragma unroll
+      for (int st = 0; st < 4; ++st) {
+        wa[st] = na[st];
+        wb[st] = nbw[st];
+      }
+    }
+  }
+  // acc[nb][i]: expert e0 + 16 wave + 4 kg + i, token t0 + 16 nb + r
+#pragma unroll
+  for (int nb = 0; nb < 4; ++nb) {
+    const int t = t0 + nb * 16 + r;
+    if (t < T) {
+      float* dst = part + ((size_t)ks * T + t) * m;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ee = e0 + wave * 16 + 4 * kg + i;
+        if (ee < m) dst[ee] = acc[nb][i];
+      }
+    }
+  }
+}
+
 constexpr int kMaxSplit = 4;  // slices of H per logit tile
 
 // Order key of token t's logit for expert e: z = sum of the KS partials in
@@ -312,19 +420,28 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
 // tiles (prefill): 2 waves and no split.
 struct LogitsSplit {
   int kw, ks;
+  bool wide;  // route_logits_wide_kernel (one slice)
 };
 
 LogitsSplit logits_split(int T, int H, int m) {
   const long tiles = (long)((T + 15) / 16) * ((m + 15) / 16);
-  if (tiles >= 1024) return {2, 1};
+  if (tiles >= 1024) {
+    if (H % kWideKc != 0) return {2, 1, false};
+    return {4, std::min(kMaxSplit, std::max(1, H / kWideKc / 4)), true};  // >= 4 chunks a slice
+  }
   const int nsteps = (H + 31) / 32;
   const int max_ks = std::min(kMaxSplit, std::max(1, nsteps / 16));  // waves keep >= 4 K steps
   const long want = (256 + tiles - 1) / tiles;
-  return {4, (int)std::max<long>(1, std::min<long>(want, max_ks))};
+  return {4, (int)std::max<long>(1, std::min<long>(want, max_ks)), false};
 }
 
 hipError_t launch_logits(const uint16_t* x, int T, const float* wr, int H, int m, float* part,
                          const LogitsSplit& sp, hipStream_t stream) {
+  if (sp.wide) {
+    const dim3 wgrid((T + kWideT - 1) / kWideT, (m + kWideE - 1) / kWideE, sp.ks);
+    route_logits_wide_kernel<<<wgrid, 256, 0, stream>>>(x, wr, part, T, H, m);
+    return hipGetLastError();
+  }
   const dim3 grid((T + 15) / 16, (m + 15) / 16, sp.ks);
   if (sp.kw == 4)
     route_logits_kernel<4><<<grid, 256, 0, stream>>>(x, wr, part, T, H, m);
@@ -441,7 +558,7 @@ __global__ __launch_bounds__(256) void mass_accumulate_kernel(
 size_t routing_mass_workspace_bytes(int T, int H, int m, int k) {
   if (T <= 0) return 0;
   const size_t P = (size_t)T * k;
-  return route_workspace_bytes(T, H, m) + 3 * align_up(P * 4, 256) +
+  return route_workspace_bytes(T, H, m, k) + 3 * align_up(P * 4, 256) +
          3 * align_up((size_t)(m + 1) * 4, 256) + 256 + 2 * align_up((size_t)T * 4, 256);
 }
 
@@ -452,7 +569,7 @@ hipError_t launch_routing_mass(const uint16_t* x, int T, const float* wr, const 
   char* p = static_cast<char*>(workspace);
   const size_t P = (size_t)T * k;
   float* part = reinterpret_cast<float*>(p);
-  p += route_workspace_bytes(T, H, m);
+  p += route_workspace_bytes(T, H, m, k);
   int* ids = reinterpret_cast<int*>(p);
   p += align_up(P * 4, 256);
   float* w = reinterpret_cast<float*>(p);
@@ -484,9 +601,15 @@ hipError_t launch_routing_mass(const uint16_t* x, int T, const float* wr, const 
   return hipGetLastError();
 }
 
-size_t route_workspace_bytes(int T, int H, int m) {
-  if (T <= 0) return 0;
+// Logit partials, then the chunked dispatch's scratch (used once the
+// partials have been read).
+static size_t part_bytes(int T, int H, int m) {
   return align_up((size_t)logits_split(T, H, m).ks * T * m * sizeof(float), 256);
+}
+
+size_t route_workspace_bytes(int T, int H, int m, int k) {
+  if (T <= 0) return 0;
+  return part_bytes(T, H, m) + dispatch_workspace_bytes(T * k, m);
 }
 
 hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* bias,
@@ -514,7 +637,8 @@ hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, cons
     hipError_t err = launch_route(x, T, wr, bias, keep_mask, H, m, k, topk_ids, topk_w, gap,
                                   workspace, stream);
     if (err != hipSuccess) return err;
-    return launch_dispatch(topk_ids, T * k, m, counts, offsets, perm, active, n_active, stream);
+    return launch_dispatch(topk_ids, T * k, m, counts, offsets, perm, active, n_active, stream,
+                           static_cast<char*>(workspace) + part_bytes(T, H, m));
   }
   float* part = static_cast<float*>(workspace);
   const LogitsSplit sp = logits_split(T, H, m);

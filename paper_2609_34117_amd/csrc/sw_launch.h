@@ -15,7 +15,7 @@ __host__ __device__ inline size_t align_up(size_t v, size_t a) { return (v + a -
 constexpr int kMaxStreamH = 2048;
 constexpr int kMaxStreamI = 1024;
 
-size_t route_workspace_bytes(int T, int H, int m);
+size_t route_workspace_bytes(int T, int H, int m, int k);
 size_t forward_workspace_bytes(int T, int H, int I, int k);
 // y [T*k, H] fp32 inside a forward workspace
 const float* forward_y(const void* workspace, int T, int H, int I, int k = 1);
@@ -39,8 +39,13 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
                         const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                         float* topk_w, float* gap, void* workspace, hipStream_t stream);
 
+// Dispatch of n_pairs expert ids; batches above a few thousand pairs run as
+// chunked multi-block kernels when `workspace` (dispatch_workspace_bytes)
+// is given, else in one block.
+size_t dispatch_workspace_bytes(int n_pairs, int m);
 hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts, int* offsets,
-                           int* perm, int* active, int* n_active, hipStream_t stream);
+                           int* perm, int* active, int* n_active, hipStream_t stream,
+                           void* workspace = nullptr);
 
 // Route, then dispatch of the selected ids; one select + dispatch block when
 // fused_route_dispatch_supported, else the separate kernels.
