@@ -6,7 +6,9 @@
 //   - A persistent grid of one 8-wave block per compute unit.  The tiles of
 //     all active experts form one list; block b owns the contiguous,
 //     equal-sized range b*per .. (b+1)*per of it, which crosses at most a few
-//     expert boundaries ("segments").
+//     expert boundaries ("segments").  When some expert has more tokens than
+//     one pass holds, the list is of (expert, pass, tile) work items instead,
+//     so every block still gets the same number of tile passes.
 //   - Per segment, the block stages the expert's token activations (gate/up:
 //     x rows; down: h hi/lo rows) in LDS once, up to 32 tokens per pass.
 //   - Each wave then owns whole tiles (16 weight rows over the full K) and
@@ -23,6 +25,8 @@
 // Tiles:  gate_up: 8 gate rows + the 8 matching up rows; epilogue writes
 //         h = silu(g) * u as a bf16 hi/lo pair.
 //         down: 16 output rows of W2; epilogue writes y (fp32) per pair.
+#include <cmath>
+
 #include "sw_device.h"
 #include "sw_launch.h"
 
@@ -36,10 +40,13 @@ constexpr int kNT = 32;           // tokens staged per pass
 constexpr int kNBk = kNT / 16;    // MFMA column blocks per pass
 constexpr int kPad = 8;           // bf16 elements of padding per staged row
 constexpr int kDepth = 3;         // streamed chunks held in registers per wave
+constexpr int kMaxExperts = 1024;  // pool size limit of the library
 
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
+  int p0;      // first token of the segment's pass (weighted walk), else 0
+  int w_end;   // work item after the segment (weighted walk)
   bool e_ok;   // expert id in range: its weights may be read
 };
 
@@ -60,6 +67,8 @@ __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const
   s.e = s.e_ok ? e : 0;
   s.cnt = counts[s.e];
   s.base = offsets[s.e];
+  s.p0 = 0;
+  s.w_end = 0;
   return s;
 }
 
@@ -77,6 +86,106 @@ __device__ __forceinline__ void block_range(int total, int* r_lo, int* r_hi) {
   const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
   *r_lo = min(total, (int)blockIdx.x * per);
   *r_hi = min(total, *r_lo + per);
+}
+
+// Token passes of expert e's pairs (0 for an invalid plan entry).
+__device__ __forceinline__ int expert_passes(int e, const int* counts, const int* offsets, int m,
+                                             int n_pairs) {
+  if (e < 0 || e >= m) return 0;
+  const int c = counts[e], b = offsets[e];
+  if (c <= 0 || b < 0 || c > n_pairs - b) return 0;
+  return (c + kNT - 1) / kNT;
+}
+
+// Counts of experts 2t and 2t + 1 (thread t) from the plan's offsets: one
+// round of independent loads (no dependent plan reads on the decode path).
+struct PairCounts {
+  int o0, o1, o2;
+};
+
+__device__ __forceinline__ PairCounts load_pair_counts(const int* offsets, int m) {
+  // unconditional loads with indices clamped to offsets[m] (branch-free, so
+  // nothing consumes them before the caller does); past m the differences
+  // are 0
+  const int e0 = 2 * (int)threadIdx.x;
+  return PairCounts{offsets[min(e0, m)], offsets[min(e0 + 1, m)], offsets[min(e0 + 2, m)]};
+}
+
+// Whether some expert has more tokens than one pass holds (a garbage plan
+// can only make this true, which takes the checked weighted walk): each
+// wave posts its verdict to its own LDS slot before a barrier, and every
+// thread reads the eight slots after it, so the check rides on a barrier
+// the kernel has anyway.  m <= 2 * kBlk.
+__device__ __forceinline__ void post_passes_verdict(const PairCounts& c, int* verdict) {
+  const bool big = c.o1 - c.o0 > kNT || c.o2 - c.o1 > kNT;
+  const bool any = __ballot(big) != 0;
+  if ((threadIdx.x & 63) == 0) verdict[threadIdx.x >> 6] = any ? 1 : 0;
+}
+
+__device__ __forceinline__ bool read_passes_verdict(const int* verdict) {
+  int v = 0;
+#pragma unroll
+  for (int w = 0; w < kWv; ++w) v |= verdict[w];
+  return v != 0;
+}
+
+// The same with a barrier of its own.  Every thread of the block calls it.
+__device__ __forceinline__ bool some_expert_needs_passes(const PairCounts& c, int* verdict) {
+  post_passes_verdict(c, verdict);
+  __syncthreads();
+  return read_passes_verdict(verdict);
+}
+
+// Work-weighted ranges, for a batch where some expert has more than kNT
+// tokens: expert slot a owns np_a * tpe work items (its tiles once per
+// token pass, pass-major) from wp[a] on, wp[n_act] being the total, and
+// blocks take equal contiguous runs of work.  A popular expert is then
+// spread over more blocks instead of lengthening the few blocks that own
+// its tiles (when every expert fits one pass, the tile ranges are already
+// balanced and this is not used).  Every thread of the block calls it;
+// n_act <= 2 * kBlk.
+__device__ void weighted_work(int n_act, int tpe, const int* active, const int* counts,
+                              const int* offsets, int m, int n_pairs, int* wp, uint32_t* scan) {
+  const int a0 = 2 * (int)threadIdx.x, a1 = a0 + 1;
+  const int n0 = a0 < n_act ? expert_passes(active[a0], counts, offsets, m, n_pairs) : 0;
+  const int n1 = a1 < n_act ? expert_passes(active[a1], counts, offsets, m, n_pairs) : 0;
+  uint32_t off, unused, total, unused_t;
+  block_exclusive_scan2((uint32_t)((n0 + n1) * tpe), 0u, scan, &off, &unused, &total, &unused_t);
+  if (a0 < n_act) wp[a0] = (int)off;
+  if (a1 < n_act) wp[a1] = (int)off + n0 * tpe;
+  if (threadIdx.x == 0) wp[n_act] = (int)total;
+  __syncthreads();
+}
+
+// Segment of the weighted walk starting at work item w < w_hi: the expert
+// slot holding w (the last a with wp[a] <= w, which has work), its pass,
+// and the run of tiles to the end of that pass or of the block's range.
+__device__ __forceinline__ Segment weighted_segment(int w, int w_hi, int n_act, const int* wp,
+                                                    int tpe, const int* active,
+                                                    const int* counts, const int* offsets,
+                                                    int m) {
+  int lo = 0, hi = n_act - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (wp[mid] <= w)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  Segment s;
+  s.a = lo;
+  const int q = w - wp[lo], pass = q / tpe, tile = q - pass * tpe;
+  const int run = min(tpe - tile, w_hi - w);
+  s.lo = lo * tpe + tile;
+  s.hi = s.lo + run;
+  s.w_end = w + run;
+  s.p0 = pass * kNT;
+  const int e = active[lo];
+  s.e_ok = e >= 0 && e < m;
+  s.e = s.e_ok ? e : 0;
+  s.cnt = counts[s.e];
+  s.base = offsets[s.e];
+  return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -170,7 +279,11 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
   }
 }
 
-template <bool kTiled>
+// kBalance: the batch has more tokens than one pass holds, so an expert
+// may need several passes and the blocks may switch to the weighted walk.
+// kSpeculate: guess n_active == m and issue the first weight chunks before
+// n_active arrives (a wrong guess redoes the first segment).
+template <bool kTiled, bool kBalance, bool kSpeculate>
 __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
     const int* __restrict__ counts, const int* __restrict__ offsets,
@@ -179,6 +292,9 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
   __shared__ uint16_t xs[kNT * (kMaxStreamH + kPad)];
   __shared__ int pid[kNT];
+  __shared__ int wp[kMaxExperts + 1];
+  __shared__ uint32_t scan[34];
+  __shared__ int verdict[kWv];
   const int tpe = I / 8;
   const int n_act = *n_active_p;
 
@@ -213,29 +329,73 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   // batch): the block's tile range and its first expert then follow from m
   // alone, so that segment's plan loads and weight chunks go out together
   // with the n_active load.  A wrong guess redoes the first segment.
-  int r_lo, r_hi;
-  block_range(m * tpe, &r_lo, &r_hi);
-  Segment sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
-  begin_segment(sg);
-  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
-  const bool all = n_act == m;
-  if (!all) {
-    block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo >= r_hi) return;
-    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+  // (Without kSpeculate the first segment waits for n_active instead.)
+  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
+  int r_lo = 0, r_hi = 0;
+  Segment sg;
+  if constexpr (kSpeculate) {
+    block_range(m * tpe, &r_lo, &r_hi);
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
     begin_segment(sg);
-  } else if (r_lo >= r_hi) {
-    return;
+  }
+  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
+  if constexpr (!kSpeculate) block_range(n_act * tpe, &r_lo, &r_hi);
+  const bool all = n_act == m;
+  // With kBalance, whether some expert needs several token passes is
+  // decided once, by the first barrier of the block's first pass (so that
+  // pass's pair-id loads are already out); a block without such a barrier
+  // decides it here.  With several passes the block switches to its range
+  // of the weighted walk.
+  bool checked = !kBalance, weighted = false;
+  int w_hi = 0;
+  auto go_weighted = [&]() {
+    weighted = true;
+    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, wp, scan);
+    block_range(wp[n_act], &r_lo, &w_hi);
+    if (r_lo >= w_hi) return false;
+    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    begin_segment(sg);
+    return true;
+  };
+  if constexpr (!kBalance) {
+    if (!all) {
+      block_range(n_act * tpe, &r_lo, &r_hi);
+      if (r_lo >= r_hi) return;
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+      begin_segment(sg);
+    } else if (r_lo >= r_hi) {
+      return;
+    }
+  } else {
+    if (kSpeculate && !all) block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo < r_hi && (!kSpeculate || !all)) {
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
+      begin_segment(sg);
+    }
+    if (r_lo >= r_hi) {
+      checked = true;
+      if (!some_expert_needs_passes(pc, verdict) || !go_weighted()) return;
+    }
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
+    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
+      checked = true;
+      if (some_expert_needs_passes(pc, verdict)) {
+        if (!go_weighted()) return;
+        continue;
+      }
+    }
     g.cnt = sg.cnt;
     const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
     g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
     g.hl = make_rsrc(h_lo + (size_t)sg.base * I, hbytes);
-    for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
-      if (p0 > 0) {
+    // one pass per segment on the weighted walk, every pass otherwise
+    const int p_end = weighted ? min(sg.cnt, sg.p0 + kNT) : sg.cnt;
+    bool restart = false;
+    for (int p0 = sg.p0; p0 < p_end; p0 += kNT) {
+      if (p0 > sg.p0) {
 #pragma unroll
         for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
       }
@@ -249,7 +409,15 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
         const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
+      if (!checked) post_passes_verdict(pc, verdict);
       __syncthreads();
+      if (!checked) {
+        checked = true;
+        if (read_passes_verdict(verdict)) {
+          restart = true;
+          break;
+        }
+      }
       if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
       __syncthreads();
       const int row8 = H / 8;
@@ -274,8 +442,17 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
         }
       }
     }
-    if (sg.hi >= r_hi) break;
-    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    if (restart) {
+      if (!go_weighted()) return;
+      continue;
+    }
+    if (weighted) {
+      if (sg.w_end >= w_hi) break;
+      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    } else {
+      if (sg.hi >= r_hi) break;
+      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    }
     begin_segment(sg);
   }
 }
@@ -352,7 +529,7 @@ __device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (
   }
 }
 
-template <bool kTiled>
+template <bool kTiled, bool kBalance, bool kSpeculate>
 __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
     const uint16_t* __restrict__ w2, const int* __restrict__ counts,
@@ -361,6 +538,9 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     int H, int I, int m, int n_pairs) {
   __shared__ uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
   __shared__ int pid[kNT];
+  __shared__ int wp[kMaxExperts + 1];
+  __shared__ uint32_t scan[34];
+  __shared__ int verdict[kWv];
   const int tpe = (H + 15) / 16;
   const int n_act = *n_active_p;
 
@@ -392,25 +572,68 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   };
 
   // Speculate a fully active pool, as in gate_up_wave_kernel.
-  int r_lo, r_hi;
-  block_range(m * tpe, &r_lo, &r_hi);
-  Segment sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
-  begin_segment(sg);
-  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
-  const bool all = n_act == m;
-  if (!all) {
-    block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo >= r_hi) return;
-    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+  // (Without kSpeculate the first segment waits for n_active instead.)
+  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
+  int r_lo = 0, r_hi = 0;
+  Segment sg;
+  if constexpr (kSpeculate) {
+    block_range(m * tpe, &r_lo, &r_hi);
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
     begin_segment(sg);
-  } else if (r_lo >= r_hi) {
-    return;
+  }
+  if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
+  if constexpr (!kSpeculate) block_range(n_act * tpe, &r_lo, &r_hi);
+  const bool all = n_act == m;
+  // With kBalance, whether some expert needs several token passes is
+  // decided once, by the first barrier of the block's first pass (so that
+  // pass's pair-id loads are already out); a block without such a barrier
+  // decides it here.  With several passes the block switches to its range
+  // of the weighted walk.
+  bool checked = !kBalance, weighted = false;
+  int w_hi = 0;
+  auto go_weighted = [&]() {
+    weighted = true;
+    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, wp, scan);
+    block_range(wp[n_act], &r_lo, &w_hi);
+    if (r_lo >= w_hi) return false;
+    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    begin_segment(sg);
+    return true;
+  };
+  if constexpr (!kBalance) {
+    if (!all) {
+      block_range(n_act * tpe, &r_lo, &r_hi);
+      if (r_lo >= r_hi) return;
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
+      begin_segment(sg);
+    } else if (r_lo >= r_hi) {
+      return;
+    }
+  } else {
+    if (kSpeculate && !all) block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo < r_hi && (!kSpeculate || !all)) {
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
+      begin_segment(sg);
+    }
+    if (r_lo >= r_hi) {
+      checked = true;
+      if (!some_expert_needs_passes(pc, verdict) || !go_weighted()) return;
+    }
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
-    for (int p0 = 0; p0 < sg.cnt; p0 += kNT) {
-      if (p0 > 0) {
+    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
+      checked = true;
+      if (some_expert_needs_passes(pc, verdict)) {
+        if (!go_weighted()) return;
+        continue;
+      }
+    }
+    const int p_end = weighted ? min(sg.cnt, sg.p0 + kNT) : sg.cnt;
+    bool restart = false;
+    for (int p0 = sg.p0; p0 < p_end; p0 += kNT) {
+      if (p0 > sg.p0) {
 #pragma unroll
         for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
       }
@@ -423,7 +646,15 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
+      if (!checked) post_passes_verdict(pc, verdict);
       __syncthreads();  // the previous pass's readers of hs and pid are done
+      if (!checked) {
+        checked = true;
+        if (read_passes_verdict(verdict)) {
+          restart = true;
+          break;
+        }
+      }
       if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
       const int row8 = I / 8;
       for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
@@ -451,8 +682,17 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         }
       }
     }
-    if (sg.hi >= r_hi) break;
-    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    if (restart) {
+      if (!go_weighted()) return;
+      continue;
+    }
+    if (weighted) {
+      if (sg.w_end >= w_hi) break;
+      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    } else {
+      if (sg.hi >= r_hi) break;
+      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    }
     begin_segment(sg);
   }
 }
@@ -493,6 +733,25 @@ __global__ __launch_bounds__(256) void pack_w2_kernel(const uint16_t* __restrict
   *reinterpret_cast<u32x4*>(dst + f * 8) = ld128(src + e * H * I + (size_t)row * I + col);
 }
 
+// Variant of a launch.  An expert receives at most one pair per token of a
+// routed batch, so a batch of T tokens gives an expert at most ceil(T / kNT)
+// passes; the weighted walk (and the check that selects it, which costs a
+// little on every launch) is compiled in once that bound exceeds two, where
+// one popular expert could otherwise make a few blocks take three or more
+// times as long as the rest.  Guessing a fully active pool pays when the
+// expected number of idle experts, m (1 - k/m)^T, is well below one.
+struct WaveMode {
+  bool balance, speculate;
+};
+
+WaveMode wave_mode(int T, int m, int k) {
+  WaveMode md;
+  md.balance = T > 2 * kNT;
+  const double idle = m * std::pow(1.0 - (double)k / m, (double)T);
+  md.speculate = !md.balance || idle < 0.25;
+  return md;
+}
+
 int stream_grid() {
   int dev = 0, cus = 256;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -512,12 +771,18 @@ hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bo
                                const int* counts, const int* offsets, const int* perm,
                                const int* active, const int* n_active, int H, int I, int m, int k,
                                uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
-  if (tiled)
-    gate_up_wave_kernel<true><<<stream_grid(), kBlk, 0, stream>>>(
-        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
-  else
-    gate_up_wave_kernel<false><<<stream_grid(), kBlk, 0, stream>>>(
-        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
+  const WaveMode md = wave_mode(T, m, k);
+#define SW_GU(TI, BA, SP)                                                                      \
+  gate_up_wave_kernel<TI, BA, SP><<<stream_grid(), kBlk, 0, stream>>>(                          \
+      x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k)
+  if (!md.balance) {
+    if (tiled) SW_GU(true, false, true); else SW_GU(false, false, true);
+  } else if (md.speculate) {
+    if (tiled) SW_GU(true, true, true); else SW_GU(false, true, true);
+  } else {
+    if (tiled) SW_GU(true, true, false); else SW_GU(false, true, false);
+  }
+#undef SW_GU
   return hipGetLastError();
 }
 
@@ -525,12 +790,18 @@ hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* co
                             const int* offsets, const int* perm, const int* active,
                             const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
                             const uint16_t* h_lo, float* y, hipStream_t stream) {
-  if (tiled)
-    down_wave_kernel<true><<<stream_grid(), kBlk, 0, stream>>>(
-        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
-  else
-    down_wave_kernel<false><<<stream_grid(), kBlk, 0, stream>>>(
-        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
+  const WaveMode md = wave_mode(T, m, k);
+#define SW_DN(TI, BA, SP)                                                                      \
+  down_wave_kernel<TI, BA, SP><<<stream_grid(), kBlk, 0, stream>>>(                             \
+      h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k)
+  if (!md.balance) {
+    if (tiled) SW_DN(true, false, true); else SW_DN(false, false, true);
+  } else if (md.speculate) {
+    if (tiled) SW_DN(true, true, true); else SW_DN(false, true, true);
+  } else {
+    if (tiled) SW_DN(true, true, false); else SW_DN(false, true, false);
+  }
+#undef SW_DN
   return hipGetLastError();
 }
 

@@ -294,6 +294,23 @@ def test_popular_expert_spans_several_token_passes(sw):
     assert int(host(s["gpu"]["plan"].counts)[3]) == 200
 
 
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
+    (512, 16, 2, 96, 300, (3, 7)),   # two experts take every token: 10 passes each,
+                                     # 2 of 16 experts active (first segment guessed, redone)
+    (256, 64, 2, 64, 100, (5,)),     # one expert with 4 passes among ~50 light ones
+                                     # (no guess: many idle experts expected)
+])
+def test_weighted_walk_over_popular_experts(sw, hidden, n_experts, top_k, inter, tokens, popular):
+    # batches above two passes per expert balance the decode kernels' blocks
+    # by tile passes instead of tiles
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=13)
+    bias = np.zeros(n_experts, np.float32)
+    bias[list(popular)] = 50.0
+    s = check_layer(sw, cfg, L, D, None, bias=bias)
+    counts = host(s["gpu"]["plan"].counts)
+    assert all(int(counts[e]) == tokens for e in popular)
+
+
 def test_bias_and_mask_together(sw):
     cfg = I.CONFIGS["skewed_stack"]
     small = I.MoEConfig("skew_small", cfg.config_id, hidden=256, n_experts=cfg.n_experts,
