@@ -799,7 +799,7 @@ static int stream_blocks(int per_cu) {
 hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                           const int* counts, const int* offsets, const int* perm,
                           const int* active, const int* n_active, int H, int I, int m, int k,
-                          void* workspace, hipStream_t stream) {
+                          void* workspace, hipStream_t stream, bool identity_plan) {
   if (T == 0) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
   if (prefill_supported(T, H, I, m, k))
@@ -807,7 +807,7 @@ hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool ti
                                   I, m, k, ws.h_hi, ws.h_lo, stream);
   if (skinny_gate_up_supported(T, H, I, m, k))
     return launch_gate_up_skinny(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I,
-                                 m, k, ws.h_hi, ws.h_lo, stream);
+                                 m, k, ws.h_hi, ws.h_lo, identity_plan, stream);
   // the tiled layout is only produced for shapes the wave kernels take
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_gate_up_wave(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m,
@@ -846,7 +846,7 @@ static void launch_down_t(const ForwardWs& ws, const uint16_t* w2, const int* co
 hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        const int* offsets, const int* perm, const int* active,
                        const int* n_active, int H, int I, int m, int k, void* workspace,
-                       hipStream_t stream) {
+                       hipStream_t stream, bool identity_plan) {
   if (T == 0) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
   if (prefill_supported(T, H, I, m, k))
@@ -854,7 +854,7 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                                ws.h_hi, ws.h_lo, ws.y, stream);
   if (skinny_down_supported(T, H, I, m, k))
     return launch_down_skinny(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
-                              ws.h_hi, ws.h_lo, ws.y, stream);
+                              ws.h_hi, ws.h_lo, ws.y, identity_plan, stream);
   if (tiled || wave_stream_supported(T, H, I, k))
     return launch_down_wave(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                             ws.h_hi, ws.h_lo, ws.y, stream);

@@ -6,9 +6,9 @@
 // With far fewer 16-row tiles than the chip has waves, giving each wave
 // whole tiles leaves most waves idle and the step waits on one long stream
 // per wave.  Here the contraction of a tile is split over S waves of a
-// block (S = 8, 4, 2 or 1, chosen so that every wave still reads at least
-// six 1 KiB K steps): wave w of the block works on tile slot w / S and K
-// slice w % S.  A wave streams its slice of the tile's weights with all of
+// block (S a power of two up to the block's 8 or 16 waves, chosen so that
+// every wave still reads a few 1 KiB K steps): wave w of the block works on
+// tile slot w / S and K slice w % S.  A wave streams its slice of the tile's weights with all of
 // its loads in flight at once and multiplies it with the matching slice of
 // the tokens' activations, read straight from L2 (no LDS staging: every
 // activation element is used by one wave only).  The S partial tiles meet
@@ -25,9 +25,13 @@
 namespace sw {
 namespace {
 
-constexpr int kWv = 8;         // waves per block
-constexpr int kBlk = 64 * kWv;
-constexpr int kKS = 8;         // K steps (32 wide) loaded per round per wave
+// Block shape per token-block count: passes of 64 tokens (NB = 4) hold
+// four times the activation fragments per K step, so they take 16 waves of
+// 4 K steps per round; narrower passes take 8 waves of 8 steps.
+template <int NB>
+constexpr int waves_of() { return NB == 4 ? 16 : 8; }
+template <int NB>
+constexpr int steps_of() { return NB == 4 ? 4 : 8; }
 
 // The expert of tile `tile` as the active list holds it, read without
 // waiting for n_active (any entry below m is safe to read): the first
@@ -73,14 +77,16 @@ __device__ __forceinline__ int group_max_count(int grp, int tps, int n_tiles, in
 // gate/up + SwiGLU
 
 template <int NB, bool kTiled>
-__global__ __launch_bounds__(kBlk, 1) void gate_up_skinny_kernel(
+__global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
     const int* __restrict__ counts, const int* __restrict__ offsets,
     const int* __restrict__ perm, const int* __restrict__ active,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
-    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs, int S) {
+    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs, int S, int identity) {
   constexpr int kNT = 16 * NB;
+  constexpr int kWv = waves_of<NB>(), kKS = steps_of<NB>();
   __shared__ f32x4 red[kWv][NB][kWave];
+  __shared__ int pid_s[kWv][kNT];  // per tile slot: the pass's pair ids
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, kg = lane >> 4;
@@ -128,23 +134,25 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_skinny_kernel(
     const auto hl = make_rsrc(h_lo + (size_t)base * I, hbytes);
 
     for (int p0 = 0; p0 < maxcnt; p0 += kNT) {
-      if (!first) __syncthreads();  // the previous pass's readers of red are done
+      if (!first) __syncthreads();  // the previous pass's readers of red and pid_s are done
       first = false;
       const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
-      // activation row of column r of each 16-token block: x[pair / k].  The
-      // pair ids are read with wave-uniform (scalar) loads, which do not
-      // wait behind the weight loads already in flight; the index is clamped
-      // into the array and the value used only for slots below cnt.
+      // the pass's pair ids: one load per lane by the slot's first wave, into
+      // LDS (an identity plan, the shared expert's, needs none)
+      if (!identity) {
+        if (slice == 0 && lane < kNT) {
+          const int sl = p0 + lane;
+          const int p = sl < cnt ? perm[base + sl] : -1;
+          pid_s[slot][lane] = (p >= 0 && p < n_pairs) ? p : -1;
+        }
+        __syncthreads();
+      }
+      // activation row of column r of each 16-token block: x[pair / k]
       uint32_t xrow[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
-        int p = -1;
-#pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int v = perm[min(base + p0 + nb * 16 + j, n_pairs - 1)];
-          p = r == j ? v : p;
-        }
         const int sl = p0 + nb * 16 + r;
+        const int p = identity ? base + sl : pid_s[slot][nb * 16 + r];
         xrow[nb] = (nb < nbn && sl < cnt && p >= 0 && p < n_pairs)
                        ? (uint32_t)(p / k) * H * 2u + kg * 16u : kOutOfRange;
       }
@@ -171,12 +179,14 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_skinny_kernel(
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
       __syncthreads();
-      if (slice == 0 && nbn > 0) {
+      // token block nb of the slot is finished by its wave nb % S (slice order)
+      if (slice < NB && nbn > 0) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          if (nb < nbn) {
-            f32x4 g4 = red[wave][nb][lane];
-            for (int q = 1; q < S; ++q) g4 += red[wave + q][nb][lane];
+          if (nb < nbn && nb % S == slice) {
+            const int w0 = slot * S;
+            f32x4 g4 = red[w0][nb][lane];
+            for (int q = 1; q < S; ++q) g4 += red[w0 + q][nb][lane];
             f32x4 u4;
 #pragma unroll
             for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
@@ -208,15 +218,17 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_skinny_kernel(
 // down projection
 
 template <int NB, bool kTiled>
-__global__ __launch_bounds__(kBlk, 1) void down_skinny_kernel(
+__global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
     const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
     const uint16_t* __restrict__ w2, const int* __restrict__ counts,
     const int* __restrict__ offsets, const int* __restrict__ perm,
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
-    int H, int I, int m, int n_pairs, int S) {
+    int H, int I, int m, int n_pairs, int S, int identity) {
   constexpr int kNT = 16 * NB;
-  constexpr int kHS = kKS / 2;  // two MFMAs (hi, lo) per weight load
+  constexpr int kWv = waves_of<NB>();
+  constexpr int kHS = steps_of<NB>() / 2;  // two MFMAs (hi, lo) per weight load
   __shared__ f32x4 red[kWv][NB][kWave];
+  __shared__ int pid_s[kWv][kNT];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r = lane & 15, kg = lane >> 4;
@@ -266,15 +278,18 @@ __global__ __launch_bounds__(kBlk, 1) void down_skinny_kernel(
       first = false;
       const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
       // h rows of the pass are the dispatch slots base + p0 + nb * 16 + r;
-      // the pair ids (y rows) are loaded now and used by the epilogue
+      // the pair ids (y rows, for the epilogue) go to LDS as in gate/up
+      if (!identity && slice == 0 && lane < kNT) {
+        const int sl = p0 + lane;
+        const int p = sl < cnt ? perm[base + sl] : -1;
+        pid_s[slot][lane] = (p >= 0 && p < n_pairs) ? p : -1;
+      }
       uint32_t hrow[NB];
-      int pid[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) {
         const int sl = p0 + nb * 16 + r;
         const bool in = nb < nbn && sl < cnt;
         hrow[nb] = in ? (uint32_t)(base + sl) * I * 2u + kg * 16u : kOutOfRange;
-        pid[nb] = in ? perm[base + sl] : -1;
       }
       f32x4 acc[NB];
 #pragma unroll
@@ -303,14 +318,16 @@ __global__ __launch_bounds__(kBlk, 1) void down_skinny_kernel(
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
       __syncthreads();
-      if (slice == 0 && nbn > 0) {
+      if (slice < NB && nbn > 0) {
         const int o = ib * 16 + kg * 4;
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
-          if (nb < nbn) {
-            f32x4 c = red[wave][nb][lane];
-            for (int q = 1; q < S; ++q) c += red[wave + q][nb][lane];
-            const int p = pid[nb];
+          if (nb < nbn && nb % S == slice) {
+            const int w0 = slot * S;
+            f32x4 c = red[w0][nb][lane];
+            for (int q = 1; q < S; ++q) c += red[w0 + q][nb][lane];
+            const int sl = p0 + nb * 16 + r;
+            const int p = sl >= cnt ? -1 : identity ? base + sl : pid_s[slot][nb * 16 + r];
             uint32_t off = kOutOfRange;
             if (p >= 0 && p < n_pairs) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
             __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, c), yr, off, 0, 0);
@@ -321,11 +338,11 @@ __global__ __launch_bounds__(kBlk, 1) void down_skinny_kernel(
   }
 }
 
-// K split: the largest S in {8, 4, 2, 1} that leaves every wave at least six
-// K steps.
-int split_factor(int nsteps) {
-  int s = 8;
-  while (s > 1 && nsteps / s < 6) s >>= 1;
+// K split of a block of wv waves: the largest S in {wv, wv/2, ..., 1} that
+// leaves every wave at least min_steps K steps.
+int split_factor(int nsteps, int wv, int min_steps) {
+  int s = wv;
+  while (s > 1 && nsteps / s < min_steps) s >>= 1;
   return s;
 }
 
@@ -335,8 +352,8 @@ int token_blocks(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : 4; }
 // Upper bound of the active experts of a call.
 int64_t max_active(int T, int m, int k) { return std::min<int64_t>(m, (int64_t)T * k); }
 
-int skinny_grid(int64_t tiles, int S) {
-  const int64_t groups = (tiles + kWv / S - 1) / (kWv / S);
+int skinny_grid(int64_t tiles, int wv, int S) {
+  const int64_t groups = (tiles + wv / S - 1) / (wv / S);
   return (int)std::max<int64_t>(1, std::min<int64_t>(groups, 4096));
 }
 
@@ -357,72 +374,79 @@ bool skinny_down_supported(int T, int H, int I, int m, int k) {
 }
 
 template <int NB>
-static void gate_up_skinny(int grid, const uint16_t* x, const uint16_t* w13, bool tiled,
+static void gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                            const int* counts, const int* offsets, const int* perm,
                            const int* active, const int* n_active, int H, int I, int m, int k,
-                           int n_pairs, int S, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+                           uint16_t* h_hi, uint16_t* h_lo, bool identity, hipStream_t stream) {
+  constexpr int wv = waves_of<NB>();
+  const int S = split_factor(H / 32, wv, NB == 4 ? 4 : 6);
+  const int grid = skinny_grid(max_active(T, m, k) * (I / 8), wv, S);
   if (tiled)
-    gate_up_skinny_kernel<NB, true><<<grid, kBlk, 0, stream>>>(
-        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, n_pairs, S);
+    gate_up_skinny_kernel<NB, true><<<grid, 64 * wv, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k, S,
+        identity ? 1 : 0);
   else
-    gate_up_skinny_kernel<NB, false><<<grid, kBlk, 0, stream>>>(
-        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, n_pairs, S);
+    gate_up_skinny_kernel<NB, false><<<grid, 64 * wv, 0, stream>>>(
+        x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k, S,
+        identity ? 1 : 0);
 }
 
 hipError_t launch_gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                                  const int* counts, const int* offsets, const int* perm,
                                  const int* active, const int* n_active, int H, int I, int m,
-                                 int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
-  const int S = split_factor(H / 32);
-  const int grid = skinny_grid(max_active(T, m, k) * (I / 8), S);
+                                 int k, uint16_t* h_hi, uint16_t* h_lo, bool identity,
+                                 hipStream_t stream) {
   switch (token_blocks(T)) {
     case 1:
-      gate_up_skinny<1>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
-                        T * k, S, h_hi, h_lo, stream);
+      gate_up_skinny<1>(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        h_hi, h_lo, identity, stream);
       break;
     case 2:
-      gate_up_skinny<2>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
-                        T * k, S, h_hi, h_lo, stream);
+      gate_up_skinny<2>(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        h_hi, h_lo, identity, stream);
       break;
     default:
-      gate_up_skinny<4>(grid, x, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
-                        T * k, S, h_hi, h_lo, stream);
+      gate_up_skinny<4>(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
+                        h_hi, h_lo, identity, stream);
   }
   return hipGetLastError();
 }
 
 template <int NB>
-static void down_skinny(int grid, const uint16_t* w2, bool tiled, const int* counts,
+static void down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
                         const int* offsets, const int* perm, const int* active,
-                        const int* n_active, int H, int I, int m, int n_pairs, int S,
-                        const uint16_t* h_hi, const uint16_t* h_lo, float* y, hipStream_t stream) {
+                        const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
+                        const uint16_t* h_lo, float* y, bool identity, hipStream_t stream) {
+  constexpr int wv = waves_of<NB>();
+  const int S = split_factor(I / 32, wv, NB == 4 ? 2 : 6);
+  const int grid = skinny_grid(max_active(T, m, k) * (H / 16), wv, S);
   if (tiled)
-    down_skinny_kernel<NB, true><<<grid, kBlk, 0, stream>>>(
-        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, n_pairs, S);
+    down_skinny_kernel<NB, true><<<grid, 64 * wv, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k, S,
+        identity ? 1 : 0);
   else
-    down_skinny_kernel<NB, false><<<grid, kBlk, 0, stream>>>(
-        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, n_pairs, S);
+    down_skinny_kernel<NB, false><<<grid, 64 * wv, 0, stream>>>(
+        h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k, S,
+        identity ? 1 : 0);
 }
 
 hipError_t launch_down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
                               const int* offsets, const int* perm, const int* active,
                               const int* n_active, int H, int I, int m, int k,
                               const uint16_t* h_hi, const uint16_t* h_lo, float* y,
-                              hipStream_t stream) {
-  const int S = split_factor(I / 32);
-  const int grid = skinny_grid(max_active(T, m, k) * (H / 16), S);
+                              bool identity, hipStream_t stream) {
   switch (token_blocks(T)) {
     case 1:
-      down_skinny<1>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
-                     h_hi, h_lo, y, stream);
+      down_skinny<1>(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k, h_hi,
+                     h_lo, y, identity, stream);
       break;
     case 2:
-      down_skinny<2>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
-                     h_hi, h_lo, y, stream);
+      down_skinny<2>(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k, h_hi,
+                     h_lo, y, identity, stream);
       break;
     default:
-      down_skinny<4>(grid, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, T * k, S,
-                     h_hi, h_lo, y, stream);
+      down_skinny<4>(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k, h_hi,
+                     h_lo, y, identity, stream);
   }
   return hipGetLastError();
 }

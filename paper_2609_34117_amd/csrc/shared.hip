@@ -108,11 +108,12 @@ hipError_t launch_shared_expert(const uint16_t* x, int T, const uint16_t* w13, c
                                                       s.perm, s.active, s.n_active, s.gates);
   hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
+  // the one-expert plan is the identity (perm[t] = t)
   err = launch_gate_up(x, T, w13, tiled, s.counts, s.offsets, s.perm, s.active, s.n_active, H, I,
-                       1, 1, s.fwd, stream);
+                       1, 1, s.fwd, stream, true);
   if (err != hipSuccess) return err;
   err = launch_down(T, w2, tiled, s.counts, s.offsets, s.perm, s.active, s.n_active, H, I, 1, 1,
-                    s.fwd, stream);
+                    s.fwd, stream, true);
   if (err != hipSuccess) return err;
   const float* y = static_cast<const float*>(forward_y(s.fwd, T, H, I));
   const size_t threads = (size_t)T * (H / 4);

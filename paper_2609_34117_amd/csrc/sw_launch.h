@@ -56,14 +56,16 @@ hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, cons
                                  int* active, int* n_active, void* workspace, hipStream_t stream);
 
 // `tiled`: weights in the fragment-major layout of sw_moe_pack_experts.
+// `identity_plan`: the caller guarantees perm[offsets[e] + s] = offsets[e] + s
+// (the shared expert's one-expert plan), so kernels may skip reading perm.
 hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                           const int* counts, const int* offsets, const int* perm,
                           const int* active, const int* n_active, int H, int I, int m, int k,
-                          void* workspace, hipStream_t stream);
+                          void* workspace, hipStream_t stream, bool identity_plan = false);
 hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        const int* offsets, const int* perm, const int* active,
                        const int* n_active, int H, int I, int m, int k, void* workspace,
-                       hipStream_t stream);
+                       hipStream_t stream, bool identity_plan = false);
 bool wave_stream_supported(int T, int H, int I, int k);
 hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                                const int* counts, const int* offsets, const int* perm,
@@ -92,12 +94,13 @@ bool skinny_down_supported(int T, int H, int I, int m, int k);
 hipError_t launch_gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                                  const int* counts, const int* offsets, const int* perm,
                                  const int* active, const int* n_active, int H, int I, int m,
-                                 int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
+                                 int k, uint16_t* h_hi, uint16_t* h_lo, bool identity,
+                                 hipStream_t stream);
 hipError_t launch_down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
                               const int* offsets, const int* perm, const int* active,
                               const int* n_active, int H, int I, int m, int k,
                               const uint16_t* h_hi, const uint16_t* h_lo, float* y,
-                              hipStream_t stream);
+                              bool identity, hipStream_t stream);
 hipError_t launch_pack_experts(const uint16_t* w13, const uint16_t* w2, uint16_t* w13_t,
                                uint16_t* w2_t, int H, int I, int m, hipStream_t stream);
 hipError_t launch_combine(int T, const float* topk_w, const int* n_active, float* out, int H,
