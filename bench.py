@@ -66,15 +66,15 @@ N_COPIES = 4
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
 # `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
-# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197790.9 KiB x
-# 1.99983 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
-# of 192-768 MiB) + WRITE_SIZE 1569.2 KiB x 1.0 (WRITE_SIZE of the copies is
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197801.8 KiB x
+# 1.99985 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
+# of 192-768 MiB) + WRITE_SIZE 1571.3 KiB x 1.0 (WRITE_SIZE of the copies is
 # exact).  The figure holds while the gate/up kernel's sources hash as below.
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="8bb2b36121af059b70b890ab30791ecd34d43d69e4d24d80e5737630c38cd9af",
+GATE_UP_TRAFFIC = dict(sources_sha256="64bba2e1cc5c90c5cc41969d2a8c99f4bca6aed784a6cddec2b5c59c5e91f2f7",
                        workload=("decode_b64", 64, 0.5, "tiled"),
-                       bytes_per_launch=int(round((197790.9 * 1.99983 + 1569.2) * 1024)))
+                       bytes_per_launch=int(round((197801.8 * 1.99985 + 1571.3) * 1024)))
 
 
 def parse():
