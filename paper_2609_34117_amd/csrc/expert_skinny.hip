@@ -19,6 +19,8 @@
 // the batch size (an expert receives at most one pair per token), and the
 // pass count of a block is the largest of its tiles', the same in every
 // wave, so the barriers stay block-uniform.
+#include <climits>
+
 #include "sw_device.h"
 #include "sw_launch.h"
 
@@ -32,6 +34,12 @@ template <int NB>
 constexpr int waves_of() { return NB == 4 ? 16 : 8; }
 template <int NB>
 constexpr int steps_of() { return NB == 4 ? 4 : 8; }
+// Whether a gate/up block loads its next group's first weights during the
+// current group's last pass.  64-token passes leave no registers for it.
+// The down kernel does not: the registers it takes cost a resident block per
+// compute unit, which is worth more there.
+template <int NB>
+constexpr bool gate_up_prefetches() { return NB < 4; }
 
 // The expert of tile `tile` as the active list holds it, read without
 // waiting for n_active (any entry below m is safe to read): the first
@@ -85,6 +93,7 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs, int S, int identity) {
   constexpr int kNT = 16 * NB;
   constexpr int kWv = waves_of<NB>(), kKS = steps_of<NB>();
+  constexpr bool kPrefetch = gate_up_prefetches<NB>();
   __shared__ f32x4 red[kWv][NB][kWave];
   __shared__ int pid_s[kWv][kNT];  // per tile slot: the pass's pair ids
   const int lane = threadIdx.x & 63;
@@ -97,31 +106,47 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
   const int n_act = *n_active_p;
   bool first = true;
 
+  struct Src {
+    __amdgpu_buffer_rsrc_t w;
+    uint32_t row;
+    int e, ib;
+  };
+  // this wave's weights in group g (the expert read without waiting for
+  // n_active); tiles from `limit` on (past the plan's tiles, once it is
+  // known) get the empty resource and load nothing
+  auto src_of = [&](int g, int limit) {
+    Src c;
+    const int tile = g * tps + slot;
+    const int e = tile < limit ? speculative_expert(tile, tpe, active, m) : -1;
+    const bool e_ok = e >= 0 && e < m;
+    c.e = e;
+    c.ib = tile - (tile / tpe) * tpe;
+    c.w = make_rsrc(w13 + (size_t)(e_ok ? e : 0) * 2 * I * H, e_ok ? 4u * (uint32_t)I * H : 0u);
+    if (kTiled) {
+      c.row = (uint32_t)c.ib * 32u * H + (uint32_t)lane * 16u;
+    } else {
+      const int wrow = r < 8 ? c.ib * 8 + r : I + c.ib * 8 + (r - 8);
+      c.row = (uint32_t)wrow * H * 2u + kg * 16u;
+    }
+    return c;
+  };
+  constexpr uint32_t stride = kTiled ? 1024u : 64u;
+  auto issue = [&](const Src& c, u32x4 (&A)[kKS], int sb) {
+#pragma unroll
+    for (int j = 0; j < kKS; ++j) {
+      const uint32_t off = sb + j < s_hi ? c.row + (uint32_t)(sb + j) * stride : kOutOfRange;
+      A[j] = kTiled ? buf_ld128_stream(c.w, off) : buf_ld128(c.w, off);
+    }
+  };
+  // a block walks several groups: the next group's first round of weights
+  // goes out as soon as the current group's last MFMAs have read theirs
+  u32x4 A[kKS];
+  Src cur = src_of(blockIdx.x, INT_MAX);
+  issue(cur, A, s_lo);
+
   for (int grp = blockIdx.x;; grp += gridDim.x) {
     const int tile = grp * tps + slot;
-    const int e = speculative_expert(tile, tpe, active, m);
-    const bool e_ok = e >= 0 && e < m;
-    const int ib = tile - (tile / tpe) * tpe;
-    const auto w = make_rsrc(w13 + (size_t)(e_ok ? e : 0) * 2 * I * H,
-                             e_ok ? 4u * (uint32_t)I * H : 0u);
-    uint32_t row, stride;
-    if (kTiled) {
-      row = (uint32_t)ib * 32u * H + (uint32_t)lane * 16u;
-      stride = 1024u;
-    } else {
-      const int wrow = r < 8 ? ib * 8 + r : I + ib * 8 + (r - 8);
-      row = (uint32_t)wrow * H * 2u + kg * 16u;
-      stride = 64u;
-    }
-    auto issue = [&](u32x4 (&A)[kKS], int sb) {
-#pragma unroll
-      for (int j = 0; j < kKS; ++j) {
-        const uint32_t off = sb + j < s_hi ? row + (uint32_t)(sb + j) * stride : kOutOfRange;
-        A[j] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
-      }
-    };
-    u32x4 A[kKS];
-    issue(A, s_lo);
+    const int e = cur.e, ib = cur.ib;
     if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
     const int n_tiles = n_act * tpe;
     if (grp * tps >= n_tiles) break;
@@ -132,8 +157,15 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
     const uint32_t hbytes = 2u * (uint32_t)cnt * (uint32_t)I;
     const auto hh = make_rsrc(h_hi + (size_t)base * I, hbytes);
     const auto hl = make_rsrc(h_lo + (size_t)base * I, hbytes);
+    const bool more = (grp + (int)gridDim.x) * tps < n_tiles;  // a next group
+    Src nxt;
+    if constexpr (kPrefetch) nxt = src_of(grp + gridDim.x, n_tiles);
+    bool prefetched = false;
 
-    for (int p0 = 0; p0 < maxcnt; p0 += kNT) {
+    // at least one pass: every path then consumes the group's first weight
+    // loads (the empty group of an invalid plan stores nothing)
+    int p0 = 0;
+    do {
       if (!first) __syncthreads();  // the previous pass's readers of red and pid_s are done
       first = false;
       const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
@@ -159,8 +191,9 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
       f32x4 acc[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int sb = s_lo; sb < s_hi; sb += kKS) {
-        if (sb != s_lo || p0 != 0) issue(A, sb);
+      int sb = s_lo;  // every slice has at least one K step
+      do {
+        if (sb != s_lo || p0 != 0) issue(cur, A, sb);
         u32x4 B[NB][kKS];
 #pragma unroll
         for (int j = 0; j < kKS; ++j)
@@ -175,6 +208,10 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int j = 0; j < kKS; ++j) acc[nb] = mfma_16x16x32(A[j], B[nb][j], acc[nb]);
+      } while ((sb += kKS) < s_hi);
+      if (kPrefetch && more && p0 + kNT >= maxcnt) {  // the group's last pass
+        issue(nxt, A, s_lo);
+        prefetched = true;
       }
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
@@ -210,6 +247,14 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
           }
         }
       }
+    } while ((p0 += kNT) < maxcnt);
+    if (!more) break;
+    if constexpr (kPrefetch) {
+      if (!prefetched) issue(nxt, A, s_lo);  // a group without passes
+      cur = nxt;
+    } else {
+      cur = src_of(grp + gridDim.x, n_tiles);
+      issue(cur, A, s_lo);
     }
   }
 }
@@ -242,29 +287,41 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
   const int n_act = *n_active_p;
   bool first = true;
 
+  struct Src {
+    __amdgpu_buffer_rsrc_t w;
+    uint32_t row;
+    int e, ib;
+  };
+  // this wave's weights in group g (the expert read without waiting for
+  // n_active); tiles from `limit` on (past the plan's tiles, once it is
+  // known) get the empty resource and load nothing
+  auto src_of = [&](int g, int limit) {
+    Src c;
+    const int tile = g * tps + slot;
+    const int e = tile < limit ? speculative_expert(tile, tpe, active, m) : -1;
+    const bool e_ok = e >= 0 && e < m;
+    c.e = e;
+    c.ib = tile - (tile / tpe) * tpe;
+    c.w = make_rsrc(w2 + (size_t)(e_ok ? e : 0) * H * I, e_ok ? 2u * (uint32_t)H * I : 0u);
+    c.row = kTiled ? (uint32_t)c.ib * 32u * I + (uint32_t)lane * 16u
+                   : (uint32_t)(c.ib * 16 + r) * I * 2u + kg * 16u;
+    return c;
+  };
+  constexpr uint32_t stride = kTiled ? 1024u : 64u;
+  auto issue = [&](const Src& c, u32x4 (&A)[kHS], int sb) {
+#pragma unroll
+    for (int j = 0; j < kHS; ++j) {
+      const uint32_t off = sb + j < s_hi ? c.row + (uint32_t)(sb + j) * stride : kOutOfRange;
+      A[j] = kTiled ? buf_ld128_stream(c.w, off) : buf_ld128(c.w, off);
+    }
+  };
+  u32x4 A[kHS];
+  Src cur = src_of(blockIdx.x, INT_MAX);
+  issue(cur, A, s_lo);
+
   for (int grp = blockIdx.x;; grp += gridDim.x) {
     const int tile = grp * tps + slot;
-    const int e = speculative_expert(tile, tpe, active, m);
-    const bool e_ok = e >= 0 && e < m;
-    const int ib = tile - (tile / tpe) * tpe;
-    const auto w = make_rsrc(w2 + (size_t)(e_ok ? e : 0) * H * I, e_ok ? 2u * (uint32_t)H * I : 0u);
-    uint32_t row, stride;
-    if (kTiled) {
-      row = (uint32_t)ib * 32u * I + (uint32_t)lane * 16u;
-      stride = 1024u;
-    } else {
-      row = (uint32_t)(ib * 16 + r) * I * 2u + kg * 16u;
-      stride = 64u;
-    }
-    auto issue = [&](u32x4 (&A)[kHS], int sb) {
-#pragma unroll
-      for (int j = 0; j < kHS; ++j) {
-        const uint32_t off = sb + j < s_hi ? row + (uint32_t)(sb + j) * stride : kOutOfRange;
-        A[j] = kTiled ? buf_ld128_stream(w, off) : buf_ld128(w, off);
-      }
-    };
-    u32x4 A[kHS];
-    issue(A, s_lo);
+    const int e = cur.e, ib = cur.ib;
     if (n_act <= 0 || n_act > m) return;
     const int n_tiles = n_act * tpe;
     if (grp * tps >= n_tiles) break;
@@ -273,7 +330,10 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
     const int maxcnt =
         tps == 1 ? cnt : group_max_count(grp, tps, n_tiles, tpe, active, counts, offsets, m, n_pairs);
 
-    for (int p0 = 0; p0 < maxcnt; p0 += kNT) {
+    // at least one pass: every path then consumes the group's first weight
+    // loads (the empty group of an invalid plan stores nothing)
+    int p0 = 0;
+    do {
       if (!first) __syncthreads();
       first = false;
       const int nbn = p0 < cnt ? (min(kNT, cnt - p0) + 15) >> 4 : 0;
@@ -294,8 +354,9 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
       f32x4 acc[NB];
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int sb = s_lo; sb < s_hi; sb += kHS) {
-        if (sb != s_lo || p0 != 0) issue(A, sb);
+      int sb = s_lo;  // every slice has at least one K step
+      do {
+        if (sb != s_lo || p0 != 0) issue(cur, A, sb);
         u32x4 BH[NB][kHS], BL[NB][kHS];
 #pragma unroll
         for (int j = 0; j < kHS; ++j)
@@ -314,7 +375,7 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
               acc[nb] = mfma_16x16x32(A[j], BH[nb][j], acc[nb]);
               acc[nb] = mfma_16x16x32(A[j], BL[nb][j], acc[nb]);
             }
-      }
+      } while ((sb += kHS) < s_hi);
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb) red[wave][nb][lane] = acc[nb];
       __syncthreads();
@@ -334,7 +395,10 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void down_skinny_kernel(
           }
         }
       }
-    }
+    } while ((p0 += kNT) < maxcnt);
+    if ((grp + (int)gridDim.x) * tps >= n_tiles) break;
+    cur = src_of(grp + gridDim.x, n_tiles);
+    issue(cur, A, s_lo);
   }
 }
 
@@ -352,9 +416,26 @@ int token_blocks(int T) { return T <= 16 ? 1 : T <= 32 ? 2 : 4; }
 // Upper bound of the active experts of a call.
 int64_t max_active(int T, int m, int k) { return std::min<int64_t>(m, (int64_t)T * k); }
 
+// Blocks of a launch.  Kernels that prefetch get no more than fit on the
+// chip at once: a block with a second group loads that group's first
+// weights during its current group's last pass, where a fresh block would
+// wait for a compute unit to free up.  The others get a block per group.
+template <bool kPrefetch, auto kKernel>
 int skinny_grid(int64_t tiles, int wv, int S) {
-  const int64_t groups = (tiles + wv / S - 1) / (wv / S);
-  return (int)std::max<int64_t>(1, std::min<int64_t>(groups, 4096));
+  const int64_t groups = std::max<int64_t>(1, (tiles + wv / S - 1) / (wv / S));
+  if (!kPrefetch) return (int)std::min<int64_t>(groups, 4096);
+  static const int per_cu = [&] {
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, kKernel, 64 * wv, 0) != hipSuccess)
+      n = 1;
+    return std::max(n, 1);
+  }();
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    cus = 256;
+  const int64_t cap = (int64_t)cus * per_cu;
+  return (int)std::min(groups, cap);
 }
 
 constexpr int kMaxSkinnyTiles = 2048;
@@ -380,15 +461,19 @@ static void gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool t
                            uint16_t* h_hi, uint16_t* h_lo, bool identity, hipStream_t stream) {
   constexpr int wv = waves_of<NB>();
   const int S = split_factor(H / 32, wv, NB == 4 ? 4 : 6);
-  const int grid = skinny_grid(max_active(T, m, k) * (I / 8), wv, S);
-  if (tiled)
-    gate_up_skinny_kernel<NB, true><<<grid, 64 * wv, 0, stream>>>(
+  const int64_t tiles = max_active(T, m, k) * (I / 8);
+  constexpr bool kPf = gate_up_prefetches<NB>();
+  if (tiled) {
+    constexpr auto kern = gate_up_skinny_kernel<NB, true>;
+    kern<<<skinny_grid<kPf, kern>(tiles, wv, S), 64 * wv, 0, stream>>>(
         x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k, S,
         identity ? 1 : 0);
-  else
-    gate_up_skinny_kernel<NB, false><<<grid, 64 * wv, 0, stream>>>(
+  } else {
+    constexpr auto kern = gate_up_skinny_kernel<NB, false>;
+    kern<<<skinny_grid<kPf, kern>(tiles, wv, S), 64 * wv, 0, stream>>>(
         x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k, S,
         identity ? 1 : 0);
+  }
 }
 
 hipError_t launch_gate_up_skinny(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
@@ -419,15 +504,18 @@ static void down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts
                         const uint16_t* h_lo, float* y, bool identity, hipStream_t stream) {
   constexpr int wv = waves_of<NB>();
   const int S = split_factor(I / 32, wv, NB == 4 ? 2 : 6);
-  const int grid = skinny_grid(max_active(T, m, k) * (H / 16), wv, S);
-  if (tiled)
-    down_skinny_kernel<NB, true><<<grid, 64 * wv, 0, stream>>>(
+  const int64_t tiles = max_active(T, m, k) * (H / 16);
+  if (tiled) {
+    constexpr auto kern = down_skinny_kernel<NB, true>;
+    kern<<<skinny_grid<false, kern>(tiles, wv, S), 64 * wv, 0, stream>>>(
         h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k, S,
         identity ? 1 : 0);
-  else
-    down_skinny_kernel<NB, false><<<grid, 64 * wv, 0, stream>>>(
+  } else {
+    constexpr auto kern = down_skinny_kernel<NB, false>;
+    kern<<<skinny_grid<false, kern>(tiles, wv, S), 64 * wv, 0, stream>>>(
         h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k, S,
         identity ? 1 : 0);
+  }
 }
 
 hipError_t launch_down_skinny(int T, const uint16_t* w2, bool tiled, const int* counts,
