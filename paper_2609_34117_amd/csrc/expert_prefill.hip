@@ -21,6 +21,8 @@
 //   - every B fragment read from LDS feeds the MFMAs of both of the wave's
 //     tiles, halving LDS traffic per MFMA.
 // Each output accumulates over K in the same order as the decode kernels.
+#include <type_traits>
+
 #include "sw_device.h"
 #include "sw_launch.h"
 
@@ -34,21 +36,23 @@ constexpr int kTpu = kWv * kTpw;       // tiles per unit
 constexpr int kNB = 10;                // 16-token column blocks per pass
 constexpr int kNT = 16 * kNB;          // tokens per pass
 constexpr int kPad = 8;                // bf16 padding per staged row
+constexpr int kRowsPad = kNT + 32;     // staged rows: the pass's, then a trash area that
+                                       // takes the idle slots of a partial staging round
 
-// gate/up: chunk = 4 K steps (128 columns of x)
-constexpr int kGuKs = 4;
+// gate/up: chunk = 2 K steps (64 columns of x), 3 chunks of weights in flight
+constexpr int kGuKs = 2;
 constexpr int kGuKc = 32 * kGuKs;
-constexpr int kGuDepth = 2;            // weight chunks held in registers per wave
+constexpr int kGuDepth = 4;            // weight chunks held in registers per wave
 constexpr int kGuRow = kGuKc + kPad;   // staged row stride (bf16)
-constexpr int kGuPieces = kNT * kGuKc / 8;                 // 16-byte pieces per chunk
-constexpr int kGuStage = (kGuPieces + kBlk - 1) / kBlk;    // per thread
-// down: chunk = 2 K steps (64 columns of h hi and of h lo)
+constexpr int kGuPpr = kGuKc / 8;      // 16-byte pieces per staged row
+// down: chunk = 2 K steps (64 columns of h hi and of h lo), 1 in flight
+// (finer chunks with more in flight measured slower: a barrier per 32
+// columns costs more than the deeper pipeline gains)
 constexpr int kDnKs = 2;
 constexpr int kDnKc = 32 * kDnKs;
-constexpr int kDnDepth = 3;
+constexpr int kDnDepth = 2;
 constexpr int kDnRow = kDnKc + kPad;
-constexpr int kDnPieces = kNT * kDnKc / 8;                 // per half (hi or lo)
-constexpr int kDnStage = (kDnPieces + kBlk - 1) / kBlk;
+constexpr int kDnPpr = kDnKc / 8;
 
 // Unit u -> (active slot a, tile group grp); the expert and its pair range,
 // validated against the plan.
@@ -81,14 +85,29 @@ __device__ __forceinline__ int unit_slot() {
   return (g & 7) ? b : (b & 7) * (g >> 3) + (b >> 3);
 }
 
-// Pair ids of one pass into LDS (-1 past the expert's count).
-__device__ __forceinline__ void load_pass_ids(const int* perm, int base, int p0, int cnt,
-                                              int n_pairs, int* pid) {
-  if ((int)threadIdx.x < kNT) {
+// Rows of one pass into LDS: the pair id of dispatch slot p0 + i divided by
+// `div` (the token for gate/up, the pair itself for down), -1 past the
+// expert's count and in the trash rows.
+__device__ __forceinline__ void load_pass_rows(const int* perm, int base, int p0, int cnt,
+                                               int n_pairs, int div, int* rows) {
+  if ((int)threadIdx.x < kRowsPad) {
     const int slot = p0 + threadIdx.x;
-    const int p = slot < cnt ? perm[base + slot] : -1;
-    pid[threadIdx.x] = (p >= 0 && p < n_pairs) ? p : -1;
+    const int p = (int)threadIdx.x < kNT && slot < cnt ? perm[base + slot] : -1;
+    rows[threadIdx.x] = (p >= 0 && p < n_pairs) ? p / div : -1;
   }
+}
+
+// Column blocks computed by a pass of nbn blocks: every MFMA loop of a pass
+// runs over a compile-time count (no per-block branch between an LDS read
+// and its MFMAs); blocks past the pass's tokens multiply zero rows.
+template <typename F>
+__device__ __forceinline__ void with_blocks(int nbn, F&& f) {
+  if (nbn <= 4)
+    f(std::integral_constant<int, 4>{});
+  else if (nbn <= 8)
+    f(std::integral_constant<int, 8>{});
+  else
+    f(std::integral_constant<int, kNB>{});
 }
 
 // ---------------------------------------------------------------------------
@@ -120,23 +139,119 @@ __device__ __forceinline__ void gu_issue(__amdgpu_buffer_rsrc_t w, const int (&i
   }
 }
 
-// x pieces of chunk c: thread piece i -> (row i / 16, 8 columns at 8 * (i % 16)).
-__device__ __forceinline__ void gu_stage_load(const uint16_t* __restrict__ x, const int* pid,
-                                              int c, int H, int k, u32x4 (&v)[kGuStage]) {
-#pragma unroll
-  for (int j = 0; j < kGuStage; ++j) {
-    const int i = (int)threadIdx.x + j * kBlk;
-    const int row = i >> 4, c8 = i & 15;
-    const int p = i < kGuPieces ? pid[row] : -1;
-    v[j] = p >= 0 ? ld128(x + (size_t)(p / k) * H + c * kGuKc + c8 * 8) : zero4();
-  }
+// Staged x of a pass of NBK column blocks: thread piece i = tid + j * kBlk
+// -> (row i / kGuPpr, 8 columns at 8 * (i % kGuPpr)) of every chunk; the
+// pieces of a partial last round land in the trash rows.
+template <int NBK>
+constexpr int gu_stage() {
+  constexpr int kSlots = (NBK * 16 * kGuPpr + kBlk - 1) / kBlk * kBlk;
+  static_assert(kSlots / kGuPpr <= kRowsPad, "trash rows hold the idle slots");
+  return kSlots / kBlk;
 }
 
-__device__ __forceinline__ void gu_stage_store(uint16_t* buf, const u32x4 (&v)[kGuStage]) {
+template <bool kTiled, int NBK>
+__device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffer_rsrc_t xr,
+                                        const int (&ib)[kTpw], const int* tok,
+                                        uint16_t (*xs)[kRowsPad * kGuRow],
+                                        __amdgpu_buffer_rsrc_t hh, __amdgpu_buffer_rsrc_t hl,
+                                        int p0, int cnt, int H, int I, int nchunks, int lane) {
+  constexpr int kStage = gu_stage<NBK>();
+  const int r = lane & 15, kg = lane >> 4;
+  // byte offset of each of this thread's x pieces in chunk 0; a row without
+  // a pair keeps an out-of-range offset in every chunk (at most H * 2 bytes
+  // are added to 2^31, still past the resource)
+  uint32_t xoff[kStage];
 #pragma unroll
-  for (int j = 0; j < kGuStage; ++j) {
+  for (int j = 0; j < kStage; ++j) {
     const int i = (int)threadIdx.x + j * kBlk;
-    if (i < kGuPieces) *reinterpret_cast<u32x4*>(buf + (i >> 4) * kGuRow + (i & 15) * 8) = v[j];
+    const int t = tok[i / kGuPpr];
+    xoff[j] = t >= 0 ? ((uint32_t)t * H + (uint32_t)(i % kGuPpr) * 8u) * 2u : kOutOfRange;
+  }
+  auto stage_load = [&](int c, u32x4 (&v)[kStage]) {
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) v[j] = buf_ld128(xr, xoff[j] + (uint32_t)c * kGuKc * 2u);
+  };
+  auto stage_store = [&](uint16_t* buf, const u32x4 (&v)[kStage]) {
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) {
+      const int i = (int)threadIdx.x + j * kBlk;
+      *reinterpret_cast<u32x4*>(buf + (i / kGuPpr) * kGuRow + (i % kGuPpr) * 8) = v[j];
+    }
+  };
+
+  u32x4 A[kGuDepth][kTpw][kGuKs];
+#pragma unroll
+  for (int d = 0; d < kGuDepth - 1; ++d) gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
+  {
+    u32x4 v[kStage];
+    stage_load(0, v);
+    stage_store(xs[0], v);
+  }
+  f32x4 acc[kTpw][NBK];
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t)
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // nchunks is a multiple of kGuDepth: every chunk body below runs, with no
+  // branch between a chunk's loads and their use (a conditional body lets
+  // the compiler sink the loads to it, past the chunk before).  The last
+  // chunk stages a chunk that is never read.
+  for (int c0 = 0; c0 < nchunks; c0 += kGuDepth) {
+#pragma unroll
+    for (int d = 0; d < kGuDepth; ++d) {
+      const int c = c0 + d;
+      __syncthreads();  // chunk c is in LDS; chunk c - 1's buffer is free
+      u32x4 v[kStage];
+      stage_load(c + 1, v);
+      gu_issue<kTiled>(w, ib, c + kGuDepth - 1, nchunks, H, I, lane,
+                       A[(d + kGuDepth - 1) % kGuDepth]);
+      // the loads stay ahead of the chunk's MFMAs (the scheduler would sink
+      // them to their first use to shorten register lifetimes)
+      __builtin_amdgcn_sched_barrier(0);
+      const uint16_t* buf = xs[c & 1];
+#pragma unroll
+      for (int st = 0; st < kGuKs; ++st) {
+#pragma unroll
+        for (int nb = 0; nb < NBK; ++nb) {
+          const u32x4 b = *reinterpret_cast<const u32x4*>(
+              buf + (nb * 16 + r) * kGuRow + st * 32 + kg * 8);
+#pragma unroll
+          for (int t = 0; t < kTpw; ++t) acc[t][nb] = mfma_16x16x32(A[d][t][st], b, acc[t][nb]);
+        }
+      }
+      stage_store(xs[(c + 1) & 1], v);
+    }
+  }
+
+  // SwiGLU of each tile's 8 (gate, up) row pairs; lanes 0-31 own the results
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t) {
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb) {
+      const f32x4 g4 = acc[t][nb];
+      f32x4 u4;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
+      uint16_t hb[4], lb[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float gt = g4[i];
+        const float hv = (gt / (1.0f + expf(-gt))) * u4[i];
+        hb[i] = f32_to_bf16(hv);
+        lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
+      }
+      const u32x2 hw = {(uint32_t)hb[0] | ((uint32_t)hb[1] << 16),
+                        (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
+      const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
+                        (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+      const int slot = p0 + nb * 16 + r;
+      uint32_t off = kOutOfRange;
+      if (lane < 32 && ib[t] >= 0 && slot < cnt)
+        off = ((uint32_t)slot * I + (uint32_t)(ib[t] * 8 + kg * 4)) * 2u;
+      __builtin_amdgcn_raw_buffer_store_b64(hw, hh, off, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b64(lw, hl, off, 0, 0);
+    }
   }
 }
 
@@ -147,15 +262,15 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
     const int* __restrict__ perm, const int* __restrict__ active,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
-  __shared__ uint16_t xs[2][kNT * kGuRow];
-  __shared__ int pid[kNT];
+  __shared__ uint16_t xs[2][kRowsPad * kGuRow];
+  __shared__ int tok[kRowsPad];
   const int n_act = *n_active_p;
   if (n_act <= 0 || n_act > m) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 15, kg = lane >> 4;
   const int tpe = I / 8;                      // tiles per expert
   const int gpe = (tpe + kTpu - 1) / kTpu;    // units per expert
   const int nchunks = H / kGuKc;
+  const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
 
   for (int u = unit_slot(); u < n_act * gpe; u += gridDim.x) {
     const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
@@ -173,83 +288,13 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
 
     for (int p0 = 0; p0 < s.cnt; p0 += kNT) {
       const int nbn = (min(kNT, s.cnt - p0) + 15) >> 4;
-      __syncthreads();  // the previous pass's readers of pid and xs are done
-      load_pass_ids(perm, s.base, p0, s.cnt, n_pairs, pid);
+      __syncthreads();  // the previous pass's readers of tok and xs are done
+      load_pass_rows(perm, s.base, p0, s.cnt, n_pairs, k, tok);
       __syncthreads();
-      u32x4 A[kGuDepth][kTpw][kGuKs];
-#pragma unroll
-      for (int d = 0; d < kGuDepth - 1; ++d) gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
-      {
-        u32x4 v[kGuStage];
-        gu_stage_load(x, pid, 0, H, k, v);
-        gu_stage_store(xs[0], v);
-      }
-      f32x4 acc[kTpw][kNB];
-#pragma unroll
-      for (int t = 0; t < kTpw; ++t)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-      for (int c0 = 0; c0 < nchunks; c0 += kGuDepth) {
-#pragma unroll
-        for (int d = 0; d < kGuDepth; ++d) {
-          const int c = c0 + d;
-          if (c < nchunks) {  // block-uniform
-            __syncthreads();  // chunk c is in LDS; chunk c - 1's buffer is free
-            u32x4 v[kGuStage];
-            const bool next = c + 1 < nchunks;
-            if (next) gu_stage_load(x, pid, c + 1, H, k, v);
-            gu_issue<kTiled>(w, ib, c + kGuDepth - 1, nchunks, H, I, lane,
-                             A[(d + kGuDepth - 1) % kGuDepth]);
-            const uint16_t* buf = xs[c & 1];
-#pragma unroll
-            for (int st = 0; st < kGuKs; ++st) {
-#pragma unroll
-              for (int nb = 0; nb < kNB; ++nb) {
-                if (nb < nbn) {
-                  const u32x4 b = *reinterpret_cast<const u32x4*>(
-                      buf + (nb * 16 + r) * kGuRow + st * 32 + kg * 8);
-#pragma unroll
-                  for (int t = 0; t < kTpw; ++t) acc[t][nb] = mfma_16x16x32(A[d][t][st], b, acc[t][nb]);
-                }
-              }
-            }
-            if (next) gu_stage_store(xs[(c + 1) & 1], v);
-          }
-        }
-      }
-
-      // SwiGLU of each tile's 8 (gate, up) row pairs; lanes 0-31 own the results
-#pragma unroll
-      for (int t = 0; t < kTpw; ++t) {
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) {
-          if (nb < nbn) {
-            const f32x4 g4 = acc[t][nb];
-            f32x4 u4;
-#pragma unroll
-            for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
-            uint16_t hb[4], lb[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float gt = g4[i];
-              const float hv = (gt / (1.0f + expf(-gt))) * u4[i];
-              hb[i] = f32_to_bf16(hv);
-              lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
-            }
-            const u32x2 hw = {(uint32_t)hb[0] | ((uint32_t)hb[1] << 16),
-                              (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
-            const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
-                              (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
-            const int slot = p0 + nb * 16 + r;
-            uint32_t off = kOutOfRange;
-            if (lane < 32 && ib[t] >= 0 && slot < s.cnt)
-              off = ((uint32_t)slot * I + (uint32_t)(ib[t] * 8 + kg * 4)) * 2u;
-            __builtin_amdgcn_raw_buffer_store_b64(hw, hh, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b64(lw, hl, off, 0, 0);
-          }
-        }
-      }
+      with_blocks(nbn, [&](auto nbk) {
+        gu_pass<kTiled, decltype(nbk)::value>(w, xr, ib, tok, xs, hh, hl, p0, s.cnt, H, I,
+                                              nchunks, lane);
+      });
     }
   }
 }
@@ -281,31 +326,115 @@ __device__ __forceinline__ void dn_issue(__amdgpu_buffer_rsrc_t w, const int (&o
   }
 }
 
-// h pieces of chunk c (hi then lo): rows are the pass's dispatch slots,
-// contiguous from base + p0.
-__device__ __forceinline__ void dn_stage_load(const uint16_t* __restrict__ h_hi,
-                                              const uint16_t* __restrict__ h_lo, int base,
-                                              int p0, int cnt, int c, int I,
-                                              u32x4 (&v)[2 * kDnStage]) {
-#pragma unroll
-  for (int j = 0; j < kDnStage; ++j) {
-    const int i = (int)threadIdx.x + j * kBlk;
-    const int row = i >> 3, c8 = i & 7;
-    const bool ok = i < kDnPieces && p0 + row < cnt;
-    const size_t off = (size_t)(base + p0 + row) * I + c * kDnKc + c8 * 8;
-    v[j] = ok ? ld128(h_hi + off) : zero4();
-    v[kDnStage + j] = ok ? ld128(h_lo + off) : zero4();
-  }
+// Staged h of a pass of NBK column blocks: thread piece i = tid + j * kBlk
+// runs over the hi rows' pieces, then the lo rows', then the trash rows of
+// a partial last round.  A wave's 64 pieces lie in one of the three (a half
+// holds a multiple of 64 pieces).
+template <int NBK>
+constexpr int dn_half() { return NBK * 16 * kDnPpr; }
+template <int NBK>
+constexpr int dn_stage() {
+  static_assert(dn_half<NBK>() % kWave == 0, "wave-uniform halves");
+  return (2 * dn_half<NBK>() + kBlk - 1) / kBlk;
 }
 
-__device__ __forceinline__ void dn_stage_store(uint16_t* buf, const u32x4 (&v)[2 * kDnStage]) {
+template <bool kTiled, int NBK>
+__device__ __forceinline__ void dn_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffer_rsrc_t hhr,
+                                        __amdgpu_buffer_rsrc_t hlr, const int (&ob)[kTpw],
+                                        const int* pid, uint16_t (*hs)[2 * kRowsPad * kDnRow],
+                                        __amdgpu_buffer_rsrc_t yr, int base, int p0, int cnt,
+                                        int H, int I, int nchunks, int lane) {
+  constexpr int kStage = dn_stage<NBK>(), kHalf = dn_half<NBK>();
+  const int r = lane & 15, kg = lane >> 4;
+  const int wave0 = __builtin_amdgcn_readfirstlane((int)(threadIdx.x & ~63u));
+  // per piece: its half (0 hi, 1 lo, 2 trash; wave-uniform), its LDS
+  // position and its h offset in chunk 0 (out of range past the expert's
+  // count and for the trash)
+  uint32_t hoff[kStage];
+  int lds[kStage];
 #pragma unroll
-  for (int j = 0; j < kDnStage; ++j) {
+  for (int j = 0; j < kStage; ++j) {
     const int i = (int)threadIdx.x + j * kBlk;
-    if (i < kDnPieces) {
-      uint16_t* dst = buf + (i >> 3) * kDnRow + (i & 7) * 8;
-      *reinterpret_cast<u32x4*>(dst) = v[j];
-      *reinterpret_cast<u32x4*>(dst + kNT * kDnRow) = v[kDnStage + j];
+    const int half = wave0 + j * kBlk < kHalf ? 0 : wave0 + j * kBlk < 2 * kHalf ? 1 : 2;
+    if (half < 2) {
+      const int q = i - half * kHalf, row = q / kDnPpr, c8 = q % kDnPpr;
+      hoff[j] = p0 + row < cnt ? ((uint32_t)(base + p0 + row) * I + (uint32_t)c8 * 8u) * 2u
+                               : kOutOfRange;
+      lds[j] = half * kRowsPad * kDnRow + row * kDnRow + c8 * 8;
+    } else {
+      const int t = i - 2 * kHalf;
+      hoff[j] = kOutOfRange;
+      lds[j] = (kNT + ((t / kDnPpr) & 31)) * kDnRow + (t % kDnPpr) * 8;
+    }
+  }
+  auto stage_load = [&](int c, u32x4 (&v)[kStage]) {
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) {
+      const bool lo = wave0 + j * kBlk >= kHalf;  // wave-uniform
+      v[j] = buf_ld128(lo ? hlr : hhr, hoff[j] + (uint32_t)c * kDnKc * 2u);
+    }
+  };
+  auto stage_store = [&](uint16_t* buf, const u32x4 (&v)[kStage]) {
+#pragma unroll
+    for (int j = 0; j < kStage; ++j) *reinterpret_cast<u32x4*>(buf + lds[j]) = v[j];
+  };
+
+  u32x4 A[kDnDepth][kTpw][kDnKs];
+#pragma unroll
+  for (int d = 0; d < kDnDepth - 1; ++d) dn_issue<kTiled>(w, ob, d, nchunks, H, I, lane, A[d]);
+  {
+    u32x4 v[kStage];
+    stage_load(0, v);
+    stage_store(hs[0], v);
+  }
+  f32x4 acc[kTpw][NBK];
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t)
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // nchunks is a multiple of kDnDepth (as for gate/up)
+  for (int c0 = 0; c0 < nchunks; c0 += kDnDepth) {
+#pragma unroll
+    for (int d = 0; d < kDnDepth; ++d) {
+      const int c = c0 + d;
+      __syncthreads();
+      u32x4 v[kStage];
+      stage_load(c + 1, v);
+      dn_issue<kTiled>(w, ob, c + kDnDepth - 1, nchunks, H, I, lane,
+                       A[(d + kDnDepth - 1) % kDnDepth]);
+      __builtin_amdgcn_sched_barrier(0);  // loads ahead of the chunk's MFMAs
+      const uint16_t* buf = hs[c & 1];
+#pragma unroll
+      for (int st = 0; st < kDnKs; ++st) {
+#pragma unroll
+        for (int nb = 0; nb < NBK; ++nb) {
+          const uint16_t* row = buf + (nb * 16 + r) * kDnRow + st * 32 + kg * 8;
+          const u32x4 bh = *reinterpret_cast<const u32x4*>(row);
+          const u32x4 bl = *reinterpret_cast<const u32x4*>(row + kRowsPad * kDnRow);
+#pragma unroll
+          for (int t = 0; t < kTpw; ++t) {
+            acc[t][nb] = mfma_16x16x32(A[d][t][st], bh, acc[t][nb]);
+            acc[t][nb] = mfma_16x16x32(A[d][t][st], bl, acc[t][nb]);
+          }
+        }
+      }
+      stage_store(hs[(c + 1) & 1], v);
+    }
+  }
+
+  // y rows of the pass's pairs: lane (r, kg) holds output rows
+  // ob * 16 + 4 kg .. + 3 of pair pid[nb * 16 + r]
+#pragma unroll
+  for (int t = 0; t < kTpw; ++t) {
+#pragma unroll
+    for (int nb = 0; nb < NBK; ++nb) {
+      const int p = pid[nb * 16 + r];
+      const int o = ob[t] * 16 + kg * 4;
+      uint32_t off = kOutOfRange;
+      if (ob[t] >= 0 && p >= 0) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[t][nb]), yr, off, 0,
+                                             0);
     }
   }
 }
@@ -317,16 +446,18 @@ __global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
     const int* __restrict__ offsets, const int* __restrict__ perm,
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
     int H, int I, int m, int n_pairs) {
-  __shared__ uint16_t hs[2][2 * kNT * kDnRow];  // [buffer][hi rows, then lo rows]
-  __shared__ int pid[kNT];
+  __shared__ uint16_t hs[2][2 * kRowsPad * kDnRow];  // [buffer][hi rows, then lo rows]
+  __shared__ int pid[kRowsPad];
   const int n_act = *n_active_p;
   if (n_act <= 0 || n_act > m) return;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int r = lane & 15, kg = lane >> 4;
   const int tpe = H / 16;
   const int gpe = (tpe + kTpu - 1) / kTpu;
   const int nchunks = I / kDnKc;
   const auto yr = make_rsrc(y, 4u * (uint32_t)n_pairs * (uint32_t)H);
+  const uint32_t hbytes = 2u * (uint32_t)n_pairs * (uint32_t)I;
+  const auto hhr = make_rsrc(h_hi, hbytes);
+  const auto hlr = make_rsrc(h_lo, hbytes);
 
   for (int u = unit_slot(); u < n_act * gpe; u += gridDim.x) {
     const Unit s = unit_of(u, gpe, active, counts, offsets, m, n_pairs);
@@ -341,71 +472,12 @@ __global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
 
     for (int p0 = 0; p0 < s.cnt; p0 += kNT) {
       const int nbn = (min(kNT, s.cnt - p0) + 15) >> 4;
-      __syncthreads();
-      load_pass_ids(perm, s.base, p0, s.cnt, n_pairs, pid);
-      u32x4 A[kDnDepth][kTpw][kDnKs];
-#pragma unroll
-      for (int d = 0; d < kDnDepth - 1; ++d) dn_issue<kTiled>(w, ob, d, nchunks, H, I, lane, A[d]);
-      {
-        u32x4 v[2 * kDnStage];
-        dn_stage_load(h_hi, h_lo, s.base, p0, s.cnt, 0, I, v);
-        dn_stage_store(hs[0], v);
-      }
-      f32x4 acc[kTpw][kNB];
-#pragma unroll
-      for (int t = 0; t < kTpw; ++t)
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-      for (int c0 = 0; c0 < nchunks; c0 += kDnDepth) {
-#pragma unroll
-        for (int d = 0; d < kDnDepth; ++d) {
-          const int c = c0 + d;
-          if (c < nchunks) {
-            __syncthreads();
-            u32x4 v[2 * kDnStage];
-            const bool next = c + 1 < nchunks;
-            if (next) dn_stage_load(h_hi, h_lo, s.base, p0, s.cnt, c + 1, I, v);
-            dn_issue<kTiled>(w, ob, c + kDnDepth - 1, nchunks, H, I, lane,
-                             A[(d + kDnDepth - 1) % kDnDepth]);
-            const uint16_t* buf = hs[c & 1];
-#pragma unroll
-            for (int st = 0; st < kDnKs; ++st) {
-#pragma unroll
-              for (int nb = 0; nb < kNB; ++nb) {
-                if (nb < nbn) {
-                  const uint16_t* row = buf + (nb * 16 + r) * kDnRow + st * 32 + kg * 8;
-                  const u32x4 bh = *reinterpret_cast<const u32x4*>(row);
-                  const u32x4 bl = *reinterpret_cast<const u32x4*>(row + kNT * kDnRow);
-#pragma unroll
-                  for (int t = 0; t < kTpw; ++t) {
-                    acc[t][nb] = mfma_16x16x32(A[d][t][st], bh, acc[t][nb]);
-                    acc[t][nb] = mfma_16x16x32(A[d][t][st], bl, acc[t][nb]);
-                  }
-                }
-              }
-            }
-            if (next) dn_stage_store(hs[(c + 1) & 1], v);
-          }
-        }
-      }
-
-      // y rows of the pass's pairs: lane (r, kg) holds output rows
-      // ob * 16 + 4 kg .. + 3 of pair pid[nb * 16 + r]
-#pragma unroll
-      for (int t = 0; t < kTpw; ++t) {
-#pragma unroll
-        for (int nb = 0; nb < kNB; ++nb) {
-          if (nb < nbn) {
-            const int p = pid[nb * 16 + r];
-            const int o = ob[t] * 16 + kg * 4;
-            uint32_t off = kOutOfRange;
-            if (ob[t] >= 0 && p >= 0) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
-            __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[t][nb]), yr, off,
-                                                   0, 0);
-          }
-        }
-      }
+      __syncthreads();  // the previous pass's readers of pid and hs are done
+      load_pass_rows(perm, s.base, p0, s.cnt, n_pairs, 1, pid);
+      with_blocks(nbn, [&](auto nbk) {
+        dn_pass<kTiled, decltype(nbk)::value>(w, hhr, hlr, ob, pid, hs, yr, s.base, p0, s.cnt, H,
+                                              I, nchunks, lane);
+      });
     }
   }
 }
@@ -422,8 +494,10 @@ int prefill_grid() {
 
 bool prefill_supported(int T, int H, int I, int m, int k) {
   // about 48 or more tokens per expert over a pool large enough to spread
-  // its units over the chip, whole K chunks, and 32-bit offsets
-  return m >= 16 && (int64_t)T * k >= (int64_t)48 * m && H % kGuKc == 0 && I % kDnKc == 0 &&
+  // its units over the chip, K in whole rounds of the weight pipelines (H
+  // a multiple of 256, I of 128), and 32-bit offsets
+  return m >= 16 && (int64_t)T * k >= (int64_t)48 * m && H % (kGuKc * kGuDepth) == 0 &&
+         I % (kDnKc * kDnDepth) == 0 &&
          H <= 32768 && 4 * (int64_t)T * k * H < ((int64_t)1 << 31);
 }
 
