@@ -43,8 +43,10 @@ constexpr int kRowsPad = kNT + 32;     // staged rows: the pass's, then a trash 
 constexpr int kGuKs = 2;
 constexpr int kGuKc = 32 * kGuKs;
 constexpr int kGuDepth = 4;            // weight chunks held in registers per wave
-constexpr int kGuRow = kGuKc + kPad;   // staged row stride (bf16)
-constexpr int kGuPpr = kGuKc / 8;      // 16-byte pieces per staged row
+constexpr int kXRing = 4;              // staged x chunks in LDS
+constexpr int kXAhead = kXRing - 1;    // chunks of x in flight ahead of the one computed
+constexpr int kSegRows = 8;            // staged rows per 1 KiB direct-to-LDS load of a wave
+static_assert(kGuKc * 2 * kSegRows == 1024, "one wave load fills kSegRows rows");
 // down: chunk = 2 K steps (64 columns of h hi and of h lo), 1 in flight
 // (finer chunks with more in flight measured slower: a barrier per 32
 // columns costs more than the deeper pipeline gains)
@@ -139,100 +141,141 @@ __device__ __forceinline__ void gu_issue(__amdgpu_buffer_rsrc_t w, const int (&i
   }
 }
 
-// Staged x of a pass of NBK column blocks: thread piece i = tid + j * kBlk
-// -> (row i / kGuPpr, 8 columns at 8 * (i % kGuPpr)) of every chunk; the
-// pieces of a partial last round land in the trash rows.
+// x of a pass of NBK column blocks goes straight from memory to LDS
+// (buffer loads with the LDS bit: lane l of a wave writes bytes 16 l .. +15
+// of a 1 KiB segment).  A segment holds kSegRows rows of the chunk's 64
+// columns, unpadded; the 16-byte pieces of row R sit in XOR-swizzled slots,
+// slot = piece ^ x_swizzle(R), so that the MFMA operand reads (16 rows, one
+// piece each, per 16 lanes) hit distinct banks.  Segments run over the
+// pass's rows and then, for a partial last round of the waves, the trash
+// rows.
+__device__ __forceinline__ int x_swizzle(int row) { return (row & 7) ^ ((row >> 3) & 1); }
+
 template <int NBK>
-constexpr int gu_stage() {
-  constexpr int kSlots = (NBK * 16 * kGuPpr + kBlk - 1) / kBlk * kBlk;
-  static_assert(kSlots / kGuPpr <= kRowsPad, "trash rows hold the idle slots");
-  return kSlots / kBlk;
+constexpr int gu_segs() {  // direct-to-LDS loads per wave per chunk
+  constexpr int kSegs = (NBK * 16 / kSegRows + kWv - 1) / kWv;
+  static_assert(kSegs * kWv * kSegRows <= kRowsPad, "trash rows hold the idle segments");
+  return kSegs;
 }
+
+// s_waitcnt immediates: at most n vector-memory loads outstanding (expcnt
+// and lgkmcnt left alone), and the same with every LDS access done
+constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int vmcnt_at_most_lds_done(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
 template <bool kTiled, int NBK>
 __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffer_rsrc_t xr,
                                         const int (&ib)[kTpw], const int* tok,
-                                        uint16_t (*xs)[kRowsPad * kGuRow],
+                                        uint16_t* __restrict__ x0, uint16_t* __restrict__ x1,
+                                        uint16_t* __restrict__ x2, uint16_t* __restrict__ x3,
                                         __amdgpu_buffer_rsrc_t hh, __amdgpu_buffer_rsrc_t hl,
-                                        int p0, int cnt, int H, int I, int nchunks, int lane) {
-  constexpr int kStage = gu_stage<NBK>();
+                                        int p0, int cnt, int H, int I, int nchunks, int lane,
+                                        int wave) {
+  // the ring slots as distinct restrict pointers: the compiler then knows
+  // that the loads into one slot do not write the slot being read, and does
+  // not wait for them before the reads
+  static_assert(kXRing == 4, "four ring slots");
+  auto slot = [&](int k) { return k == 0 ? x0 : k == 1 ? x1 : k == 2 ? x2 : x3; };
+  constexpr int kSegs = gu_segs<NBK>();
+  constexpr int kWloads = kTpw * kGuKs;  // weight loads per wave per chunk
   const int r = lane & 15, kg = lane >> 4;
-  // byte offset of each of this thread's x pieces in chunk 0; a row without
-  // a pair keeps an out-of-range offset in every chunk (at most H * 2 bytes
-  // are added to 2^31, still past the resource)
-  uint32_t xoff[kStage];
+  // source byte offset of this lane's piece of each segment in chunk 0; a
+  // row without a pair reads out of range in every chunk (at most H * 2
+  // bytes are added to 2^31, still past the resource)
+  uint32_t soff[kSegs];
 #pragma unroll
-  for (int j = 0; j < kStage; ++j) {
-    const int i = (int)threadIdx.x + j * kBlk;
-    const int t = tok[i / kGuPpr];
-    xoff[j] = t >= 0 ? ((uint32_t)t * H + (uint32_t)(i % kGuPpr) * 8u) * 2u : kOutOfRange;
+  for (int j = 0; j < kSegs; ++j) {
+    const int row = (wave + j * kWv) * kSegRows + (lane >> 3);
+    const int piece = (lane & 7) ^ x_swizzle(row);
+    const int t = tok[row];
+    soff[j] = t >= 0 ? ((uint32_t)t * H + (uint32_t)piece * 8u) * 2u : kOutOfRange;
   }
-  auto stage_load = [&](int c, u32x4 (&v)[kStage]) {
+  auto stage = [&](int c, int k) {  // chunk c into ring slot k = c % kXRing
+    uint16_t* buf = slot(k);
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) v[j] = buf_ld128(xr, xoff[j] + (uint32_t)c * kGuKc * 2u);
+    for (int j = 0; j < kSegs; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          xr, (__attribute__((address_space(3))) void*)(buf + (wave + j * kWv) * kSegRows * kGuKc),
+          16, soff[j] + (uint32_t)c * kGuKc * 2u, 0, 0, 0);
   };
-  auto stage_store = [&](uint16_t* buf, const u32x4 (&v)[kStage]) {
+  // this lane's operand slot in a staged row, per K step (row & 15 = r)
+  int bslot[kGuKs];
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) {
-      const int i = (int)threadIdx.x + j * kBlk;
-      *reinterpret_cast<u32x4*>(buf + (i / kGuPpr) * kGuRow + (i % kGuPpr) * 8) = v[j];
-    }
-  };
+  for (int st = 0; st < kGuKs; ++st) bslot[st] = ((st * 4 + kg) ^ x_swizzle(r)) * 8;
 
+  // prologue: x chunks 0 .. kXAhead - 1, then weight chunks 0 .. kGuDepth - 2
+#pragma unroll
+  for (int c = 0; c < kXAhead; ++c) stage(c, c);
+  __builtin_amdgcn_sched_barrier(0);  // the load order the waits below count on
   u32x4 A[kGuDepth][kTpw][kGuKs];
 #pragma unroll
   for (int d = 0; d < kGuDepth - 1; ++d) gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
-  {
-    u32x4 v[kStage];
-    stage_load(0, v);
-    stage_store(xs[0], v);
-  }
   f32x4 acc[kTpw][NBK];
 #pragma unroll
   for (int t = 0; t < kTpw; ++t)
 #pragma unroll
     for (int nb = 0; nb < NBK; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // nchunks is a multiple of kGuDepth: every chunk body below runs, with no
-  // branch between a chunk's loads and their use (a conditional body lets
-  // the compiler sink the loads to it, past the chunk before).  The last
-  // chunk stages a chunk that is never read.
+  // Each chunk issues x chunk c + kXAhead and weight chunk c + kGuDepth - 1,
+  // unconditionally (nchunks is a multiple of kGuDepth; past the end the
+  // loads read out of range or land in ring slots never read again), so the
+  // count of loads issued after x chunk c is known: the wait below lets
+  // exactly those stay outstanding.  The compiler does not track the LDS
+  // writes of these loads, hence the explicit wait and a plain barrier
+  // (a __syncthreads fence would wait for every load, weights included).
+  constexpr int kAfter = (kXAhead - 1) * (kSegs + kWloads) + kWloads;
+  static_assert(kGuDepth - 1 == kXAhead && kGuDepth == kXRing,
+                "prologue and steady state leave the same count; ring slot = d");
   for (int c0 = 0; c0 < nchunks; c0 += kGuDepth) {
 #pragma unroll
     for (int d = 0; d < kGuDepth; ++d) {
       const int c = c0 + d;
-      __syncthreads();  // chunk c is in LDS; chunk c - 1's buffer is free
-      u32x4 v[kStage];
-      stage_load(c + 1, v);
+      // this wave's part of chunk c landed and its reads of chunk c - 1 are done
+      __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(kAfter));
+      __builtin_amdgcn_s_barrier();  // so for every wave: chunk c - 1's slot is free
+      stage(c + kXAhead, (d + kXAhead) % kXRing);  // c0 is a multiple of kXRing
+      __builtin_amdgcn_sched_barrier(0);  // x loads first, then the weights (the count)
       gu_issue<kTiled>(w, ib, c + kGuDepth - 1, nchunks, H, I, lane,
                        A[(d + kGuDepth - 1) % kGuDepth]);
       // the loads stay ahead of the chunk's MFMAs (the scheduler would sink
       // them to their first use to shorten register lifetimes)
       __builtin_amdgcn_sched_barrier(0);
-      const uint16_t* buf = xs[c & 1];
+      const uint16_t* buf = slot(d);
 #pragma unroll
       for (int st = 0; st < kGuKs; ++st) {
 #pragma unroll
         for (int nb = 0; nb < NBK; ++nb) {
-          const u32x4 b = *reinterpret_cast<const u32x4*>(
-              buf + (nb * 16 + r) * kGuRow + st * 32 + kg * 8);
+          const u32x4 b =
+              *reinterpret_cast<const u32x4*>(buf + (nb * 16 + r) * kGuKc + bslot[st]);
 #pragma unroll
           for (int t = 0; t < kTpw; ++t) acc[t][nb] = mfma_16x16x32(A[d][t][st], b, acc[t][nb]);
         }
       }
-      stage_store(xs[(c + 1) & 1], v);
     }
   }
+  // the x loads past the last chunk write ring slots that the next pass
+  // stages into: they land before this pass ends
+  __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));
 
-  // SwiGLU of each tile's 8 (gate, up) row pairs; lanes 0-31 own the results
+  // SwiGLU of each tile's 8 (gate, up) row pairs, two column blocks (a, b)
+  // at a time so that every lane finishes an output: lanes 0-31 hold a's
+  // gates and lanes 32-63 a's ups (likewise for b); one exchange across the
+  // halves hands lanes 0-31 a's ups and lanes 32-63 b's gates.  The
+  // arithmetic per output is unchanged.
+  static_assert(NBK % 2 == 0, "column blocks in pairs");
+  const int half = lane >> 5, kgx = (lane >> 4) & 1;
 #pragma unroll
   for (int t = 0; t < kTpw; ++t) {
 #pragma unroll
-    for (int nb = 0; nb < NBK; ++nb) {
-      const f32x4 g4 = acc[t][nb];
-      f32x4 u4;
+    for (int nb = 0; nb < NBK; nb += 2) {
+      f32x4 g4, u4;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
+      for (int i = 0; i < 4; ++i) {
+        const float a = acc[t][nb][i], b = acc[t][nb + 1][i];
+        const float y = __shfl_xor(half ? a : b, 32);  // lanes < 32: a's up; else b's gate
+        g4[i] = half ? y : a;
+        u4[i] = half ? b : y;
+      }
       uint16_t hb[4], lb[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -245,10 +288,9 @@ __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
                         (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
       const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
                         (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
-      const int slot = p0 + nb * 16 + r;
+      const int slot = p0 + (nb + half) * 16 + r;
       uint32_t off = kOutOfRange;
-      if (lane < 32 && ib[t] >= 0 && slot < cnt)
-        off = ((uint32_t)slot * I + (uint32_t)(ib[t] * 8 + kg * 4)) * 2u;
+      if (ib[t] >= 0 && slot < cnt) off = ((uint32_t)slot * I + (uint32_t)(ib[t] * 8 + kgx * 4)) * 2u;
       __builtin_amdgcn_raw_buffer_store_b64(hw, hh, off, 0, 0);
       __builtin_amdgcn_raw_buffer_store_b64(lw, hl, off, 0, 0);
     }
@@ -262,11 +304,15 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
     const int* __restrict__ perm, const int* __restrict__ active,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
-  __shared__ uint16_t xs[2][kRowsPad * kGuRow];
+  __shared__ __attribute__((aligned(1024))) uint16_t xs0[kRowsPad * kGuKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t xs1[kRowsPad * kGuKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t xs2[kRowsPad * kGuKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t xs3[kRowsPad * kGuKc];
   __shared__ int tok[kRowsPad];
   const int n_act = *n_active_p;
   if (n_act <= 0 || n_act > m) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int tpe = I / 8;                      // tiles per expert
   const int gpe = (tpe + kTpu - 1) / kTpu;    // units per expert
   const int nchunks = H / kGuKc;
@@ -292,8 +338,8 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
       load_pass_rows(perm, s.base, p0, s.cnt, n_pairs, k, tok);
       __syncthreads();
       with_blocks(nbn, [&](auto nbk) {
-        gu_pass<kTiled, decltype(nbk)::value>(w, xr, ib, tok, xs, hh, hl, p0, s.cnt, H, I,
-                                              nchunks, lane);
+        gu_pass<kTiled, decltype(nbk)::value>(w, xr, ib, tok, xs0, xs1, xs2, xs3, hh, hl, p0,
+                                              s.cnt, H, I, nchunks, lane, wave);
       });
     }
   }
