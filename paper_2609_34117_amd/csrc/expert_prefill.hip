@@ -42,19 +42,19 @@ constexpr int kRowsPad = kNT + 32;     // staged rows: the pass's, then a trash 
 // gate/up: chunk = 2 K steps (64 columns of x), 3 chunks of weights in flight
 constexpr int kGuKs = 2;
 constexpr int kGuKc = 32 * kGuKs;
-constexpr int kGuDepth = 4;            // weight chunks held in registers per wave
-constexpr int kXRing = 4;              // staged x chunks in LDS
-constexpr int kXAhead = kXRing - 1;    // chunks of x in flight ahead of the one computed
+// Pipeline depth D: D chunks of weights held in registers per wave and D
+// ring slots of staged activations in LDS, so D - 1 chunks of each are in
+// flight ahead of the one computed.  The code takes 2 or 4; 2 measured
+// faster for both kernels (about 4% for gate/up, 14% for down at the
+// 4096-token prefill shape).
+constexpr int kDepth = 2;
 constexpr int kSegRows = 8;            // staged rows per 1 KiB direct-to-LDS load of a wave
 static_assert(kGuKc * 2 * kSegRows == 1024, "one wave load fills kSegRows rows");
-// down: chunk = 2 K steps (64 columns of h hi and of h lo), 1 in flight
-// (finer chunks with more in flight measured slower: a barrier per 32
-// columns costs more than the deeper pipeline gains)
+// down: chunk = 2 K steps (64 columns of h hi and of h lo), 3 in flight;
+// the staged h goes through the same kind of ring as gate/up's x
 constexpr int kDnKs = 2;
 constexpr int kDnKc = 32 * kDnKs;
-constexpr int kDnDepth = 2;
-constexpr int kDnRow = kDnKc + kPad;
-constexpr int kDnPpr = kDnKc / 8;
+static_assert(kDnKc == kGuKc, "one segment geometry for both staged operands");
 
 // Unit u -> (active slot a, tile group grp); the expert and its pair range,
 // validated against the plan.
@@ -88,8 +88,7 @@ __device__ __forceinline__ int unit_slot() {
 }
 
 // Rows of one pass into LDS: the pair id of dispatch slot p0 + i divided by
-// `div` (the token for gate/up, the pair itself for down), -1 past the
-// expert's count and in the trash rows.
+// `div` (k: the token), -1 past the expert's count and in the trash rows.
 __device__ __forceinline__ void load_pass_rows(const int* perm, int base, int p0, int cnt,
                                                int n_pairs, int div, int* rows) {
   if ((int)threadIdx.x < kRowsPad) {
@@ -163,7 +162,7 @@ constexpr int gu_segs() {  // direct-to-LDS loads per wave per chunk
 constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 constexpr int vmcnt_at_most_lds_done(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
-template <bool kTiled, int NBK>
+template <bool kTiled, int D, int NBK>
 __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffer_rsrc_t xr,
                                         const int (&ib)[kTpw], const int* tok,
                                         uint16_t* __restrict__ x0, uint16_t* __restrict__ x1,
@@ -174,7 +173,8 @@ __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
   // the ring slots as distinct restrict pointers: the compiler then knows
   // that the loads into one slot do not write the slot being read, and does
   // not wait for them before the reads
-  static_assert(kXRing == 4, "four ring slots");
+  static_assert(D == 2 || D == 4, "two or four ring slots");
+  constexpr int kAhead = D - 1;
   auto slot = [&](int k) { return k == 0 ? x0 : k == 1 ? x1 : k == 2 ? x2 : x3; };
   constexpr int kSegs = gu_segs<NBK>();
   constexpr int kWloads = kTpw * kGuKs;  // weight loads per wave per chunk
@@ -190,7 +190,7 @@ __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
     const int t = tok[row];
     soff[j] = t >= 0 ? ((uint32_t)t * H + (uint32_t)piece * 8u) * 2u : kOutOfRange;
   }
-  auto stage = [&](int c, int k) {  // chunk c into ring slot k = c % kXRing
+  auto stage = [&](int c, int k) {  // chunk c into ring slot k = c % D
     uint16_t* buf = slot(k);
 #pragma unroll
     for (int j = 0; j < kSegs; ++j)
@@ -203,40 +203,42 @@ __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
 #pragma unroll
   for (int st = 0; st < kGuKs; ++st) bslot[st] = ((st * 4 + kg) ^ x_swizzle(r)) * 8;
 
-  // prologue: x chunks 0 .. kXAhead - 1, then weight chunks 0 .. kGuDepth - 2
+  // prologue: x chunks 0 .. D - 2, then weight chunks 0 .. D - 2
 #pragma unroll
-  for (int c = 0; c < kXAhead; ++c) stage(c, c);
+  for (int c = 0; c < kAhead; ++c) stage(c, c);
   __builtin_amdgcn_sched_barrier(0);  // the load order the waits below count on
-  u32x4 A[kGuDepth][kTpw][kGuKs];
+  u32x4 A[D][kTpw][kGuKs];
 #pragma unroll
-  for (int d = 0; d < kGuDepth - 1; ++d) gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
+  for (int d = 0; d < kAhead; ++d) {  // in chunk order: the waits assume it
+    gu_issue<kTiled>(w, ib, d, nchunks, H, I, lane, A[d]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
   f32x4 acc[kTpw][NBK];
 #pragma unroll
   for (int t = 0; t < kTpw; ++t)
 #pragma unroll
     for (int nb = 0; nb < NBK; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // Each chunk issues x chunk c + kXAhead and weight chunk c + kGuDepth - 1,
-  // unconditionally (nchunks is a multiple of kGuDepth; past the end the
+  // Each chunk issues x chunk c + D - 1 and weight chunk c + D - 1,
+  // unconditionally (nchunks is a multiple of D; past the end the
   // loads read out of range or land in ring slots never read again), so the
   // count of loads issued after x chunk c is known: the wait below lets
   // exactly those stay outstanding.  The compiler does not track the LDS
   // writes of these loads, hence the explicit wait and a plain barrier
   // (a __syncthreads fence would wait for every load, weights included).
-  constexpr int kAfter = (kXAhead - 1) * (kSegs + kWloads) + kWloads;
-  static_assert(kGuDepth - 1 == kXAhead && kGuDepth == kXRing,
-                "prologue and steady state leave the same count; ring slot = d");
-  for (int c0 = 0; c0 < nchunks; c0 += kGuDepth) {
+  // (the prologue leaves the same count ahead of chunk 0 as a chunk body
+  // leaves ahead of chunk c + D - 1, and the ring slot of chunk c is d)
+  constexpr int kAfter = (kAhead - 1) * (kSegs + kWloads) + kWloads;
+  for (int c0 = 0; c0 < nchunks; c0 += D) {
 #pragma unroll
-    for (int d = 0; d < kGuDepth; ++d) {
+    for (int d = 0; d < D; ++d) {
       const int c = c0 + d;
       // this wave's part of chunk c landed and its reads of chunk c - 1 are done
       __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(kAfter));
       __builtin_amdgcn_s_barrier();  // so for every wave: chunk c - 1's slot is free
-      stage(c + kXAhead, (d + kXAhead) % kXRing);  // c0 is a multiple of kXRing
+      stage(c + kAhead, (d + kAhead) % D);  // c0 is a multiple of D
       __builtin_amdgcn_sched_barrier(0);  // x loads first, then the weights (the count)
-      gu_issue<kTiled>(w, ib, c + kGuDepth - 1, nchunks, H, I, lane,
-                       A[(d + kGuDepth - 1) % kGuDepth]);
+      gu_issue<kTiled>(w, ib, c + kAhead, nchunks, H, I, lane, A[(d + kAhead) % D]);
       // the loads stay ahead of the chunk's MFMAs (the scheduler would sink
       // them to their first use to shorten register lifetimes)
       __builtin_amdgcn_sched_barrier(0);
@@ -297,7 +299,7 @@ __device__ __forceinline__ void gu_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
   }
 }
 
-template <bool kTiled>
+template <bool kTiled, int D>
 __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
     const int* __restrict__ counts, const int* __restrict__ offsets,
@@ -338,7 +340,7 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_prefill_kernel(
       load_pass_rows(perm, s.base, p0, s.cnt, n_pairs, k, tok);
       __syncthreads();
       with_blocks(nbn, [&](auto nbk) {
-        gu_pass<kTiled, decltype(nbk)::value>(w, xr, ib, tok, xs0, xs1, xs2, xs3, hh, hl, p0,
+        gu_pass<kTiled, D, decltype(nbk)::value>(w, xr, ib, tok, xs0, xs1, xs2, xs3, hh, hl, p0,
                                               s.cnt, H, I, nchunks, lane, wave);
       });
     }
@@ -372,66 +374,77 @@ __device__ __forceinline__ void dn_issue(__amdgpu_buffer_rsrc_t w, const int (&o
   }
 }
 
-// Staged h of a pass of NBK column blocks: thread piece i = tid + j * kBlk
-// runs over the hi rows' pieces, then the lo rows', then the trash rows of
-// a partial last round.  A wave's 64 pieces lie in one of the three (a half
-// holds a multiple of 64 pieces).
+// h of a pass of NBK column blocks goes straight to LDS like gate/up's x:
+// per ring slot the hi rows, then the lo rows, each kNT rows of the chunk's
+// 64 columns in swizzled 1 KiB segments.  The rows are the expert's dispatch
+// slots base + p0 + row, contiguous, so no pair id is needed to stage them.
 template <int NBK>
-constexpr int dn_half() { return NBK * 16 * kDnPpr; }
-template <int NBK>
-constexpr int dn_stage() {
-  static_assert(dn_half<NBK>() % kWave == 0, "wave-uniform halves");
-  return (2 * dn_half<NBK>() + kBlk - 1) / kBlk;
+constexpr int dn_segs() {  // direct-to-LDS loads per wave per chunk (both halves)
+  static_assert(2 * NBK * 16 / kSegRows % kWv == 0, "whole rounds of segments");
+  return 2 * NBK * 16 / kSegRows / kWv;
 }
 
-template <bool kTiled, int NBK>
+template <bool kTiled, int D, int NBK>
 __device__ __forceinline__ void dn_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffer_rsrc_t hhr,
                                         __amdgpu_buffer_rsrc_t hlr, const int (&ob)[kTpw],
-                                        const int* pid, uint16_t (*hs)[2 * kRowsPad * kDnRow],
+                                        const int* __restrict__ perm, int n_pairs,
+                                        uint16_t* __restrict__ s0, uint16_t* __restrict__ s1,
+                                        uint16_t* __restrict__ s2, uint16_t* __restrict__ s3,
                                         __amdgpu_buffer_rsrc_t yr, int base, int p0, int cnt,
-                                        int H, int I, int nchunks, int lane) {
-  constexpr int kStage = dn_stage<NBK>(), kHalf = dn_half<NBK>();
+                                        int H, int I, int nchunks, int lane, int wave) {
+  static_assert(D == 2 || D == 4, "two or four ring slots");
+  constexpr int kAhead = D - 1;
+  auto slot = [&](int k) { return k == 0 ? s0 : k == 1 ? s1 : k == 2 ? s2 : s3; };
+  constexpr int kSegs = dn_segs<NBK>(), kSegsHalf = NBK * 16 / kSegRows;
+  constexpr int kWloads = kTpw * kDnKs;
   const int r = lane & 15, kg = lane >> 4;
-  const int wave0 = __builtin_amdgcn_readfirstlane((int)(threadIdx.x & ~63u));
-  // per piece: its half (0 hi, 1 lo, 2 trash; wave-uniform), its LDS
-  // position and its h offset in chunk 0 (out of range past the expert's
-  // count and for the trash)
-  uint32_t hoff[kStage];
-  int lds[kStage];
+  // the pair (y row) of each of this lane's output columns, for the
+  // epilogue; loaded now, before the staging loads that the waits count
+  int pid[NBK];
 #pragma unroll
-  for (int j = 0; j < kStage; ++j) {
-    const int i = (int)threadIdx.x + j * kBlk;
-    const int half = wave0 + j * kBlk < kHalf ? 0 : wave0 + j * kBlk < 2 * kHalf ? 1 : 2;
-    if (half < 2) {
-      const int q = i - half * kHalf, row = q / kDnPpr, c8 = q % kDnPpr;
-      hoff[j] = p0 + row < cnt ? ((uint32_t)(base + p0 + row) * I + (uint32_t)c8 * 8u) * 2u
-                               : kOutOfRange;
-      lds[j] = half * kRowsPad * kDnRow + row * kDnRow + c8 * 8;
-    } else {
-      const int t = i - 2 * kHalf;
-      hoff[j] = kOutOfRange;
-      lds[j] = (kNT + ((t / kDnPpr) & 31)) * kDnRow + (t % kDnPpr) * 8;
-    }
+  for (int nb = 0; nb < NBK; ++nb) {
+    const int sl = p0 + nb * 16 + r;
+    const int p = sl < cnt ? perm[base + sl] : -1;
+    pid[nb] = p >= 0 && p < n_pairs ? p : -1;
   }
-  auto stage_load = [&](int c, u32x4 (&v)[kStage]) {
+  // source offset of this lane's piece of each segment in chunk 0 (out of
+  // range past the expert's count), its half and its LDS segment
+  uint32_t soff[kSegs];
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) {
-      const bool lo = wave0 + j * kBlk >= kHalf;  // wave-uniform
-      v[j] = buf_ld128(lo ? hlr : hhr, hoff[j] + (uint32_t)c * kDnKc * 2u);
+  for (int j = 0; j < kSegs; ++j) {
+    const int g = wave + j * kWv;                    // wave-uniform
+    const int gh = g < kSegsHalf ? g : g - kSegsHalf;
+    const int row = gh * kSegRows + (lane >> 3);
+    const int piece = (lane & 7) ^ x_swizzle(row);
+    soff[j] = p0 + row < cnt
+                  ? ((uint32_t)(base + p0 + row) * I + (uint32_t)piece * 8u) * 2u
+                  : kOutOfRange;
+  }
+  auto stage = [&](int c, int k) {  // chunk c into ring slot k = c % D
+    uint16_t* buf = slot(k);
+#pragma unroll
+    for (int j = 0; j < kSegs; ++j) {
+      const int g = wave + j * kWv;
+      const bool lo = g >= kSegsHalf;
+      const int gh = lo ? g - kSegsHalf : g;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          lo ? hlr : hhr,
+          (__attribute__((address_space(3))) void*)(buf + ((lo ? kNT : 0) + gh * kSegRows) * kDnKc),
+          16, soff[j] + (uint32_t)c * kDnKc * 2u, 0, 0, 0);
     }
   };
-  auto stage_store = [&](uint16_t* buf, const u32x4 (&v)[kStage]) {
+  int bslot[kDnKs];
 #pragma unroll
-    for (int j = 0; j < kStage; ++j) *reinterpret_cast<u32x4*>(buf + lds[j]) = v[j];
-  };
+  for (int st = 0; st < kDnKs; ++st) bslot[st] = ((st * 4 + kg) ^ x_swizzle(r)) * 8;
 
-  u32x4 A[kDnDepth][kTpw][kDnKs];
 #pragma unroll
-  for (int d = 0; d < kDnDepth - 1; ++d) dn_issue<kTiled>(w, ob, d, nchunks, H, I, lane, A[d]);
-  {
-    u32x4 v[kStage];
-    stage_load(0, v);
-    stage_store(hs[0], v);
+  for (int c = 0; c < kAhead; ++c) stage(c, c);
+  __builtin_amdgcn_sched_barrier(0);  // the load order the waits below count on
+  u32x4 A[D][kTpw][kDnKs];
+#pragma unroll
+  for (int d = 0; d < kAhead; ++d) {  // in chunk order: the waits assume it
+    dn_issue<kTiled>(w, ob, d, nchunks, H, I, lane, A[d]);
+    __builtin_amdgcn_sched_barrier(0);
   }
   f32x4 acc[kTpw][NBK];
 #pragma unroll
@@ -439,25 +452,26 @@ __device__ __forceinline__ void dn_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
 #pragma unroll
     for (int nb = 0; nb < NBK; ++nb) acc[t][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // nchunks is a multiple of kDnDepth (as for gate/up)
-  for (int c0 = 0; c0 < nchunks; c0 += kDnDepth) {
+  // nchunks is a multiple of D; the waits work as for gate/up
+  constexpr int kAfter = (kAhead - 1) * (kSegs + kWloads) + kWloads;
+  for (int c0 = 0; c0 < nchunks; c0 += D) {
 #pragma unroll
-    for (int d = 0; d < kDnDepth; ++d) {
+    for (int d = 0; d < D; ++d) {
       const int c = c0 + d;
-      __syncthreads();
-      u32x4 v[kStage];
-      stage_load(c + 1, v);
-      dn_issue<kTiled>(w, ob, c + kDnDepth - 1, nchunks, H, I, lane,
-                       A[(d + kDnDepth - 1) % kDnDepth]);
+      __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(kAfter));
+      __builtin_amdgcn_s_barrier();
+      stage(c + kAhead, (d + kAhead) % D);
+      __builtin_amdgcn_sched_barrier(0);
+      dn_issue<kTiled>(w, ob, c + kAhead, nchunks, H, I, lane, A[(d + kAhead) % D]);
       __builtin_amdgcn_sched_barrier(0);  // loads ahead of the chunk's MFMAs
-      const uint16_t* buf = hs[c & 1];
+      const uint16_t* buf = slot(d);
 #pragma unroll
       for (int st = 0; st < kDnKs; ++st) {
 #pragma unroll
         for (int nb = 0; nb < NBK; ++nb) {
-          const uint16_t* row = buf + (nb * 16 + r) * kDnRow + st * 32 + kg * 8;
+          const uint16_t* row = buf + (nb * 16 + r) * kDnKc + bslot[st];
           const u32x4 bh = *reinterpret_cast<const u32x4*>(row);
-          const u32x4 bl = *reinterpret_cast<const u32x4*>(row + kRowsPad * kDnRow);
+          const u32x4 bl = *reinterpret_cast<const u32x4*>(row + kNT * kDnKc);
 #pragma unroll
           for (int t = 0; t < kTpw; ++t) {
             acc[t][nb] = mfma_16x16x32(A[d][t][st], bh, acc[t][nb]);
@@ -465,38 +479,41 @@ __device__ __forceinline__ void dn_pass(__amdgpu_buffer_rsrc_t w, __amdgpu_buffe
           }
         }
       }
-      stage_store(hs[(c + 1) & 1], v);
     }
   }
+  __builtin_amdgcn_s_waitcnt(vmcnt_at_most(0));  // the loads past the end landed
 
   // y rows of the pass's pairs: lane (r, kg) holds output rows
-  // ob * 16 + 4 kg .. + 3 of pair pid[nb * 16 + r]
+  // ob * 16 + 4 kg .. + 3 of pair pid[nb]
 #pragma unroll
   for (int t = 0; t < kTpw; ++t) {
 #pragma unroll
     for (int nb = 0; nb < NBK; ++nb) {
-      const int p = pid[nb * 16 + r];
       const int o = ob[t] * 16 + kg * 4;
       uint32_t off = kOutOfRange;
-      if (ob[t] >= 0 && p >= 0) off = ((uint32_t)p * H + (uint32_t)o) * 4u;
+      if (ob[t] >= 0 && pid[nb] >= 0) off = ((uint32_t)pid[nb] * H + (uint32_t)o) * 4u;
       __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc[t][nb]), yr, off, 0,
                                              0);
     }
   }
 }
 
-template <bool kTiled>
+template <bool kTiled, int D>
 __global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
     const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
     const uint16_t* __restrict__ w2, const int* __restrict__ counts,
     const int* __restrict__ offsets, const int* __restrict__ perm,
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
     int H, int I, int m, int n_pairs) {
-  __shared__ uint16_t hs[2][2 * kRowsPad * kDnRow];  // [buffer][hi rows, then lo rows]
-  __shared__ int pid[kRowsPad];
+  // the h ring: four slots of hi rows then lo rows
+  __shared__ __attribute__((aligned(1024))) uint16_t hs0[2 * kNT * kDnKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t hs1[2 * kNT * kDnKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t hs2[2 * kNT * kDnKc];
+  __shared__ __attribute__((aligned(1024))) uint16_t hs3[2 * kNT * kDnKc];
   const int n_act = *n_active_p;
   if (n_act <= 0 || n_act > m) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int tpe = H / 16;
   const int gpe = (tpe + kTpu - 1) / kTpu;
   const int nchunks = I / kDnKc;
@@ -518,11 +535,11 @@ __global__ __launch_bounds__(kBlk, 1) void down_prefill_kernel(
 
     for (int p0 = 0; p0 < s.cnt; p0 += kNT) {
       const int nbn = (min(kNT, s.cnt - p0) + 15) >> 4;
-      __syncthreads();  // the previous pass's readers of pid and hs are done
-      load_pass_rows(perm, s.base, p0, s.cnt, n_pairs, 1, pid);
+      __syncthreads();  // the previous pass's reads of the ring are done
       with_blocks(nbn, [&](auto nbk) {
-        dn_pass<kTiled, decltype(nbk)::value>(w, hhr, hlr, ob, pid, hs, yr, s.base, p0, s.cnt, H,
-                                              I, nchunks, lane);
+        dn_pass<kTiled, D, decltype(nbk)::value>(w, hhr, hlr, ob, perm, n_pairs, hs0, hs1, hs2,
+                                                 hs3, yr, s.base, p0, s.cnt, H, I, nchunks, lane,
+                                                 wave);
       });
     }
   }
@@ -540,10 +557,10 @@ int prefill_grid() {
 
 bool prefill_supported(int T, int H, int I, int m, int k) {
   // about 48 or more tokens per expert over a pool large enough to spread
-  // its units over the chip, K in whole rounds of the weight pipelines (H
-  // a multiple of 256, I of 128), and 32-bit offsets
-  return m >= 16 && (int64_t)T * k >= (int64_t)48 * m && H % (kGuKc * kGuDepth) == 0 &&
-         I % (kDnKc * kDnDepth) == 0 &&
+  // its units over the chip, K in whole rounds of the pipelines (H and I
+  // multiples of 128), and 32-bit offsets
+  return m >= 16 && (int64_t)T * k >= (int64_t)48 * m && H % (kDepth * kGuKc) == 0 &&
+         I % (kDepth * kDnKc) == 0 &&
          H <= 32768 && 4 * (int64_t)T * k * H < ((int64_t)1 << 31);
 }
 
@@ -552,10 +569,10 @@ hipError_t launch_gate_up_prefill(const uint16_t* x, int T, const uint16_t* w13,
                                   const int* active, const int* n_active, int H, int I, int m,
                                   int k, uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
   if (tiled)
-    gate_up_prefill_kernel<true><<<prefill_grid(), kBlk, 0, stream>>>(
+    gate_up_prefill_kernel<true, kDepth><<<prefill_grid(), kBlk, 0, stream>>>(
         x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
   else
-    gate_up_prefill_kernel<false><<<prefill_grid(), kBlk, 0, stream>>>(
+    gate_up_prefill_kernel<false, kDepth><<<prefill_grid(), kBlk, 0, stream>>>(
         x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k);
   return hipGetLastError();
 }
@@ -566,10 +583,10 @@ hipError_t launch_down_prefill(int T, const uint16_t* w2, bool tiled, const int*
                                const uint16_t* h_hi, const uint16_t* h_lo, float* y,
                                hipStream_t stream) {
   if (tiled)
-    down_prefill_kernel<true><<<prefill_grid(), kBlk, 0, stream>>>(
+    down_prefill_kernel<true, kDepth><<<prefill_grid(), kBlk, 0, stream>>>(
         h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
   else
-    down_prefill_kernel<false><<<prefill_grid(), kBlk, 0, stream>>>(
+    down_prefill_kernel<false, kDepth><<<prefill_grid(), kBlk, 0, stream>>>(
         h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k);
   return hipGetLastError();
 }

@@ -140,9 +140,11 @@ def _layer_in_batches(sw, D, k, nb, layout, mask=None, bias=None):
 
 @pytest.mark.parametrize("tiled", [False, True])
 @pytest.mark.parametrize("masked", [False, True])
-def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked):
-    # 512 tokens, 16 experts, top-4: ~128 tokens per expert, the prefill kernels
-    cfg, L, D = small_layer(256, 16, 4, 128, 512, seed=7)
+@pytest.mark.parametrize("hidden", [256, 384])
+def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked, hidden):
+    # 512 tokens, 16 experts, top-4: ~128 tokens per expert, the prefill
+    # kernels (4 and 6 gate/up chunks of K, 2 down chunks)
+    cfg, L, D = small_layer(hidden, 16, 4, 128, 512, seed=7)
     mask = mask_for(cfg, L, 0.25) if masked else None
     layout = sw.ROW_MAJOR
     if tiled:
@@ -164,9 +166,10 @@ def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked):
 @pytest.mark.parametrize("tiled", [False, True])
 def test_prefill_path_expert_with_several_passes(sw, tiled):
     # a bias makes expert 3 every token's first choice: 400 pairs on one
-    # expert (passes of 160, 160 and 80 tokens)
-    cfg, L, D = small_layer(256, 8, 2, 128, 400, seed=8)
-    bias = np.zeros(8, np.float32)
+    # expert (passes of 160, 160 and 80 tokens); 16 experts keep the layer
+    # on the prefill kernels
+    cfg, L, D = small_layer(256, 16, 2, 128, 400, seed=8)
+    bias = np.zeros(16, np.float32)
     bias[3] = 50.0
     layout = sw.ROW_MAJOR
     if tiled:
