@@ -73,8 +73,20 @@ typedef struct {
 /* Human-readable name of a status code (static string, never NULL). */
 const char* sw_status_str(int status);
 
+/* Kernel families of the expert FFN calls, as sw_moe_forward_kernels
+ * reports them.  Every family computes the same products; the split-K
+ * family adds a tile's K slices in a different order than the others, so
+ * its results can differ from theirs in the last bits. */
+typedef enum {
+  SW_KERNELS_NONE = 0,    /* T == 0: nothing is launched */
+  SW_KERNELS_PREFILL = 1, /* >= 48 tokens per expert, pool >= 16, H and I multiples of 128 */
+  SW_KERNELS_SPLIT_K = 2, /* few tiles with a long K (a token or two, the shared expert) */
+  SW_KERNELS_WAVE = 3,    /* the decode streaming kernels (and any tiled pool otherwise) */
+  SW_KERNELS_GENERIC = 4  /* row-major shapes outside the others' limits */
+} sw_kernel_family;
+
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 5
+#define SW_ABI_VERSION 6
 int32_t sw_abi_version(void);
 
 /*
@@ -191,6 +203,18 @@ sw_status sw_moe_pack_experts(const sw_moe_dims* d, const uint16_t* w13, const u
 
 /* Workspace bytes sw_moe_forward (and its phases) need for T tokens. */
 size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
+
+/*
+ * The kernel families (sw_kernel_family) that sw_moe_forward, and
+ * sw_moe_forward_gate_up / sw_moe_forward_down, launch for T tokens of this
+ * shape and weight layout.  Host-side only: no device work, no stream.
+ *   gate_up_family, down_family   out, one int32 each
+ * Errors: SW_ERR_NULL (d or an output NULL), SW_ERR_SHAPE (bad dims, T < 0,
+ * unknown layout), SW_ERR_UNSUPPORTED (a tiled layout the kernels do not
+ * take for this shape), as sw_moe_forward would return them.
+ */
+sw_status sw_moe_forward_kernels(const sw_moe_dims* d, int32_t n_tokens, int32_t layout,
+                                 int32_t* gate_up_family, int32_t* down_family);
 
 /*
  * Expert FFNs and combine (Section 2.1 / 3.1: each token is processed by

@@ -209,6 +209,20 @@ size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {
   return sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k);
 }
 
+sw_status sw_moe_forward_kernels(const sw_moe_dims* d, int32_t n_tokens, int32_t layout,
+                                 int32_t* gate_up_family, int32_t* down_family) {
+  if (!d || !gate_up_family || !down_family) return SW_ERR_NULL;
+  SW_TRY(check_dims(d));
+  if (n_tokens < 0) return SW_ERR_SHAPE;
+  SW_TRY(check_layout(d, n_tokens, layout));
+  const bool tiled = layout == SW_LAYOUT_TILED;
+  *gate_up_family = (int32_t)sw::gate_up_kernels(n_tokens, d->hidden, d->inter, d->n_experts,
+                                                 d->top_k, tiled);
+  *down_family = (int32_t)sw::down_kernels(n_tokens, d->hidden, d->inter, d->n_experts,
+                                           d->top_k, tiled);
+  return SW_OK;
+}
+
 sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
                                  const uint16_t* w13, int32_t layout, const int32_t* counts,
                                  const int32_t* offsets, const int32_t* perm,

@@ -796,20 +796,37 @@ static int stream_blocks(int per_cu) {
   return round8((long)cus * per_cu);
 }
 
+Kernels gate_up_kernels(int T, int H, int I, int m, int k, bool tiled) {
+  if (T <= 0) return Kernels::kNone;
+  if (prefill_supported(T, H, I, m, k)) return Kernels::kPrefill;
+  if (skinny_gate_up_supported(T, H, I, m, k)) return Kernels::kSplitK;
+  // the tiled layout is only produced for shapes the wave kernels take
+  if (tiled || wave_stream_supported(T, H, I, k)) return Kernels::kWave;
+  return Kernels::kGeneric;
+}
+
+Kernels down_kernels(int T, int H, int I, int m, int k, bool tiled) {
+  if (T <= 0) return Kernels::kNone;
+  if (prefill_supported(T, H, I, m, k)) return Kernels::kPrefill;
+  if (skinny_down_supported(T, H, I, m, k)) return Kernels::kSplitK;
+  if (tiled || wave_stream_supported(T, H, I, k)) return Kernels::kWave;
+  return Kernels::kGeneric;
+}
+
 hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                           const int* counts, const int* offsets, const int* perm,
                           const int* active, const int* n_active, int H, int I, int m, int k,
                           void* workspace, hipStream_t stream, bool identity_plan) {
-  if (T == 0) return hipSuccess;
+  const Kernels family = gate_up_kernels(T, H, I, m, k, tiled);
+  if (family == Kernels::kNone) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
-  if (prefill_supported(T, H, I, m, k))
+  if (family == Kernels::kPrefill)
     return launch_gate_up_prefill(x, T, w13, tiled, counts, offsets, perm, active, n_active, H,
                                   I, m, k, ws.h_hi, ws.h_lo, stream);
-  if (skinny_gate_up_supported(T, H, I, m, k))
+  if (family == Kernels::kSplitK)
     return launch_gate_up_skinny(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I,
                                  m, k, ws.h_hi, ws.h_lo, identity_plan, stream);
-  // the tiled layout is only produced for shapes the wave kernels take
-  if (tiled || wave_stream_supported(T, H, I, k))
+  if (family == Kernels::kWave)
     return launch_gate_up_wave(x, T, w13, tiled, counts, offsets, perm, active, n_active, H, I, m,
                                k, ws.h_hi, ws.h_lo, stream);
   const int per_wave = (((H + 31) >> 5) + 3) >> 2;
@@ -847,15 +864,16 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        const int* offsets, const int* perm, const int* active,
                        const int* n_active, int H, int I, int m, int k, void* workspace,
                        hipStream_t stream, bool identity_plan) {
-  if (T == 0) return hipSuccess;
+  const Kernels family = down_kernels(T, H, I, m, k, tiled);
+  if (family == Kernels::kNone) return hipSuccess;
   const ForwardWs ws = carve(workspace, T * k, H, I);
-  if (prefill_supported(T, H, I, m, k))
+  if (family == Kernels::kPrefill)
     return launch_down_prefill(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                                ws.h_hi, ws.h_lo, ws.y, stream);
-  if (skinny_down_supported(T, H, I, m, k))
+  if (family == Kernels::kSplitK)
     return launch_down_skinny(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                               ws.h_hi, ws.h_lo, ws.y, identity_plan, stream);
-  if (tiled || wave_stream_supported(T, H, I, k))
+  if (family == Kernels::kWave)
     return launch_down_wave(T, w2, tiled, counts, offsets, perm, active, n_active, H, I, m, k,
                             ws.h_hi, ws.h_lo, ws.y, stream);
   const int per_wave = (((I + 31) >> 5) + 3) >> 2;  // K steps of one wave

@@ -55,6 +55,12 @@ hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, cons
                                  float* topk_w, float* gap, int* counts, int* offsets, int* perm,
                                  int* active, int* n_active, void* workspace, hipStream_t stream);
 
+// Kernel family serving a gate/up or a down call of a shape; the launchers
+// dispatch on it (values as sw_kernel_family in the ABI header).
+enum class Kernels : int { kNone = 0, kPrefill = 1, kSplitK = 2, kWave = 3, kGeneric = 4 };
+Kernels gate_up_kernels(int T, int H, int I, int m, int k, bool tiled);
+Kernels down_kernels(int T, int H, int I, int m, int k, bool tiled);
+
 // `tiled`: weights in the fragment-major layout of sw_moe_pack_experts.
 // `identity_plan`: the caller guarantees perm[offsets[e] + s] = offsets[e] + s
 // (the shared expert's one-expert plan), so kernels may skip reading perm.

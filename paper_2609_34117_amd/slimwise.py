@@ -45,6 +45,7 @@ def _load() -> ctypes.CDLL:
         "sw_moe_route_dispatch": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
                                   ctypes.c_int),
         "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
+        "sw_moe_forward_kernels": ([D, I32, I32, P, P], ctypes.c_int),
         "sw_moe_pack_experts": ([D, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward": ([D, P, I32, P, P, I32, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_gate_up": ([D, P, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
@@ -64,8 +65,10 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 5
+ABI_VERSION = 6
 ROW_MAJOR, TILED = 0, 1
+# sw_kernel_family values
+KERNEL_FAMILIES = {0: "none", 1: "prefill", 2: "split_k", 3: "wave", 4: "generic"}
 if LIB.sw_abi_version() != ABI_VERSION:
     raise ImportError(f"libslimwise ABI {LIB.sw_abi_version()} != binding ABI {ABI_VERSION}")
 
@@ -109,6 +112,15 @@ def sw_moe_route_workspace_bytes(d: Dims, n_tokens: int) -> int:
 
 def sw_moe_forward_workspace_bytes(d: Dims, n_tokens: int) -> int:
     return LIB.sw_moe_forward_workspace_bytes(ctypes.byref(d), n_tokens)
+
+
+def sw_moe_forward_kernels(d: Dims, n_tokens: int, layout: int = TILED) -> tuple:
+    """The kernel families (names of ``KERNEL_FAMILIES``) that serve the
+    gate/up and the down projection of ``n_tokens`` tokens of this shape."""
+    gu, dn = ctypes.c_int32(), ctypes.c_int32()
+    _check(LIB.sw_moe_forward_kernels(ctypes.byref(d), n_tokens, layout, ctypes.byref(gu),
+                                      ctypes.byref(dn)), "sw_moe_forward_kernels")
+    return KERNEL_FAMILIES[gu.value], KERNEL_FAMILIES[dn.value]
 
 
 def workspace(nbytes: int, device) -> torch.Tensor:

@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 5
+    assert lib.sw_abi_version() == 6
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -218,6 +218,42 @@ def test_forward_validation(lib):
     d.hidden, d.inter = 72, 40                   # tiled layout needs multiples of 32
     need2 = q(ctypes.byref(d), 4)
     assert call(nbytes=need2, lay=1) == SW_ERR_UNSUPPORTED
+
+
+def _families(lib, d, T, layout=1):
+    gu, dn = ctypes.c_int32(-1), ctypes.c_int32(-1)
+    st = lib.sw_moe_forward_kernels(ctypes.byref(d), T, layout, ctypes.byref(gu), ctypes.byref(dn))
+    return st, gu.value, dn.value
+
+
+def test_forward_kernel_families(lib):
+    # sw_kernel_family: none 0, prefill 1, split-K 2, wave 3, generic 4 (host logic only)
+    NONE, PREFILL, SPLIT_K, WAVE, GENERIC = range(5)
+    dec = Dims(2048, 768, 64, 8)      # the pruned batch-64 decode layer
+    assert _families(lib, dec, 64) == (SW_OK, WAVE, WAVE)
+    assert _families(lib, dec, 1) == (SW_OK, SPLIT_K, SPLIT_K)
+    assert _families(lib, dec, 0) == (SW_OK, NONE, NONE)
+    pre = Dims(2048, 512, 256, 8)     # the 4096-token prefill layer
+    assert _families(lib, pre, 4096) == (SW_OK, PREFILL, PREFILL)
+    assert _families(lib, pre, 4096, layout=0) == (SW_OK, PREFILL, PREFILL)
+    # under ~48 tokens per expert, or a pool under 16, the decode kernels
+    assert _families(lib, pre, 1024)[1:] == (WAVE, WAVE)
+    assert _families(lib, Dims(256, 128, 8, 2), 400)[1:] == (WAVE, WAVE)
+    # the prefill test shapes (hidden 256 and 384, I 128) do take the prefill kernels
+    assert _families(lib, Dims(256, 128, 16, 4), 512)[1:] == (PREFILL, PREFILL)
+    assert _families(lib, Dims(384, 128, 16, 4), 512)[1:] == (PREFILL, PREFILL)
+    assert _families(lib, Dims(256, 128, 16, 2), 400)[1:] == (PREFILL, PREFILL)
+    # K not in whole pipeline rounds: not the prefill kernels
+    assert _families(lib, Dims(2048, 192, 256, 8), 4096)[2] != PREFILL
+    # a row-major shape outside the streaming kernels' limits
+    assert _families(lib, Dims(40, 40, 16, 2), 8, layout=0)[1:] == (GENERIC, GENERIC)
+    # errors as sw_moe_forward reports them
+    gu = ctypes.c_int32()
+    assert lib.sw_moe_forward_kernels(None, 1, 1, ctypes.byref(gu), ctypes.byref(gu)) == SW_ERR_NULL
+    assert lib.sw_moe_forward_kernels(ctypes.byref(dec), 1, 1, None, ctypes.byref(gu)) == SW_ERR_NULL
+    assert _families(lib, dec, -1)[0] == SW_ERR_SHAPE
+    assert _families(lib, dec, 4, layout=7)[0] == SW_ERR_SHAPE
+    assert _families(lib, Dims(40, 40, 16, 2), 8, layout=1)[0] == SW_ERR_UNSUPPORTED
 
 
 def test_pack_validation(lib):

@@ -118,6 +118,8 @@ def test_prefill_shape_parity(sw):
     cfg, L, D = layer_inputs("decode_sweep")  # same layer shape, 4096 tokens through the full pool
     pcfg = I.CONFIGS["prefill"]
     x = I.make_x(pcfg)
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    assert sw.sw_moe_forward_kernels(d, pcfg.tokens, sw.ROW_MAJOR) == ("prefill", "prefill")
     s = check_layer(sw, cfg, dict(L, x=x), dict(D, x=dev(x)), None,
                     sample=np.array([0, 1, 777, 2048, 4000, 4095]))
     assert s["n_active"] == cfg.n_experts
@@ -151,6 +153,9 @@ def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked, hidden)
         D = dict(D)
         D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
         layout = sw.TILED
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    assert sw.sw_moe_forward_kernels(d, 512, layout) == ("prefill", "prefill")
+    assert sw.sw_moe_forward_kernels(d, 16, layout) == ("wave", "wave")
     keep = None if mask is None else dev(mask)
     g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], cfg.top_k, keep_mask=keep, layout=layout)
     g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
@@ -176,6 +181,9 @@ def test_prefill_path_expert_with_several_passes(sw, tiled):
         D = dict(D)
         D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
         layout = sw.TILED
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    assert sw.sw_moe_forward_kernels(d, 400, layout) == ("prefill", "prefill")
+    assert sw.sw_moe_forward_kernels(d, 16, layout) == ("wave", "wave")
     g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], 2, bias=dev(bias), layout=layout)
     assert int(host(g["plan"].counts)[3]) == 400
     g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
