@@ -168,6 +168,29 @@ def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked, hidden)
     assert torch.equal(g["out"], small)
 
 
+def test_prefill_path_uneven_experts(sw):
+    # graded router biases: expert loads from ~460 tokens (passes of 160,
+    # 160 and ~140) down to one, so every pass shape of the prefill kernels
+    # (4, 8 and 10 column blocks) runs, several with only 1-3 blocks used
+    cfg, L, D = small_layer(256, 16, 4, 128, 512, seed=9)
+    bias = np.linspace(1.0, -1.0, 16).astype(np.float32)
+    layout = sw.TILED
+    D = dict(D)
+    D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    assert sw.sw_moe_forward_kernels(d, 512, layout) == ("prefill", "prefill")
+    g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], 4, bias=dev(bias), layout=layout)
+    counts = host(g["plan"].counts)
+    last = [c % 160 for c in counts if c > 0]
+    assert counts.max() > 320 and any(0 < r <= 64 for r in last) and any(64 < r <= 128 for r in last)
+    g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
+    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], 4, bias=bias, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 4)
+    compare_out(host(g["out"]), oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w))
+    small = _layer_in_batches(sw, D, 4, 16, layout, bias=dev(bias))
+    assert torch.equal(g["out"], small)
+
+
 @pytest.mark.parametrize("tiled", [False, True])
 def test_prefill_path_expert_with_several_passes(sw, tiled):
     # a bias makes expert 3 every token's first choice: 400 pairs on one
