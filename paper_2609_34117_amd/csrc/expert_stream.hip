@@ -42,6 +42,27 @@ constexpr int kPad = 8;           // bf16 elements of padding per staged row
 constexpr int kDepth = 3;         // streamed chunks held in registers per wave
 constexpr int kMaxExperts = 1024;  // pool size limit of the library
 
+// One staged row of `bytes` (a multiple of 16) into LDS at `dst`, straight
+// from memory: a wave's buffer load with the LDS bit moves 64 x 16 bytes,
+// lane l to dst + 16 l, so the row is bytes / 1 KiB such loads, the last
+// one on the lanes still inside the row.  src is the row's byte offset in
+// the resource (out of range: the lanes read zeros).  dst and the loop are
+// wave-uniform; the caller waits for vmcnt before the rows are read (the
+// compiler does not track these LDS writes).
+__device__ __forceinline__ void stage_row(__amdgpu_buffer_rsrc_t r, uint32_t src, uint16_t* dst,
+                                          int bytes, int lane) {
+  for (int q = 0; q * 1024 < bytes; ++q) {
+    if (q * 1024 + lane * 16 < bytes)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          r, (__attribute__((address_space(3))) void*)(dst + q * 512), 16,
+          src == kOutOfRange ? kOutOfRange : src + (uint32_t)(q * 1024 + lane * 16), 0, 0, 0);
+  }
+}
+
+// s_waitcnt: every vector-memory load of this wave done (lgkmcnt and expcnt
+// left alone)
+constexpr int kVmcntZero = (7 << 4) | (15 << 8);
+
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
@@ -290,13 +311,14 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const int* __restrict__ perm, const int* __restrict__ active,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
-  __shared__ uint16_t xs[kNT * (kMaxStreamH + kPad)];
+  __shared__ __attribute__((aligned(16))) uint16_t xs[kNT * (kMaxStreamH + kPad)];
   __shared__ int pid[kNT];
   __shared__ int wp[kMaxExperts + 1];
   __shared__ uint32_t scan[34];
   __shared__ int verdict[kWv];
   const int tpe = I / 8;
   const int n_act = *n_active_p;
+  const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
 
   GuWave g;
   g.xs = xs;
@@ -305,7 +327,7 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   g.nsteps = H / 32;
   g.cpt = (g.nsteps + kKC - 1) / kKC;
   g.lane = threadIdx.x & 63;
-  g.wave = threadIdx.x >> 6;
+  g.wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   g.r = g.lane & 15;
   g.kg = g.lane >> 4;
   g.tpe = tpe;
@@ -420,13 +442,14 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
       }
       if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
       __syncthreads();
-      const int row8 = H / 8;
-      for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
-        const int tok = idx / row8, c8 = idx - tok * row8;
+      // the pass's token rows of x, straight into LDS: wave w stages rows
+      // w, w + kWv, ... (rows without a pair read zeros), then one wait
+      for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
         const int p = pid[tok];
-        const u32x4 v = p >= 0 ? ld128(x + (size_t)(p / k) * H + c8 * 8) : zero4();
-        *reinterpret_cast<u32x4*>(xs + tok * (H + kPad) + c8 * 8) = v;
+        stage_row(xr, p >= 0 ? (uint32_t)(p / k) * (uint32_t)H * 2u : kOutOfRange,
+                  xs + tok * (H + kPad), 2 * H, g.lane);
       }
+      __builtin_amdgcn_s_waitcnt(kVmcntZero);
       __syncthreads();
 
       f32x4 acc[kNBk];
@@ -536,7 +559,7 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     const int* __restrict__ offsets, const int* __restrict__ perm,
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
     int H, int I, int m, int n_pairs) {
-  __shared__ uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
+  __shared__ __attribute__((aligned(16))) uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
   __shared__ int pid[kNT];
   __shared__ int wp[kMaxExperts + 1];
   __shared__ uint32_t scan[34];
@@ -553,11 +576,14 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   g.nsteps = I / 32;
   g.cpt = (g.nsteps + kKC - 1) / kKC;
   g.lane = threadIdx.x & 63;
-  g.wave = threadIdx.x >> 6;
+  g.wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   g.r = g.lane & 15;
   g.kg = g.lane >> 4;
   g.tpe = tpe;
   const int lo_rows = kNT * (I + kPad);
+  const uint32_t hbytes = 2u * (uint32_t)n_pairs * (uint32_t)I;
+  const auto hhr = make_rsrc(h_hi, hbytes);
+  const auto hlr = make_rsrc(h_lo, hbytes);
 
   u32x4 A[kDepth][kKC];
   int Q = 0;
@@ -656,19 +682,16 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         }
       }
       if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
-      const int row8 = I / 8;
-      for (int idx = threadIdx.x; idx < g.nbn * 16 * row8; idx += kBlk) {
-        const int tok = idx / row8, c8 = idx - tok * row8;
+      // the pass's h rows (hi, then lo), straight into LDS: wave w stages
+      // rows w, w + kWv, ... of both halves, then one wait
+      for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
         const int slot = p0 + tok;
-        u32x4 vh = zero4(), vl = zero4();
-        if (slot < sg.cnt) {
-          const size_t off = (size_t)(sg.base + slot) * I + c8 * 8;
-          vh = ld128(h_hi + off);
-          vl = ld128(h_lo + off);
-        }
-        *reinterpret_cast<u32x4*>(hs + tok * (I + kPad) + c8 * 8) = vh;
-        *reinterpret_cast<u32x4*>(hs + lo_rows + tok * (I + kPad) + c8 * 8) = vl;
+        const uint32_t src =
+            slot < sg.cnt ? (uint32_t)(sg.base + slot) * (uint32_t)I * 2u : kOutOfRange;
+        stage_row(hhr, src, hs + tok * (I + kPad), 2 * I, g.lane);
+        stage_row(hlr, src, hs + lo_rows + tok * (I + kPad), 2 * I, g.lane);
       }
+      __builtin_amdgcn_s_waitcnt(kVmcntZero);
       __syncthreads();
 
       f32x4 acc[kNBk];
