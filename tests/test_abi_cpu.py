@@ -95,12 +95,13 @@ def test_workspace_queries(lib):
     # h hi/lo (2 x T*k*I bf16) + y (T*k*H fp32)
     assert f(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 2 * 512 * 512 * 2 + 512 * 2048 * 4
     # router logits in up to 4 slices of H: a decode batch (few 16 x 16 tiles)
-    # keeps 4 partial planes, prefill (many tiles) one
+    # keeps 4 partial planes
     assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 64) == 4 * 64 * 256 * 4
-    # four planes (64x64 tiles over 4 slices of H), then the chunked
-    # dispatch's scratch: 32 chunks of 1024 pairs (a histogram and a flag each)
+    # prefill: two planes (64x64 tiles over slices of at least 8 chunks of
+    # 128 columns of H), then the chunked dispatch's scratch: 32 chunks of
+    # 1024 pairs (a histogram and a flag each)
     assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(2048, 512, 256, 8)), 4096) == (
-        4 * 4096 * 256 * 4 + 32 * 256 * 4 + 256)
+        2 * 4096 * 256 * 4 + 32 * 256 * 4 + 256)
     assert lib.sw_moe_route_workspace_bytes(ctypes.byref(Dims(256, 128, 16, 2)), 8) == 8 * 16 * 4
 
 
