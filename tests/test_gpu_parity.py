@@ -533,6 +533,8 @@ def _assert_same_route_dispatch(a, b):
     (2048, 256, 8, 1, False, True),       # one token, 256 experts, with bias
     (2048, 256, 16, 32, True, True),      # largest fused k
     (2048, 128, 8, 64, False, False),     # 64 tokens: multi-block top-k, then dispatch
+    (2048, 256, 8, 256, False, True),     # 2048 pairs: the largest one-block dispatch
+    (1024, 200, 16, 100, True, False),    # k = 16, ragged last top-k block
     (2048, 256, 8, 600, False, False),    # 4800 pairs: chunked multi-block dispatch
     (2048, 256, 8, 4096, True, False),    # prefill: wide logit tiles, 32 dispatch chunks
     (1536, 100, 6, 700, False, True),     # wide logit tiles with ragged token and expert tiles
@@ -568,6 +570,12 @@ def test_route_dispatch_in_band_errors_and_empty_batch(sw):
     b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
     _assert_same_route_dispatch(a, b)
     assert int(b[3].n_active.item()) == -1      # the missing third choice flags the batch
+    # the same flag after the multi-block top-k (40 tokens, 120 pairs)
+    cfg, L, D = small_layer(64, 8, 3, 32, 40, seed=5)
+    a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
+    b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
+    _assert_same_route_dispatch(a, b)
+    assert int(b[3].n_active.item()) == -1
     # the same in-band flag from the chunked dispatch (3000 pairs)
     cfg, L, D = small_layer(64, 8, 3, 32, 1000, seed=4)
     a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
