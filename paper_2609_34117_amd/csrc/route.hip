@@ -462,7 +462,11 @@ void launch_topk_t(const float* part, int KS, const float* bias, const uint8_t* 
 
 void launch_topk(const float* part, int KS, const float* bias, const uint8_t* keep_mask, int T,
                  int m, int k, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
-  if (k <= 16 && m <= 256) {
+  // one token per 16-lane row for small batches; from 64 tokens on, one token
+  // per wave (more waves in flight) measured faster: 8.3 against 12.5 us at
+  // 4096 tokens, 2-3% of a 40-layer batch-256 step, 2 us of a batch-64 step
+  // over 128 experts
+  if (k <= 16 && m <= 256 && T < 64) {
     const int kpl = (m + 15) / 16;
     if (kpl <= 4)
       launch_topk_t<4, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
