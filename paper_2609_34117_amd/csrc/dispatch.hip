@@ -3,7 +3,8 @@
 // selected expert ids, its exclusive scan, the active-expert list and the
 // stable permutation that groups pairs by expert.
 //
-// Up to kSingleBlockPairs pairs, one 1024-thread block builds everything.
+// Up to kSingleBlockPairs pairs, one block builds everything (1024 threads,
+// or 512 for at most 512 pairs over at most 512 experts).
 // Larger batches (prefill) split the pairs into 1024-pair chunks, one block
 // each, in two launches:
 //   1. per-chunk histograms (and id validation);

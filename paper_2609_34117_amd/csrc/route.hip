@@ -417,12 +417,14 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
 }
 
 // Split of the router contraction for T tokens and m experts: KW waves per
-// block, KS blocks per 16 x 16 output tile.  Few tiles (decode): 4 waves and
-// up to 4 slices of H, so that about 256 blocks share the router bytes; many
-// tiles (prefill): 2 waves and no split.
+// block, KS slices of H (blocks per output tile).  Few tiles (decode): 4
+// waves and up to 4 slices of H, so that about 256 blocks share the router
+// bytes; many tiles (prefill): route_logits_wide_kernel's 64 x 64 tiles over
+// slices of at least 8 chunks of H (2 at H = 2048), or, when H is not a
+// whole number of chunks, 2-wave 16 x 16 tiles and no split.
 struct LogitsSplit {
   int kw, ks;
-  bool wide;  // route_logits_wide_kernel (one slice)
+  bool wide;  // route_logits_wide_kernel
 };
 
 LogitsSplit logits_split(int T, int H, int m) {
