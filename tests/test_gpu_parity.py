@@ -410,6 +410,25 @@ def test_dispatch_skewed_and_large(sw):
         np.testing.assert_array_equal(host(plan.active)[:n_active], active)
 
 
+@pytest.mark.parametrize("tokens,m,k", [
+    (64, 512, 8),    # 512 pairs over 512 experts: the half-size plan block at both limits
+    (57, 512, 9),    # 513 pairs: the full block
+    (64, 513, 8),    # 513 experts: the full block
+    (1, 1, 1),       # one pair, one expert
+    (73, 7, 7),      # 511 pairs, every token picks every expert
+])
+def test_dispatch_plan_block_size_boundaries(sw, tokens, m, k):
+    g = np.random.default_rng(tokens * 1000 + m)
+    ids = np.stack([g.choice(m, size=k, replace=False) for _ in range(tokens)]).astype(np.int32)
+    plan = sw.sw_moe_dispatch(dev(ids), m)
+    counts, offsets, perm, active, n_active = oracle.dispatch(ids, m)
+    np.testing.assert_array_equal(host(plan.counts), counts)
+    np.testing.assert_array_equal(host(plan.offsets), offsets)
+    np.testing.assert_array_equal(host(plan.perm)[: tokens * k], perm)
+    assert int(host(plan.n_active)[0]) == n_active
+    np.testing.assert_array_equal(host(plan.active)[:n_active], active)
+
+
 def test_exact_logit_ties_break_to_smaller_id(sw):
     # identical router rows give bit-identical logits on both sides
     cfg, L, D = small_layer(256, 40, 6, 32, 33, seed=2)
