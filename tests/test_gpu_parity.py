@@ -429,6 +429,18 @@ def test_dispatch_plan_block_size_boundaries(sw, tokens, m, k):
     np.testing.assert_array_equal(host(plan.active)[:n_active], active)
 
 
+@pytest.mark.parametrize("n_experts,top_k", [(64, 8), (128, 8), (256, 16), (40, 3)])
+def test_topk_row_and_wave_forms_agree_bit_for_bit(sw, n_experts, top_k):
+    # 63 tokens take one token per 16-lane row, 64 one token per wave; the
+    # logits of the shared tokens are the same, so ids, gates and gaps must be
+    cfg, L, D = small_layer(2048, n_experts, top_k, 32, 64, seed=13)
+    ids64, w64, gap64 = sw.sw_moe_route(D["x"], D["wr"], top_k)
+    ids63, w63, gap63 = sw.sw_moe_route(D["x"][:63].contiguous(), D["wr"], top_k)
+    assert torch.equal(ids64[:63], ids63)
+    assert torch.equal(w64[:63], w63)
+    assert torch.equal(gap64[:63], gap63)
+
+
 def test_exact_logit_ties_break_to_smaller_id(sw):
     # identical router rows give bit-identical logits on both sides
     cfg, L, D = small_layer(256, 40, 6, 32, 33, seed=2)
