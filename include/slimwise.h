@@ -169,7 +169,7 @@ sw_status sw_moe_dispatch(const sw_moe_dims* d, const int32_t* topk_ids, int32_t
  * of its topk_ids would write, with the same arguments, workspace
  * (sw_moe_route_workspace_bytes) and in-band errors.  For small decode
  * batches (T <= 32, m <= 256, k <= 16) the selection and the dispatch plan
- * are built by one block, which saves a kernel launch per step; above 2048
+ * are built by one block (one wave for T <= 4), which saves a kernel launch per step; above 2048
  * pairs the dispatch runs as chunked multi-block kernels whose scratch is in
  * the workspace (sw_moe_dispatch, which has no workspace, keeps one block).
  * T = 0 writes the empty plan (counts and offsets 0, *n_active = 0).

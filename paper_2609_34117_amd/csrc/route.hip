@@ -389,6 +389,7 @@ constexpr int kFusedThreads = 512;
 constexpr int kFusedMaxPool = 256;
 constexpr int kFusedMaxTokens = 32;
 constexpr int kFusedMaxK = 16;
+constexpr int kWaveFusedTokens = 4;  // one wave: 4 rows of 16 lanes, <= 64 pairs
 
 template <int KPL>
 __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
@@ -414,6 +415,76 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
   __syncthreads();
   const DispatchLds lds{cursor, wave_base, wave_cnt, scan_scratch, &bad};
   dispatch_block(ids_s, T * k, m, lds, counts, offsets, perm, active, n_active);
+}
+
+// Route + dispatch of at most 4 tokens (at most 64 pairs) in one wave: the
+// rows of 16 lanes select the tokens as above, then lane q takes pair q's id
+// and the wave builds the plan with ballots and wave scans, without a
+// barrier.  Expert i's count and offset live on lane i % 64, slot i / 64
+// (m <= 256).  The plan is the one dispatch_block builds, value for value.
+template <int KPL>
+__global__ __launch_bounds__(64) void route_select_dispatch_wave_kernel(
+    const float* __restrict__ part, int KS, const float* __restrict__ bias,
+    const uint8_t* __restrict__ keep_mask, int T, int m, int k, int* __restrict__ topk_ids,
+    float* __restrict__ topk_w, float* __restrict__ gap, int* __restrict__ counts,
+    int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
+    int* __restrict__ n_active) {
+  const int lane = threadIdx.x, t = lane >> 4, r = lane & 15;
+  const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
+  if (t < T) store_selection(s, t, k, r, topk_ids, topk_w, gap);
+  // pair q = t' * k + j was selected by lane 16 t' + j
+  const int n_pairs = T * k;
+  const bool valid = lane < n_pairs;
+  const int e = __shfl(s.id, valid ? (lane / k) * 16 + lane % k : 0);
+  if (__ballot(valid && (e < 0 || e >= m)) != 0) {  // the flagged plan
+    for (int i = lane; i <= m; i += 64) {
+      if (i < m) counts[i] = 0;
+      offsets[i] = 0;
+    }
+    if (valid) perm[lane] = lane;
+    if (lane == 0) *n_active = -1;
+    return;
+  }
+  int cnt[4] = {0, 0, 0, 0};
+  for (int q = 0; q < n_pairs; ++q) {
+    const int eq = __builtin_amdgcn_readlane(e, q);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (j == (eq >> 6) && lane == (eq & 63)) ++cnt[j];
+  }
+  // offsets = exclusive scan of the counts, active = the experts with pairs,
+  // both in expert order (slot-major)
+  int off[4] = {0, 0, 0, 0};
+  uint32_t run_off = 0, run_act = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (j * 64 >= m) break;  // uniform
+    const int i = j * 64 + lane;
+    const uint32_t c = i < m ? (uint32_t)cnt[j] : 0u, a = c > 0 ? 1u : 0u;
+    const uint32_t ic = wave_inclusive_scan_u32(c), ia = wave_inclusive_scan_u32(a);
+    off[j] = (int)(run_off + ic - c);
+    if (i < m) {
+      counts[i] = (int)c;
+      offsets[i] = off[j];
+      if (c > 0) active[run_act + ia - a] = i;
+    }
+    run_off += __builtin_amdgcn_readlane(ic, 63);
+    run_act += __builtin_amdgcn_readlane(ia, 63);
+  }
+  if (lane == 0) {
+    offsets[m] = (int)run_off;
+    *n_active = (int)run_act;
+  }
+  // stable scatter: pair q goes after the earlier pairs of its expert
+  const uint64_t peers = match_peers(e, valid, id_bits(m));
+  const int rank = __popcll(peers & ((1ull << lane) - 1ull));
+  int base = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int v = __shfl(off[j], e & 63);
+    if (j == (e >> 6)) base = v;
+  }
+  if (valid) perm[base + rank] = lane;
 }
 
 // Split of the router contraction for T tokens and m experts: KW waves per
@@ -655,6 +726,20 @@ hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, cons
   hipError_t err = launch_logits(x, T, wr, H, m, part, sp, stream);
   if (err != hipSuccess) return err;
   const int kpl = (m + 15) / 16;
+  if (T <= kWaveFusedTokens) {
+#define SW_WF(KPL)                                                                             \
+  route_select_dispatch_wave_kernel<KPL><<<1, 64, 0, stream>>>(part, sp.ks, bias, keep_mask, T, m, \
+                                                               k, topk_ids, topk_w, gap, counts,   \
+                                                               offsets, perm, active, n_active)
+    if (kpl <= 4)
+      SW_WF(4);
+    else if (kpl <= 8)
+      SW_WF(8);
+    else
+      SW_WF(16);
+#undef SW_WF
+    return hipGetLastError();
+  }
   if (kpl <= 4)
     route_select_dispatch_kernel<4><<<1, kFusedThreads, 0, stream>>>(
         part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,

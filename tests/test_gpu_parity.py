@@ -562,6 +562,10 @@ def _assert_same_route_dispatch(a, b):
     (2048, 64, 8, 32, False, False),      # largest fused batch, compacted 64-expert pool
     (2048, 128, 8, 21, True, False),      # full pool under a 50% mask, ragged last wave
     (2048, 256, 8, 1, False, True),       # one token, 256 experts, with bias
+    (2048, 64, 8, 4, True, False),        # 4 tokens: the one-wave route + plan, 32 pairs
+    (2048, 128, 16, 4, False, True),      # 64 pairs: the one-wave path at its limit
+    (512, 256, 1, 3, False, False),       # k = 1 on the one-wave path
+    (256, 16, 2, 5, False, False),        # 5 tokens: the 512-thread block again
     (2048, 256, 16, 32, True, True),      # largest fused k
     (2048, 128, 8, 64, False, False),     # 64 tokens: multi-block top-k, then dispatch
     (2048, 256, 8, 256, False, True),     # 2048 pairs: the largest one-block dispatch
