@@ -70,7 +70,7 @@ CONFIGS = {
 }
 
 SWEEP_BATCHES = (1, 8, 32, 64, 128, 256)
-SWEEP_PRUNING = (0.0, 0.25, 0.5)
+SWEEP_PRUNING = (0.0, 0.25, 0.5, 0.75)
 
 
 def rng(config_id: int, layer: int, tensor_id: int, rep: int = 0) -> np.random.Generator:

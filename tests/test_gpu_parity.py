@@ -7,7 +7,8 @@ import pytest
 
 import oracle
 from paper_2609_34117_amd import inputs as I
-from parity import compare_out, compare_routing
+from guard import Guards
+from parity import compare_out, compare_routing, oracle_forward_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -62,15 +63,42 @@ def run_gpu_layer(sw, D, k, mask=None, x=None, bias=None):
     return sw.moe_layer(xm, D["wr"], D["w13"], D["w2"], k, keep_mask=keep, bias=bias)
 
 
-def check_layer(sw, cfg, L, D, mask, bias=None, sample=None):
-    """Route, dispatch and forward on the GPU vs the oracle; returns stats."""
+def guarded_layer(sw, D, k, mask=None, bias=None, layout=None):
+    """Route + dispatch and forward with every output and workspace inside a
+    canaried allocation (poisoned interiors: an unwritten output shows as -7
+    or NaN); the margins are checked after the call."""
+    x, wr = D["x"], D["wr"]
+    t, m = x.shape[0], wr.shape[0]
+    G = Guards()
+    out3 = (G.empty((t, k), torch.int32, poison=-7), G.empty((t, k), torch.float32, poison=float("nan")),
+            G.empty(t, torch.float32, poison=float("nan")))
+    plan = sw.Plan(G.empty(m, torch.int32, poison=-7), G.empty(m + 1, torch.int32, poison=-7),
+                   G.empty(max(t * k, 1), torch.int32, poison=-7), G.empty(m, torch.int32, poison=-7),
+                   G.empty(1, torch.int32, poison=-7))
+    rd = sw.dims(x.shape[1], 8, m, k)
+    ids, w, gap, plan = sw.sw_moe_route_dispatch(
+        x, wr, k, keep_mask=None if mask is None else dev(mask), bias=bias, out=out3, plan=plan,
+        ws=G.workspace(sw.sw_moe_route_workspace_bytes(rd, t)))
+    lay = sw.ROW_MAJOR if layout is None else layout
+    fd = sw.dims(x.shape[1], D["w13"].shape[1] // 2, D["w13"].shape[0], k)
+    out = G.empty((t, x.shape[1]), torch.float32, poison=float("nan"))
+    sw.sw_moe_forward(x, D["w13"], D["w2"], w, plan, layout=lay, out=out,
+                      ws=G.workspace(sw.sw_moe_forward_workspace_bytes(fd, t)))
+    G.check()
+    return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)
+
+
+def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=None):
+    """Route, dispatch and forward on the GPU vs the oracle; returns stats.
+    The forward is compared on every token unless `rows` names a subset."""
     k = cfg.top_k
     b_dev = None if bias is None else dev(bias)
-    g = run_gpu_layer(sw, D, k, mask=mask, bias=b_dev)
-    g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
+    g = guarded_layer(sw, D, k, mask=mask, bias=b_dev, layout=layout)
+    g_ids, g_w, g_gap = host(g["topk_ids"]), host(g["topk_w"]), host(g["gap"])
     o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], k, keep_mask=mask, bias=bias,
                                           want_logits=True)
-    n_near = compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, k)
+    r = compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, k, g_gap=g_gap, o_gap=o_gap,
+                        what=what or cfg.name)
     # dispatch: bit-exact against the oracle's dispatch of the GPU's own ids
     counts, offsets, perm, active, n_active = oracle.dispatch(g_ids, cfg.n_experts)
     plan = g["plan"]
@@ -79,12 +107,12 @@ def check_layer(sw, cfg, L, D, mask, bias=None, sample=None):
     np.testing.assert_array_equal(host(plan.perm)[: g_ids.size], perm)
     assert int(host(plan.n_active)[0]) == n_active
     np.testing.assert_array_equal(host(plan.active)[:n_active], active)
-    # forward: against the oracle on the GPU's routing (sampled tokens at large T)
-    rows = np.arange(g_ids.shape[0]) if sample is None else sample
-    o_out = oracle.forward(np.ascontiguousarray(L["x"][rows]), L["w13"], L["w2"],
-                           np.ascontiguousarray(g_ids[rows]), np.ascontiguousarray(g_w[rows]))
+    # forward: against the oracle on the GPU's routing
+    rows = np.arange(g_ids.shape[0]) if rows is None else np.asarray(rows)
+    o_out = oracle_forward_rows(oracle.forward, L["x"], L["w13"], L["w2"], g_ids, g_w, rows)
     err, rel = compare_out(host(g["out"])[rows], o_out)
-    return dict(n_near=n_near, n_active=n_active, err=err, rel=rel, gpu=g)
+    return dict(n_near=r["near_ties"], routing=r, n_active=n_active, err=err, rel=rel, gpu=g,
+                counts=counts)
 
 
 # --------------------------------------------------------------------------
@@ -95,7 +123,7 @@ def check_layer(sw, cfg, L, D, mask, bias=None, sample=None):
 def test_layer_parity(sw, name, pruning):
     cfg, L, D = layer_inputs(name)
     mask = mask_for(cfg, L, pruning)
-    s = check_layer(sw, cfg, L, D, mask)
+    s = check_layer(sw, cfg, L, D, mask, what=f"{name} p={pruning}")
     print(f"{name} p={pruning}: n_active={s['n_active']} near_ties={s['n_near']} "
           f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
 
@@ -103,27 +131,54 @@ def test_layer_parity(sw, name, pruning):
 @pytest.mark.parametrize("batch", I.SWEEP_BATCHES)
 @pytest.mark.parametrize("pruning", I.SWEEP_PRUNING)
 def test_decode_sweep_parity(sw, batch, pruning):
+    # every batch of the sweep at 0/25/50/75% pruning, every token compared
     cfg, L, D = layer_inputs("decode_sweep")
     mask = mask_for(cfg, L, pruning)
     x = I.make_x(cfg, tokens=batch, rep=batch)
     L2 = dict(L, x=x)
     D2 = dict(D, x=dev(x))
-    sample = np.unique(np.linspace(0, batch - 1, min(batch, 6)).astype(int))
-    s = check_layer(sw, cfg, L2, D2, mask, sample=sample)
-    print(f"sweep B={batch} p={pruning}: n_active={s['n_active']} near_ties={s['n_near']} "
+    s = check_layer(sw, cfg, L2, D2, mask, what=f"sweep B={batch} p={pruning}")
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    fam = sw.sw_moe_forward_kernels(d, batch, sw.ROW_MAJOR)
+    if batch >= 64:
+        assert fam == ("wave", "wave")
+    if batch == 256 and pruning == 0.75:
+        # 2048 pairs over 64 experts: experts with more than one 32-token pass
+        assert s["counts"].max() > 32
+    print(f"sweep B={batch} p={pruning}: kernels={fam} n_active={s['n_active']} "
+          f"max pairs/expert={s['counts'].max()} near_ties={s['n_near']} "
           f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
 
 
 def test_prefill_shape_parity(sw):
-    cfg, L, D = layer_inputs("decode_sweep")  # same layer shape, 4096 tokens through the full pool
+    # 4096 tokens through the full pool of the sweep's layer shape, every token
+    cfg, L, D = layer_inputs("decode_sweep")
     pcfg = I.CONFIGS["prefill"]
     x = I.make_x(pcfg)
     d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
     assert sw.sw_moe_forward_kernels(d, pcfg.tokens, sw.ROW_MAJOR) == ("prefill", "prefill")
-    s = check_layer(sw, cfg, dict(L, x=x), dict(D, x=dev(x)), None,
-                    sample=np.array([0, 1, 777, 2048, 4000, 4095]))
+    s = check_layer(sw, cfg, dict(L, x=x), dict(D, x=dev(x)), None, what="prefill T=4096")
     assert s["n_active"] == cfg.n_experts
     print(f"prefill T=4096: near_ties={s['n_near']} max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+@pytest.mark.parametrize("pruning", [0.0, 0.5])
+def test_skew_routed_batch256_parity(sw, pruning):
+    # the skewed stack's routing (Zipf(1.1) logit bias, kept set = the most
+    # popular half) on the sweep layer's host-drawn experts at batch 256:
+    # popular experts take up to ~80 pairs (several 32-token passes); every
+    # token is compared
+    cfg, L, D = layer_inputs("decode_sweep")
+    scfg = I.CONFIGS["skewed_stack"]
+    S = I.make_layer(scfg, layer=0, experts=False)
+    mask = None if pruning == 0 else oracle.prune_compact(S["importance"], scfg.n_keep(pruning),
+                                                          scfg.top_k)[2]
+    L2 = dict(L, x=S["x"], wr=S["wr"])
+    D2 = dict(D, x=dev(S["x"]), wr=dev(S["wr"]))
+    s = check_layer(sw, cfg, L2, D2, mask, bias=S["bias"], what=f"skew-routed B=256 p={pruning}")
+    assert s["counts"].max() > 64
+    print(f"skew-routed B=256 p={pruning}: n_active={s['n_active']} max pairs/expert="
+          f"{s['counts'].max()} near_ties={s['n_near']} max|err|={s['err']:.3g} rel={s['rel']:.3g}")
 
 
 # --------------------------------------------------------------------------
@@ -159,8 +214,8 @@ def test_prefill_path_parity_and_equal_to_decode_path(sw, tiled, masked, hidden)
     keep = None if mask is None else dev(mask)
     g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], cfg.top_k, keep_mask=keep, layout=layout)
     g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
-    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], cfg.top_k, keep_mask=mask, want_logits=True)
-    compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, cfg.top_k)
+    o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], cfg.top_k, keep_mask=mask, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, mask, cfg.top_k, g_gap=host(g["gap"]), o_gap=o_gap)
     o_out = oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w)
     compare_out(host(g["out"]), o_out)
     # each output accumulates in the same order on both paths: bit for bit
@@ -184,8 +239,8 @@ def test_prefill_path_uneven_experts(sw):
     last = [c % 160 for c in counts if c > 0]
     assert counts.max() > 320 and any(0 < r <= 64 for r in last) and any(64 < r <= 128 for r in last)
     g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
-    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], 4, bias=bias, want_logits=True)
-    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 4)
+    o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], 4, bias=bias, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 4, g_gap=host(g["gap"]), o_gap=o_gap)
     compare_out(host(g["out"]), oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w))
     small = _layer_in_batches(sw, D, 4, 16, layout, bias=dev(bias))
     assert torch.equal(g["out"], small)
@@ -210,8 +265,8 @@ def test_prefill_path_expert_with_several_passes(sw, tiled):
     g = sw.moe_layer(D["x"], D["wr"], D["w13"], D["w2"], 2, bias=dev(bias), layout=layout)
     assert int(host(g["plan"].counts)[3]) == 400
     g_ids, g_w = host(g["topk_ids"]), host(g["topk_w"])
-    o_ids, o_w, _, o_z = oracle.route(L["x"], L["wr"], 2, bias=bias, want_logits=True)
-    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 2)
+    o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], 2, bias=bias, want_logits=True)
+    compare_routing(g_ids, g_w, o_ids, o_w, o_z, None, 2, g_gap=host(g["gap"]), o_gap=o_gap)
     compare_out(host(g["out"]), oracle.forward(L["x"], L["w13"], L["w2"], g_ids, g_w))
     small = _layer_in_batches(sw, D, 2, 16, layout, bias=dev(bias))
     assert torch.equal(g["out"], small)
@@ -452,6 +507,7 @@ def test_exact_logit_ties_break_to_smaller_id(sw):
     o_ids, o_w, o_gap = oracle.route(L["x"], wr, 6)
     np.testing.assert_array_equal(host(ids), o_ids)
     np.testing.assert_allclose(host(w), o_w, atol=1e-5)
+    np.testing.assert_allclose(host(gap), o_gap, atol=1e-5)
     for r in host(ids):
         pos = {int(e): j for j, e in enumerate(r)}
         if 3 in pos and 7 in pos:
@@ -517,10 +573,8 @@ def test_tiled_forward_parity_and_bitwise_equal_to_row_major(sw, name, pruning, 
     tl = sw.moe_layer(x, D["wr"], t13, t2, cfg.top_k, keep_mask=keep, layout=sw.TILED)
     assert torch.equal(rm["out"], tl["out"])
     ids, w = host(tl["topk_ids"]), host(tl["topk_w"])
-    rows = np.unique(np.linspace(0, x_np.shape[0] - 1, min(x_np.shape[0], 8)).astype(int))
-    o_out = oracle.forward(np.ascontiguousarray(x_np[rows]), L["w13"], L["w2"],
-                           np.ascontiguousarray(ids[rows]), np.ascontiguousarray(w[rows]))
-    compare_out(host(tl["out"])[rows], o_out)
+    o_out = oracle_forward_rows(oracle.forward, x_np, L["w13"], L["w2"], ids, w)
+    compare_out(host(tl["out"]), o_out)
 
 
 def test_compacting_a_tiled_pool_equals_tiling_the_compacted_pool(sw):
@@ -592,9 +646,10 @@ def test_route_dispatch_equals_route_then_dispatch(sw, hidden, n_experts, top_k,
     # and the routing itself against the oracle
     mask_np = host(kw["keep_mask"]) if masked else None
     bias_np = host(kw["bias"]) if biased else None
-    ids_o, w_o, _, z_o = oracle.route(L["x"], L["wr"], top_k, keep_mask=mask_np, bias=bias_np,
-                                      want_logits=True)
-    compare_routing(host(b[0]), host(b[1]), ids_o, w_o, z_o, mask_np, top_k)
+    ids_o, w_o, gap_o, z_o = oracle.route(L["x"], L["wr"], top_k, keep_mask=mask_np, bias=bias_np,
+                                          want_logits=True)
+    compare_routing(host(b[0]), host(b[1]), ids_o, w_o, z_o, mask_np, top_k, g_gap=host(b[2]),
+                    o_gap=gap_o)
 
 
 def test_route_dispatch_in_band_errors_and_empty_batch(sw):
