@@ -11,9 +11,10 @@
  * Conventions shared by every call:
  *   - Every array pointer is a DEVICE pointer on the current HIP device;
  *     the caller allocates and owns all memory.  The library never
- *     allocates, never synchronises, keeps no mutable global state and is
- *     re-entrant; calls are ordered on `stream` (a hipStream_t; NULL = the
- *     default stream).  Calls on one stream that share output or workspace
+ *     allocates, never synchronises and is re-entrant; calls are ordered on
+ *     `stream` (a hipStream_t; NULL = the default stream).  It keeps no
+ *     mutable global state, except the static per-device scratch of
+ *     sw_moe_forward_no_alloc (see there).  Calls on one stream that share output or workspace
  *     buffers must not overlap with calls on other streams.
  *   - bf16 tensors are passed as their raw 16-bit patterns (uint16_t).
  *   - Layouts are dense row-major:
@@ -86,7 +87,7 @@ typedef enum {
 } sw_kernel_family;
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 6
+#define SW_ABI_VERSION 7
 int32_t sw_abi_version(void);
 
 /*
@@ -241,6 +242,38 @@ sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_toke
                          const float* topk_w, const int32_t* counts, const int32_t* offsets,
                          const int32_t* perm, const int32_t* active, const int32_t* n_active,
                          float* out, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * sw_moe_forward without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  It runs the same kernels as
+ * sw_moe_forward (bit for bit the same output) with their scratch (the
+ * per-pair h and y of the call) in a static device array of
+ * SW_NO_ALLOC_SCRATCH_BYTES inside the library, so it allocates nothing:
+ * no hipMalloc, no hipFree, no allocating library routine.
+ *
+ *   arguments   as for sw_moe_forward, minus workspace / workspace_bytes
+ * Errors: as sw_moe_forward, and SW_ERR_WORKSPACE when the call needs more
+ * scratch than the array holds (sw_moe_forward_workspace_bytes(d, T) >
+ * SW_NO_ALLOC_SCRATCH_BYTES: T * k above 2978 routed pairs at H 2048, I 768,
+ * i.e. 372 tokens at top-8; the scratch is (4 I + 4 H) bytes a pair), and
+ * SW_ERR_DEVICE if the array's device address cannot be found.
+ * The array is per device: each GPU the library runs on holds its own copy
+ * until the process ends, and the first call on a device looks up its
+ * address (kept for later calls).  Every call on one GPU shares that GPU's
+ * array and leaves the last call's contents in it (each call writes all the
+ * scratch it reads before reading it, so nothing needs clearing): calls
+ * that can overlap on one GPU -- on different streams, or from different
+ * host threads onto different streams -- race and must be serialised by
+ * the caller.
+ */
+#define SW_NO_ALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+sw_status sw_moe_forward_no_alloc(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                  const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                                  const float* topk_w, const int32_t* counts,
+                                  const int32_t* offsets, const int32_t* perm,
+                                  const int32_t* active, const int32_t* n_active, float* out,
+                                  void* stream);
 
 /*
  * The three phases of sw_moe_forward, in order, for callers that time them

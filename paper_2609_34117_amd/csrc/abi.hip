@@ -2,8 +2,17 @@
 // caller's stream.  Nothing is launched unless every check passes.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include "../../include/slimwise.h"
 #include "sw_launch.h"
+
+// Scratch of sw_moe_forward_no_alloc (the per-pair h and y of one call).
+// Each device the library runs on holds its own copy until the process
+// ends.  In host code `scratch` names a host-side stand-in, never the device
+// memory: every use goes through the device address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[SW_NO_ALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -64,6 +73,28 @@ hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
     if (st_ != SW_OK) return st_;    \
   } while (0)
 
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+sw_status scratch_on_current_device(void** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return SW_ERR_DEVICE;
+  if (dev < 0 || dev >= kMaxDevices) return SW_ERR_UNSUPPORTED;
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    const hipError_t err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return SW_ERR_DEVICE;
+    }
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *ptr = p;
+  return SW_OK;
+}
+
 sw_status check_forward_common(const sw_moe_dims* d, int32_t n_tokens, const int32_t* counts,
                                const int32_t* offsets, const int32_t* perm,
                                const int32_t* active, const int32_t* n_active, void* workspace,
@@ -78,6 +109,33 @@ sw_status check_forward_common(const sw_moe_dims* d, int32_t n_tokens, const int
   if (workspace_bytes < sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k))
     return SW_ERR_WORKSPACE;
   return SW_OK;
+}
+
+// The forward's operands other than the plan and the workspace (T > 0).
+sw_status check_forward_operands(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                 const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                                 const float* topk_w, const float* out) {
+  SW_TRY(check_layout(d, n_tokens, layout));
+  if (!x || !w13 || !w2 || !topk_w || !out) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) || !aligned4(topk_w))
+    return SW_ERR_ALIGN;
+  return SW_OK;
+}
+
+// gate/up, down and combine on `workspace` (arguments already validated).
+sw_status launch_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                         const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                         const float* topk_w, const int32_t* counts, const int32_t* offsets,
+                         const int32_t* perm, const int32_t* active, const int32_t* n_active,
+                         float* out, void* workspace, hipStream_t s) {
+  (void)hipGetLastError();
+  const int H = d->hidden, I = d->inter, m = d->n_experts, k = d->top_k;
+  const bool tiled = layout == SW_LAYOUT_TILED;
+  SW_TRY(launched(sw::launch_gate_up(x, n_tokens, w13, tiled, counts, offsets, perm, active,
+                                     n_active, H, I, m, k, workspace, s)));
+  SW_TRY(launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active, H,
+                                  I, m, k, workspace, s)));
+  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, m, k, workspace, s));
 }
 
 }  // namespace
@@ -333,19 +391,33 @@ sw_status sw_moe_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_toke
   SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
                               workspace_bytes));
   if (n_tokens == 0) return SW_OK;
-  SW_TRY(check_layout(d, n_tokens, layout));
-  if (!x || !w13 || !w2 || !topk_w || !out) return SW_ERR_NULL;
-  if (!aligned16(x) || !aligned16(w13) || !aligned16(w2) || !aligned16(out) || !aligned4(topk_w))
+  SW_TRY(check_forward_operands(d, x, n_tokens, w13, w2, layout, topk_w, out));
+  return launch_forward(d, x, n_tokens, w13, w2, layout, topk_w, counts, offsets, perm, active,
+                        n_active, out, workspace, as_stream(stream));
+}
+
+sw_status sw_moe_forward_no_alloc(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                  const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                                  const float* topk_w, const int32_t* counts,
+                                  const int32_t* offsets, const int32_t* perm,
+                                  const int32_t* active, const int32_t* n_active, float* out,
+                                  void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_tokens(d, n_tokens));
+  if (n_tokens == 0) return SW_OK;
+  if (sw::forward_workspace_bytes(n_tokens, d->hidden, d->inter, d->top_k) >
+      SW_NO_ALLOC_SCRATCH_BYTES)
+    return SW_ERR_WORKSPACE;
+  if (!counts || !offsets || !perm || !active || !n_active) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(perm) || !aligned4(active) ||
+      !aligned4(n_active))
     return SW_ERR_ALIGN;
-  (void)hipGetLastError();
-  const hipStream_t s = as_stream(stream);
-  const int H = d->hidden, I = d->inter, m = d->n_experts, k = d->top_k;
-  const bool tiled = layout == SW_LAYOUT_TILED;
-  SW_TRY(launched(sw::launch_gate_up(x, n_tokens, w13, tiled, counts, offsets, perm, active,
-                                     n_active, H, I, m, k, workspace, s)));
-  SW_TRY(launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active, H,
-                                  I, m, k, workspace, s)));
-  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, m, k, workspace, s));
+  SW_TRY(check_forward_operands(d, x, n_tokens, w13, w2, layout, topk_w, out));
+  // every argument is valid: only now is the device touched
+  void* ws = nullptr;
+  SW_TRY(scratch_on_current_device(&ws));
+  return launch_forward(d, x, n_tokens, w13, w2, layout, topk_w, counts, offsets, perm, active,
+                        n_active, out, ws, as_stream(stream));
 }
 
 }  // extern "C"

@@ -48,6 +48,7 @@ def _load() -> ctypes.CDLL:
         "sw_moe_forward_kernels": ([D, I32, I32, P, P], ctypes.c_int),
         "sw_moe_pack_experts": ([D, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward": ([D, P, I32, P, P, I32, P, P, P, P, P, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_forward_no_alloc": ([D, P, I32, P, P, I32, P, P, P, P, P, P, P, P], ctypes.c_int),
         "sw_moe_forward_gate_up": ([D, P, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_down": ([D, I32, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_forward_combine": ([D, I32, P, P, P, P, SZ, P], ctypes.c_int),
@@ -65,7 +66,8 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 6
+ABI_VERSION = 7
+NO_ALLOC_SCRATCH_BYTES = 32 << 20
 ROW_MAJOR, TILED = 0, 1
 # sw_kernel_family values
 KERNEL_FAMILIES = {0: "none", 1: "prefill", 2: "split_k", 3: "wave", 4: "generic"}
@@ -281,6 +283,26 @@ def sw_moe_forward(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor, topk_w:
                             _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
                             _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "sw_moe_forward")
+    return out
+
+
+def sw_moe_forward_no_alloc(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
+                            topk_w: torch.Tensor, plan: Plan, *, layout: int = ROW_MAJOR, out=None,
+                            stream=None) -> torch.Tensor:
+    """``sw_moe_forward`` on the library's static scratch: no workspace
+    argument and no device allocation inside the call (``out`` may be
+    passed in so that the caller allocates nothing either)."""
+    t = x.shape[0]
+    d = _fwd_dims(x, w13, topk_w.shape[1])
+    if out is None:
+        out = _empty((t, d.hidden), torch.float32, x.device)
+    st = LIB.sw_moe_forward_no_alloc(ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"),
+                                     _ptr(w2, _BF16, "w2"), layout,
+                                     _ptr(topk_w, (torch.float32,), "topk_w"), _ptr(plan.counts),
+                                     _ptr(plan.offsets), _ptr(plan.perm), _ptr(plan.active),
+                                     _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"),
+                                     _stream(stream))
+    _check(st, "sw_moe_forward_no_alloc")
     return out
 
 

@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 6
+    assert lib.sw_abi_version() == 7
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -219,6 +219,39 @@ def test_forward_validation(lib):
     d.hidden, d.inter = 72, 40                   # tiled layout needs multiples of 32
     need2 = q(ctypes.byref(d), 4)
     assert call(nbytes=need2, lay=1) == SW_ERR_UNSUPPORTED
+
+
+def test_forward_no_alloc_validation(lib):
+    # every rejection happens before the device is touched (no GPU here)
+    P = ctypes.c_void_p
+    f = lib.sw_moe_forward_no_alloc
+    f.argtypes = [ctypes.POINTER(Dims), P, ctypes.c_int32, P, P, ctypes.c_int32, P, P, P, P, P, P,
+                  P, P]
+    q = lib.sw_moe_forward_workspace_bytes
+    q.argtypes = [ctypes.POINTER(Dims), ctypes.c_int32]
+    q.restype = ctypes.c_size_t
+    limit = 32 << 20
+    d = Dims(2048, 768, 128, 8)
+    args = dict(x=16, w13=16, w2=16, lay=0, tw=16, c=16, o=16, p=16, a=16, na=16, out=16)
+
+    def call(T, **kw):
+        a = dict(args, **kw)
+        return f(ctypes.byref(d), a["x"], T, a["w13"], a["w2"], a["lay"], a["tw"], a["c"], a["o"],
+                 a["p"], a["a"], a["na"], a["out"], None)
+
+    # the scratch holds (4I + 4H) bytes a pair: 2978 pairs at H 2048, I 768
+    assert q(ctypes.byref(d), 372) <= limit < q(ctypes.byref(d), 373)
+    assert call(373) == SW_ERR_WORKSPACE
+    assert call(4096) == SW_ERR_WORKSPACE
+    assert call(0) == SW_OK                      # nothing to do, nothing launched
+    assert call(-1) == SW_ERR_SHAPE
+    assert call(64, na=None) == SW_ERR_NULL
+    assert call(64, x=None) == SW_ERR_NULL
+    assert call(64, p=18) == SW_ERR_ALIGN
+    assert call(64, out=20) == SW_ERR_ALIGN
+    assert call(64, lay=2) == SW_ERR_SHAPE
+    d.top_k = 200
+    assert call(4) == SW_ERR_SHAPE               # k > m
 
 
 def _families(lib, d, T, layout=1):
