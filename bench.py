@@ -62,6 +62,18 @@ HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 N_X = 16
 N_COPIES = 4
+# The paper's own decode-throughput gains of the pruned decoder (Section 4.3,
+# Fig. 4): end-to-end serving ratios on two A100-80GB GPUs under vLLM, at a
+# fixed per-user latency target, including larger batches from the freed
+# expert memory.  Context for the layer-level speedup measured here, not a
+# target.
+PAPER_CONTEXT = {
+    "decode_gain_50pct_pd_disaggregated": "1.40-1.81x",
+    "decode_gain_75pct_pd_disaggregated": "1.65-2.39x",
+    "decode_gain_50pct_pd_colocated": "1.36-1.72x",
+    "hardware": "2x A100-80GB, vLLM, end to end, 256-expert top-8 40-layer model",
+    "where": "Section 4.3, Fig. 4",
+}
 
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
@@ -98,14 +110,18 @@ def parse():
 class Pool:
     """One expert pool (full or compacted) resident on the device, N_COPIES times."""
 
-    def __init__(self, w13, w2, wr, layout, bias=None, shared=None):
+    def __init__(self, w13, w2, wr, layout, bias=None, shared=None, n_shared=0):
         self.w13 = [w13] + [w13.clone() for _ in range(N_COPIES - 1)]
         self.w2 = [w2] + [w2.clone() for _ in range(N_COPIES - 1)]
         self.wr = wr
         self.bias = bias
         self.layout = layout
-        self.m = wr.shape[0]
-        self.shared = shared  # (w13_s, w2_s, gate_w) of the shared expert, or None
+        # n_shared > 0: the shared expert folded into the plan -- its parts
+        # follow the routed experts in w13 / w2 and its gate row follows the
+        # router rows in wr
+        self.n_shared = n_shared
+        self.m = wr.shape[0] - (1 if n_shared else 0)  # routed experts
+        self.shared = shared  # (w13_s, w2_s, gate_w) run by the separate call, or None
         self.keep_mask = None  # router mask over this pool (colocated decode), or None
 
 
@@ -115,31 +131,44 @@ class Runner:
     def __init__(self, sw, torch, pool: Pool, cfg, T, dev):
         self.sw, self.torch, self.pool, self.cfg, self.T = sw, torch, pool, cfg, T
         k, H, Iw = cfg.top_k, cfg.hidden, cfg.inter
-        self.ids = torch.empty((T, k), dtype=torch.int32, device=dev)
-        self.w = torch.empty((T, k), dtype=torch.float32, device=dev)
+        S = pool.n_shared
+        self.kout, self.m_plan = k + S, pool.m + S  # slots a token, experts of the plan
+        self.ids = torch.empty((T, self.kout), dtype=torch.int32, device=dev)
+        self.w = torch.empty((T, self.kout), dtype=torch.float32, device=dev)
         self.gap = torch.empty(T, dtype=torch.float32, device=dev)
-        self.plan = sw.alloc_plan(T, pool.m, k, dev)
+        self.plan = sw.alloc_plan(T, self.m_plan, self.kout, dev)
         self.out = torch.empty((T, H), dtype=torch.float32, device=dev)
         d = sw.dims(H, Iw, pool.m, k)
-        self.rws = sw.workspace(sw.sw_moe_route_workspace_bytes(d, T), dev)
-        self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(d, T), dev)
+        rbytes = (sw.sw_moe_route_shared_workspace_bytes(d, T, S) if S else
+                  sw.sw_moe_route_workspace_bytes(d, T))
+        self.rws = sw.workspace(rbytes, dev)
+        self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(
+            sw.dims(H, Iw, self.m_plan, self.kout), T), dev)
         self.sws = None
         if pool.shared is not None:
             ds = sw.dims(H, pool.shared[1].shape[-1], 1, 1)
             self.sws = sw.workspace(sw.sw_moe_shared_workspace_bytes(ds, T), dev)
 
+    def route(self, x, plan):
+        sw, p = self.sw, self.pool
+        if p.n_shared:
+            sw.sw_moe_route_dispatch_shared(x, p.wr, self.cfg.top_k, p.n_shared, bias=p.bias,
+                                            keep_mask=p.keep_mask,
+                                            out=(self.ids, self.w, self.gap), plan=plan,
+                                            ws=self.rws)
+        else:
+            sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
+                                     out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
+
     def plan_for(self, x):
         """A dispatch plan of its own for batch `x` (route + dispatch)."""
-        sw, p = self.sw, self.pool
-        plan = sw.alloc_plan(self.T, p.m, self.cfg.top_k, x.device)
-        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
-                                 out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
+        plan = self.sw.alloc_plan(self.T, self.m_plan, self.kout, x.device)
+        self.route(x, plan)
         return plan
 
     def step(self, x, c, ev=None):
         sw, p = self.sw, self.pool
-        sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
-                                 out=(self.ids, self.w, self.gap), plan=self.plan, ws=self.rws)
+        self.route(x, self.plan)
         if ev is None:
             sw.sw_moe_forward(x, p.w13[c], p.w2[c], self.w, self.plan, layout=p.layout,
                               out=self.out, ws=self.fws)
@@ -147,12 +176,12 @@ class Runner:
                 sw.sw_moe_shared_expert(x, *p.shared, self.out, layout=p.layout, ws=self.sws)
             return
         ev[0].record()
-        sw.sw_moe_forward_gate_up(x, p.w13[c], self.cfg.top_k, self.plan, self.fws, layout=p.layout)
+        sw.sw_moe_forward_gate_up(x, p.w13[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[1].record()
-        sw.sw_moe_forward_down(self.T, p.w2[c], self.cfg.top_k, self.plan, self.fws, layout=p.layout)
+        sw.sw_moe_forward_down(self.T, p.w2[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[2].record()
-        sw.sw_moe_forward_combine(self.w, self.cfg.hidden, self.cfg.inter, p.m, self.plan, self.out,
-                                  self.fws)
+        sw.sw_moe_forward_combine(self.w, self.cfg.hidden, self.cfg.inter, self.m_plan, self.plan,
+                                  self.out, self.fws)
         ev[3].record()
 
 
@@ -221,7 +250,7 @@ def time_kernels(torch, r: Runner, xs, steps):
     the batches (each with its own plan) and the pool copies.  (The small
     kernels are shorter than a host call, so their durations come from the
     kernel trace instead.)"""
-    sw, p, k = r.sw, r.pool, r.cfg.top_k
+    sw, p, k = r.sw, r.pool, r.kout
     plans = [r.plan_for(x) for x in xs]
     torch.cuda.synchronize()
     out = {}
@@ -254,10 +283,56 @@ def sources_sha256():
     return h.hexdigest()
 
 
-def cpu_baseline(cfg, L, pruning, seconds, tokens):
+def host_details():
+    """The GPU machine's host as the oracle ran on it: logical CPUs, CPU model,
+    and how the oracle was compiled."""
+    import subprocess
+
+    import oracle
+
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        cc = subprocess.run(["gcc", "--version"], capture_output=True, text=True).stdout.splitlines()[0]
+    except (OSError, IndexError):
+        cc = "gcc"
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return dict(nproc=os.cpu_count(), usable_cpus=usable, cpu_model=model, compiler=cc,
+                cflags=" ".join(oracle.CFLAGS))
+
+
+def routing_check(cfg, wr, xs_np, gpu_ids, keep_mask=None, bias=None):
+    """Near ties of the benchmark's own batches (tokens whose oracle gap
+    z_(k) - z_(k+1) is below 1e-5) and the tokens whose GPU top-k set differs
+    from the oracle's without such a tie (expected 0)."""
+    import oracle
+
+    near = differ = tokens = 0
+    for x, g in zip(xs_np, gpu_ids):
+        o_ids, _, o_gap = oracle.route(x, wr, cfg.top_k, keep_mask=keep_mask, bias=bias)
+        tie = o_gap < 1e-5
+        same = np.all(np.sort(o_ids, axis=1) == np.sort(g, axis=1), axis=1)
+        near += int(tie.sum())
+        differ += int((~same & ~tie).sum())
+        tokens += x.shape[0]
+    return dict(tokens=tokens, near_ties=near, topk_sets_differing_without_a_tie=differ)
+
+
+def cpu_baseline(cfg, L, pruning, seconds, tokens, gpu_ids=None):
     """The C oracle (single-threaded) on the same layer: whole batches of
     `tokens` tokens through route + dispatch + forward until `seconds` have
-    passed."""
+    passed.  With `gpu_ids` (the GPU's top-k ids of the benchmark's batches on
+    the pruned pool), also the routing check of those batches."""
     import oracle
 
     k = cfg.top_k
@@ -275,9 +350,14 @@ def cpu_baseline(cfg, L, pruning, seconds, tokens):
         elapsed += time.perf_counter() - t0
         done += x.shape[0]
         batches += 1
-    return dict(value=round(done / elapsed, 2), unit="tokens/s", cores=1, kind="oracle",
-                sample=f"{batches} batch(es) of {tokens} tokens through the {int(pruning * 100)}% "
-                       f"pruned {cfg.name} layer (route+dispatch+forward), {elapsed:.1f} s, 1 thread")
+    out = dict(value=round(done / elapsed, 2), unit="tokens/s", cores=1, kind="oracle",
+               sample=f"{batches} batch(es) of {tokens} tokens through the {int(pruning * 100)}% "
+                      f"pruned {cfg.name} layer (route+dispatch+forward), {elapsed:.1f} s, 1 thread")
+    out.update(host_details())
+    if gpu_ids is not None:
+        xs_np = [I.make_x(cfg, tokens=tokens, rep=r) for r in range(len(gpu_ids))]
+        out["bench_batches_routing"] = routing_check(cfg, wr, xs_np, gpu_ids)
+    return out
 
 
 def up(torch, dev, a):
@@ -316,7 +396,8 @@ def measure(sw, torch, pool, cfg, T, xs, steps, warmup, dev):
     return dict(t_step_us=t_step * 1e6, tokens_per_s=T / t_step,
                 t_step_graph_us=kern["graph_step"] * 1e6, tokens_per_s_graph=T / kern["graph_step"],
                 t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
-                n_active_mean=n_mean, eq1_expected=float(m * (1 - (1 - k / m) ** T)),
+                n_active_mean=n_mean,
+                eq1_expected=float(m * (1 - (1 - k / m) ** T)) + pool.n_shared,
                 unique_MiB_per_step=float(U.mean() / 2 ** 20),
                 gate_up_launch_us=kern["gate_up"] * 1e6, down_launch_us=kern["down"] * 1e6,
                 gate_up_GBps=n_mean * 2 * H * Iw * 2 / kern["gate_up"] / 1e9,
@@ -387,9 +468,14 @@ def run_decode_b64(args, sw, torch, dev):
         "pruned": rounded(sp), "full": rounded(sf),
         "speedup_pruned_vs_full": round(sf["t_step_us"] / sp["t_step_us"], 3),
         "ideal_byte_ratio": round(sf["n_active_mean"] / sp["n_active_mean"], 3),
+        "paper_context": PAPER_CONTEXT,
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, L, args.pruning, args.cpu_seconds, T)
+        gpu_ids = [sw.sw_moe_route(x, pools[args.pruning].wr, cfg.top_k)[0].cpu().numpy()
+                   for x in xs]
+        line["cpu_baseline"] = cpu_baseline(cfg, L, args.pruning, args.cpu_seconds, T,
+                                            gpu_ids=gpu_ids)
+        line["detail"]["near_ties"] = line["cpu_baseline"]["bench_batches_routing"]["near_ties"]
     return line
 
 
@@ -473,45 +559,61 @@ def run_decode_shared(args, sw, torch, dev):
 
     cfg = I.CONFIGS["decode_sweep"]
     T, H, Iw = 64, cfg.hidden, cfg.inter
-    Is = 2 * Iw  # the distilled decoder's shared expert: twice the original width
+    S = 2
+    Is = S * Iw  # the distilled decoder's shared expert: twice the original width
     L = I.make_layer(cfg)
     layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
     pools = build_pools(sw, torch, cfg, L, (0.5, 0.0), layout, dev)
     g = np.random.default_rng([cfg.config_id, 0, 6])
-    w13s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((1, 2 * Is, H), dtype=np.float32))
-    w2s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((1, H, Is), dtype=np.float32))
+    w13s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((2 * Is, H), dtype=np.float32))
+    w2s = I.to_bf16_bits(np.float32(cfg.w_std) * g.standard_normal((H, Is), dtype=np.float32))
     gate_w = (cfg.wr_std * g.standard_normal(H)).astype(np.float32)
-    w13s_d, w2s_d = up(torch, dev, w13s), up(torch, dev, w2s)
+    # the separate call's operands: one expert of width Is
+    w13s_d, w2s_d = up(torch, dev, w13s[None]), up(torch, dev, w2s[None])
+    # the folded form: S parts of width I appended to the pool, the gate row
+    # to the router (part s = intermediate units s*I .. (s+1)*I - 1)
+    p13 = np.stack([np.concatenate([w13s[s * Iw:(s + 1) * Iw], w13s[Is + s * Iw:Is + (s + 1) * Iw]])
+                    for s in range(S)])
+    p2 = np.stack([np.ascontiguousarray(w2s[:, s * Iw:(s + 1) * Iw]) for s in range(S)])
+    p13_d, p2_d = up(torch, dev, p13), up(torch, dev, p2)
     if layout == sw.TILED:
         w13s_d, w2s_d = sw.sw_moe_pack_experts(w13s_d, w2s_d)
-    shared = (w13s_d, w2s_d, up(torch, dev, gate_w))
+        p13_d, p2_d = sw.sw_moe_pack_experts(p13_d, p2_d)
+    gate_d = up(torch, dev, gate_w)
     xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
     res = {}
     for p in (0.5, 0.0):
-        res[(p, False)] = measure(sw, torch, pools[p], cfg, T, xs, args.steps, args.warmup, dev)
-        with_se = copy.copy(pools[p])
-        with_se.shared = shared
-        res[(p, True)] = measure(sw, torch, with_se, cfg, T, xs, args.steps, args.warmup, dev)
-    head = res[(0.5, True)]
+        base = pools[p]
+        res[(p, "none")] = measure(sw, torch, base, cfg, T, xs, args.steps, args.warmup, dev)
+        folded = Pool(torch.cat([base.w13[0], p13_d]), torch.cat([base.w2[0], p2_d]),
+                      torch.cat([base.wr, gate_d[None]]), layout, n_shared=S)
+        res[(p, "folded")] = measure(sw, torch, folded, cfg, T, xs, args.steps, args.warmup, dev)
+        del folded
+        separate = copy.copy(base)
+        separate.shared = (w13s_d, w2s_d, gate_d)
+        res[(p, "separate")] = measure(sw, torch, separate, cfg, T, xs, args.steps, args.warmup, dev)
+    head = res[(0.5, "folded")]
     line = base_line(args, cfg, T, head["tokens_per_s"], head["t_step_us"], args.steps)
     line["config"] = {
         "workload": f"decode_shared: decode MoE layer H {H}, {cfg.n_experts} experts, top-{cfg.top_k}, "
                     f"I {Iw}, batch {T}, 50% pruned ({cfg.n_keep(0.5)} kept, compacted) plus a shared "
-                    f"expert of width {Is} behind a sigmoid gate",
+                    f"expert of width {Is} behind a sigmoid gate, folded into the plan as {S} parts",
         "hidden": H, "n_experts": cfg.n_experts, "n_kept": cfg.n_keep(0.5), "top_k": cfg.top_k,
-        "inter": Iw, "shared_inter": Is, "batch": T, "pruning": 0.5, "weight_layout": args.layout,
-        "parallelism": "none (1 GPU)",
+        "inter": Iw, "shared_inter": Is, "shared_parts": S, "batch": T, "pruning": 0.5,
+        "weight_layout": args.layout, "parallelism": "none (1 GPU)",
     }
-    line["roofline"] = hbm_roofline(cfg, T, 0.5, args.layout, res[(0.5, True)])
-    shared_bytes = 3 * H * Is * 2
-    line["detail"] = {
-        f"{int(p * 100)}%{' + shared' if s else ''}": rounded(v) for (p, s), v in res.items()}
+    line["roofline"] = hbm_roofline(cfg, T, 0.5, args.layout, head)
+    line["detail"] = {f"{int(p * 100)}% {how}": rounded(v) for (p, how), v in res.items()}
     line["detail"]["shared_expert_us"] = {
-        f"{int(p * 100)}%": round(res[(p, True)]["t_step_us"] - res[(p, False)]["t_step_us"], 3)
-        for p in (0.5, 0.0)}
-    line["detail"]["shared_expert_MiB"] = shared_bytes / 2 ** 20
+        f"{int(p * 100)}% {how}": round(res[(p, how)]["t_step_us"] - res[(p, "none")]["t_step_us"], 3)
+        for p in (0.5, 0.0) for how in ("folded", "separate")}
+    line["detail"]["shared_expert_us_graph"] = {
+        f"{int(p * 100)}% {how}": round(res[(p, how)]["t_step_graph_us"]
+                                       - res[(p, "none")]["t_step_graph_us"], 3)
+        for p in (0.5, 0.0) for how in ("folded", "separate")}
+    line["detail"]["shared_expert_MiB"] = 3 * H * Is * 2 / 2 ** 20
     line["detail"]["speedup_pruned_vs_full_with_shared"] = round(
-        res[(0.0, True)]["t_step_us"] / res[(0.5, True)]["t_step_us"], 3)
+        res[(0.0, "folded")]["t_step_us"] / res[(0.5, "folded")]["t_step_us"], 3)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(cfg, L, 0.5, args.cpu_seconds, T)
     return line

@@ -87,7 +87,7 @@ typedef enum {
 } sw_kernel_family;
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 7
+#define SW_ABI_VERSION 8
 int32_t sw_abi_version(void);
 
 /*
@@ -182,6 +182,49 @@ sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t
                                 int32_t* n_active, void* workspace, size_t workspace_bytes,
                                 void* stream);
 
+/* Workspace bytes sw_moe_route_dispatch_shared needs (0 on invalid
+ * arguments). */
+size_t sw_moe_route_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens,
+                                           int32_t n_shared);
+
+/*
+ * Route + dispatch with the always-on shared expert folded into the plan
+ * (Section 3.3: the distilled pruned decoder keeps a shared SwiGLU expert,
+ * the frozen SE1 plus the added SE2, behind one sigmoid gate).  The shared
+ * expert's SwiGLU is separable over its intermediate units, so a shared
+ * expert of width n_shared * I is n_shared experts of the routed width I
+ * whose down projections add.  This call gives every token, after its k
+ * routed slots, n_shared more slots naming those parts, each with the gate
+ * sigmoid(wr[m] . x_t):
+ *   topk_ids[t, k + s] = m + s,   topk_w[t, k + s] = sigmoid(wr[m] . x_t),
+ * and builds the plan over the m + n_shared experts.  sw_moe_forward with
+ * dims {H, I, m + n_shared, k + n_shared} on a pool that holds the m routed
+ * experts followed by the n_shared parts (part s: the gate and up rows of
+ * the shared expert's intermediate units s*I .. (s+1)*I - 1, and the
+ * matching I columns of its down projection) then adds
+ *   sigmoid(wr[m] . x_t) * W2s (silu(W1s x_t) * W3s x_t)
+ * to each token's output on the routed experts' launches.
+ *
+ *   d          the routed dims: n_experts = m, top_k = k
+ *   wr         fp32 [m + 1, H]: the router rows, then the shared gate row
+ *   bias, keep_mask  as for sw_moe_route (over the m routed experts)
+ *   n_shared   parts of the shared expert, >= 1; m + n_shared <= 1024 and
+ *              k + n_shared <= 32 (else SW_ERR_UNSUPPORTED)
+ *   topk_ids, topk_w  out [T, k + n_shared]
+ *   gap        nullable out fp32 [T], of the routed selection
+ *   counts, active  out int32 [m + n_shared]; offsets [m + n_shared + 1];
+ *              perm [T (k + n_shared)]; n_active [1]
+ *   workspace  >= sw_moe_route_shared_workspace_bytes(d, T, n_shared) bytes
+ * In-band errors as sw_moe_route_dispatch.
+ */
+sw_status sw_moe_route_dispatch_shared(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                       const float* wr, const float* bias,
+                                       const uint8_t* keep_mask, int32_t n_shared,
+                                       int32_t* topk_ids, float* topk_w, float* gap,
+                                       int32_t* counts, int32_t* offsets, int32_t* perm,
+                                       int32_t* active, int32_t* n_active, void* workspace,
+                                       size_t workspace_bytes, void* stream);
+
 /*
  * Re-lay an expert pool out for streaming (offline, once per pool; a device
  * layout choice, not part of the paper's method).  SW_LAYOUT_TILED stores
@@ -223,9 +266,16 @@ sw_status sw_moe_forward_kernels(const sw_moe_dims* d, int32_t n_tokens, int32_t
  * For every active expert e and every pair routed to it, the SwiGLU FFN
  *     g = W13[e, 0:I] x_t,  u = W13[e, I:2I] x_t,  a = silu(g) * u,
  *     y = W2[e] a                          (fp32 accumulation)
- * and out[t] = sum_j topk_w[t, j] * y(t, j), summed in slot order.  Each
- * active expert's weights are read from HBM once per call.  The same call
- * serves the full pool (prefill shape) and the pruned pool (decode shape).
+ * and out[t] = sum_j topk_w[t, j] * y(t, j), summed in slot order.  The
+ * same call serves the full pool (prefill shape) and the pruned pool
+ * (decode shape).  Weight traffic: each active expert's weights are read
+ * from HBM once per pass over its tokens.  One pass holds every token of
+ * an expert with up to 64 pairs (up to 128 in the gate/up projection and
+ * 96 in the down projection for batches of more than 64 tokens, 160 on the
+ * prefill-sized kernels), so each expert of a routed batch of up to 64
+ * tokens -- an expert takes at most one pair a token -- is read exactly
+ * once; the split-K kernels of batches of one or two tokens read each
+ * expert once.
  *
  *   layout     sw_weight_layout of w13 and w2 (SW_LAYOUT_TILED needs the
  *              shapes sw_moe_pack_experts accepts, and 4*T*k*H < 2^31)

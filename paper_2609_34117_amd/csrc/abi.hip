@@ -122,6 +122,17 @@ sw_status check_forward_operands(const sw_moe_dims* d, const uint16_t* x, int32_
   return SW_OK;
 }
 
+// Routed dims plus n_shared parts of a shared expert: the extended pool
+// and slots must stay within the kernels' limits, and so must the router
+// with its gate row.
+sw_status check_shared(const sw_moe_dims* d, int32_t n_shared) {
+  if (n_shared < 1) return SW_ERR_SHAPE;
+  if (d->n_experts + n_shared > kMaxExperts || d->top_k + n_shared > kMaxTopK)
+    return SW_ERR_UNSUPPORTED;
+  if (4 * ((int64_t)d->n_experts + 1) * d->hidden >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
+  return SW_OK;
+}
+
 // gate/up, down and combine on `workspace` (arguments already validated).
 sw_status launch_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
                          const uint16_t* w13, const uint16_t* w2, int32_t layout,
@@ -260,6 +271,48 @@ sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t
                                             d->n_experts, d->top_k, topk_ids, topk_w, gap, counts,
                                             offsets, perm, active, n_active, workspace,
                                             as_stream(stream)));
+}
+
+size_t sw_moe_route_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens,
+                                           int32_t n_shared) {
+  if (check_dims(d) != SW_OK || check_tokens(d, n_tokens) != SW_OK ||
+      check_shared(d, n_shared) != SW_OK)
+    return 0;
+  return sw::route_shared_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k, n_shared);
+}
+
+sw_status sw_moe_route_dispatch_shared(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                       const float* wr, const float* bias,
+                                       const uint8_t* keep_mask, int32_t n_shared,
+                                       int32_t* topk_ids, float* topk_w, float* gap,
+                                       int32_t* counts, int32_t* offsets, int32_t* perm,
+                                       int32_t* active, int32_t* n_active, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  SW_TRY(check_dims(d));
+  SW_TRY(check_shared(d, n_shared));
+  const sw_moe_dims ext{d->hidden, d->inter, d->n_experts + n_shared, d->top_k + n_shared};
+  SW_TRY(check_tokens(&ext, n_tokens));
+  if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(active) || !aligned4(n_active))
+    return SW_ERR_ALIGN;
+  if (n_tokens == 0) {
+    (void)hipGetLastError();
+    return launched(sw::launch_dispatch(nullptr, 0, ext.n_experts, counts, offsets, nullptr,
+                                        active, n_active, as_stream(stream)));
+  }
+  if (!x || !wr || !topk_ids || !topk_w || !perm || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
+      !aligned4(topk_w) || !aligned4(perm) || (gap && !aligned4(gap)) ||
+      (bias && !aligned4(bias)))
+    return SW_ERR_ALIGN;
+  if (workspace_bytes < sw::route_shared_workspace_bytes(n_tokens, d->hidden, d->n_experts,
+                                                         d->top_k, n_shared))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  return launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, d->hidden,
+                                            d->n_experts, d->top_k, topk_ids, topk_w, gap, counts,
+                                            offsets, perm, active, n_active, workspace,
+                                            as_stream(stream), n_shared));
 }
 
 size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {

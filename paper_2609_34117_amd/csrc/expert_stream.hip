@@ -6,22 +6,31 @@
 //   - A persistent grid of one 8-wave block per compute unit.  The tiles of
 //     all active experts form one list; block b owns the contiguous,
 //     equal-sized range b*per .. (b+1)*per of it, which crosses at most a few
-//     expert boundaries ("segments").  When some expert has more tokens than
-//     one pass holds, the list is of (expert, pass, tile) work items instead,
-//     so every block still gets the same number of tile passes.
-//   - Per segment, the block stages the expert's token activations (gate/up:
-//     x rows; down: h hi/lo rows) in LDS once, up to 32 tokens per pass.
-//   - Each wave then owns whole tiles (16 weight rows over the full K) and
-//     streams them as 8 KiB chunks through a kDepth-deep register pipeline:
+//     expert boundaries ("segments").
+//   - Each wave owns whole tiles (16 weight rows over the full K) and
+//     streams them as 8 KiB chunks through a kDepth-deep register pipeline
+//     (3, or 2 where a wide pass needs the registers for its accumulators):
 //     the kDepth - 1 chunks ahead are always in flight.  The B operand
 //     (tokens) comes from LDS, so waiting for activations never waits on
-//     weights, and there is no cross-wave reduction and no barrier inside a
-//     segment.  The first chunks of a segment are issued as soon as its
+//     weights.  The first chunks of a segment are issued as soon as its
 //     expert id is known, before the activation staging and its barriers.
+//   - Each tile is streamed once for all of its expert's tokens (up to
+//     kNbMax * 16 of them, 64 to 128 by variant; more take further passes).  When the segment's
+//     tokens fit in LDS with the whole contraction (K = H for gate/up, I for
+//     down) they are staged once and the waves run through their tiles
+//     with no barrier ("whole-K" pass).  Otherwise ("sliced" pass) K is cut
+//     into slices of whole chunks that fit for all of the tokens: the block
+//     takes one tile per wave at a time, and for each slice stages that
+//     slice of every token row, then each wave streams its tile's chunks of
+//     the slice into accumulators that live across the slices.  A popular
+//     expert thus costs the same weight bytes as any other; its tokens are
+//     re-read from L2 once per group of 8 tiles.
 //   - Every step issues the same memory operations (out-of-range offsets
 //     for missing chunks and for epilogue stores on non-final chunks), so
 //     the compiler's wait counts are exact and the pipeline never drains on
-//     a conservative wait.
+//     a conservative wait; the slice staging waits only for its own loads
+//     and the chunks before it (an explicit count, with the load order
+//     pinned), not for the weights issued after it.
 // Tiles:  gate_up: 8 gate rows + the 8 matching up rows; epilogue writes
 //         h = silu(g) * u as a bf16 hi/lo pair.
 //         down: 16 output rows of W2; epilogue writes y (fp32) per pair.
@@ -36,11 +45,19 @@ namespace {
 constexpr int kWv = 8;            // waves per block
 constexpr int kBlk = 64 * kWv;    // threads per block
 constexpr int kKC = 8;            // 32-wide K steps per streamed chunk
-constexpr int kNT = 32;           // tokens staged per pass
-constexpr int kNBk = kNT / 16;    // MFMA column blocks per pass
+constexpr int kChunkCols = 32 * kKC;
+constexpr int kNT = 32;           // tokens of the whole-K pass of a small batch
 constexpr int kPad = 8;           // bf16 elements of padding per staged row
-constexpr int kDepth = 3;         // streamed chunks held in registers per wave
-constexpr int kMaxExperts = 1024;  // pool size limit of the library
+// LDS of the staged activations (bf16 elements): 32 whole rows of the
+// largest H, or of both h planes at the largest I, with room to spare for
+// the sliced passes' larger token counts
+constexpr int kStage = 76800;
+static_assert(kNT * (kMaxStreamH + kPad) <= kStage, "whole-K rows of a 32-token pass");
+static_assert(2 * kNT * (kMaxStreamI + kPad) <= kStage, "whole-K h rows of a 32-token pass");
+// the narrowest slice (one chunk) of the widest passes fits: 128 tokens of
+// x, 96 tokens of h hi and lo
+static_assert(128 * (kChunkCols + kPad) <= kStage && 2 * 96 * (kChunkCols + kPad) <= kStage,
+              "one-chunk slices of the widest passes");
 
 // One staged row of `bytes` (a multiple of 16) into LDS at `dst`, straight
 // from memory: a wave's buffer load with the LDS bit moves 64 x 16 bytes,
@@ -59,15 +76,37 @@ __device__ __forceinline__ void stage_row(__amdgpu_buffer_rsrc_t r, uint32_t src
   }
 }
 
-// s_waitcnt: every vector-memory load of this wave done (lgkmcnt and expcnt
-// left alone)
-constexpr int kVmcntZero = (7 << 4) | (15 << 8);
+// s_waitcnt immediates (gfx9 encoding): at most n vector-memory operations
+// outstanding, expcnt and lgkmcnt left alone
+constexpr int vmcnt_at_most(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kVmcntZero = vmcnt_at_most(0);
+// ... and every LDS access of this wave done
+constexpr int vmcnt_at_most_lds_done(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+// only this wave's LDS accesses done (vmcnt at its maximum)
+constexpr int kLdsDone = vmcnt_at_most_lds_done(63);
+
+// The barriers around the staging of a K slice.  Plain s_barriers with
+// explicit waits: a __syncthreads fence could also wait for the weight
+// loads in flight, which must stay outstanding across the staging.
+// Before: every wave's reads of the previous slice are done.
+__device__ __forceinline__ void slice_barrier_before() {
+  __builtin_amdgcn_s_waitcnt(kLdsDone);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
+// After: the slice's loads of every wave have landed; `after` loads issued
+// since the staging stay outstanding.
+template <int kAfter>
+__device__ __forceinline__ void slice_barrier_after() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(kAfter));
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+}
 
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
-  int p0;      // first token of the segment's pass (weighted walk), else 0
-  int w_end;   // work item after the segment (weighted walk)
   bool e_ok;   // expert id in range: its weights may be read
 };
 
@@ -88,8 +127,6 @@ __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const
   s.e = s.e_ok ? e : 0;
   s.cnt = counts[s.e];
   s.base = offsets[s.e];
-  s.p0 = 0;
-  s.w_end = 0;
   return s;
 }
 
@@ -109,104 +146,39 @@ __device__ __forceinline__ void block_range(int total, int* r_lo, int* r_hi) {
   *r_hi = min(total, *r_lo + per);
 }
 
-// Token passes of expert e's pairs (0 for an invalid plan entry).
-__device__ __forceinline__ int expert_passes(int e, const int* counts, const int* offsets, int m,
-                                             int n_pairs) {
-  if (e < 0 || e >= m) return 0;
-  const int c = counts[e], b = offsets[e];
-  if (c <= 0 || b < 0 || c > n_pairs - b) return 0;
-  return (c + kNT - 1) / kNT;
-}
-
-// Counts of experts 2t and 2t + 1 (thread t) from the plan's offsets: one
-// round of independent loads (no dependent plan reads on the decode path).
-struct PairCounts {
-  int o0, o1, o2;
+// How one pass of a segment is staged.  A pass takes up to pmax tokens
+// (passes of a segment are balanced); `planes` staged rows per token (1:
+// x, 2: h hi and lo) of K columns.  Whole-K when all of them fit, else the
+// widest slice of whole chunks that fits.
+struct PassShape {
+  int n;       // tokens of the pass
+  int nbn;     // 16-token MFMA column blocks
+  int cps;     // chunks per K slice (cpt for a whole-K pass)
+  int stride;  // LDS elements per staged row
+  bool sliced;
 };
 
-__device__ __forceinline__ PairCounts load_pair_counts(const int* offsets, int m) {
-  // unconditional loads with indices clamped to offsets[m] (branch-free, so
-  // nothing consumes them before the caller does); past m the differences
-  // are 0
-  const int e0 = 2 * (int)threadIdx.x;
-  return PairCounts{offsets[min(e0, m)], offsets[min(e0 + 1, m)], offsets[min(e0 + 2, m)]};
+__device__ __forceinline__ int pass_tokens(int cnt, int pmax) {
+  const int np = (cnt + pmax - 1) / pmax;
+  return (cnt + np - 1) / np;
 }
 
-// Whether some expert has more tokens than one pass holds (a garbage plan
-// can only make this true, which takes the checked weighted walk): each
-// wave posts its verdict to its own LDS slot before a barrier, and every
-// thread reads the eight slots after it, so the check rides on a barrier
-// the kernel has anyway.  m <= 2 * kBlk.
-__device__ __forceinline__ void post_passes_verdict(const PairCounts& c, int* verdict) {
-  const bool big = c.o1 - c.o0 > kNT || c.o2 - c.o1 > kNT;
-  const bool any = __ballot(big) != 0;
-  if ((threadIdx.x & 63) == 0) verdict[threadIdx.x >> 6] = any ? 1 : 0;
-}
-
-__device__ __forceinline__ bool read_passes_verdict(const int* verdict) {
-  int v = 0;
-#pragma unroll
-  for (int w = 0; w < kWv; ++w) v |= verdict[w];
-  return v != 0;
-}
-
-// The same with a barrier of its own.  Every thread of the block calls it.
-__device__ __forceinline__ bool some_expert_needs_passes(const PairCounts& c, int* verdict) {
-  post_passes_verdict(c, verdict);
-  __syncthreads();
-  return read_passes_verdict(verdict);
-}
-
-// Work-weighted ranges, for a batch where some expert has more than kNT
-// tokens: expert slot a owns np_a * tpe work items (its tiles once per
-// token pass, pass-major) from wp[a] on, wp[n_act] being the total, and
-// blocks take equal contiguous runs of work.  A popular expert is then
-// spread over more blocks instead of lengthening the few blocks that own
-// its tiles (when every expert fits one pass, the tile ranges are already
-// balanced and this is not used).  Every thread of the block calls it;
-// n_act <= 2 * kBlk.
-__device__ void weighted_work(int n_act, int tpe, const int* active, const int* counts,
-                              const int* offsets, int m, int n_pairs, int* wp, uint32_t* scan) {
-  const int a0 = 2 * (int)threadIdx.x, a1 = a0 + 1;
-  const int n0 = a0 < n_act ? expert_passes(active[a0], counts, offsets, m, n_pairs) : 0;
-  const int n1 = a1 < n_act ? expert_passes(active[a1], counts, offsets, m, n_pairs) : 0;
-  uint32_t off, unused, total, unused_t;
-  block_exclusive_scan2((uint32_t)((n0 + n1) * tpe), 0u, scan, &off, &unused, &total, &unused_t);
-  if (a0 < n_act) wp[a0] = (int)off;
-  if (a1 < n_act) wp[a1] = (int)off + n0 * tpe;
-  if (threadIdx.x == 0) wp[n_act] = (int)total;
-  __syncthreads();
-}
-
-// Segment of the weighted walk starting at work item w < w_hi: the expert
-// slot holding w (the last a with wp[a] <= w, which has work), its pass,
-// and the run of tiles to the end of that pass or of the block's range.
-__device__ __forceinline__ Segment weighted_segment(int w, int w_hi, int n_act, const int* wp,
-                                                    int tpe, const int* active,
-                                                    const int* counts, const int* offsets,
-                                                    int m) {
-  int lo = 0, hi = n_act - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (wp[mid] <= w)
-      lo = mid;
-    else
-      hi = mid - 1;
+__device__ __forceinline__ PassShape pass_shape(int n, int K, int cpt, int planes) {
+  PassShape ps;
+  ps.n = n;
+  ps.nbn = (n + 15) >> 4;
+  const int rows = ps.nbn * 16 * planes;
+  if (rows * (K + kPad) <= kStage) {
+    ps.cps = cpt;
+    ps.stride = K + kPad;
+    ps.sliced = false;
+  } else {
+    const int c = (kStage / rows - kPad) / kChunkCols;
+    ps.cps = max(1, min(c, cpt));
+    ps.stride = ps.cps * kChunkCols + kPad;
+    ps.sliced = true;
   }
-  Segment s;
-  s.a = lo;
-  const int q = w - wp[lo], pass = q / tpe, tile = q - pass * tpe;
-  const int run = min(tpe - tile, w_hi - w);
-  s.lo = lo * tpe + tile;
-  s.hi = s.lo + run;
-  s.w_end = w + run;
-  s.p0 = pass * kNT;
-  const int e = active[lo];
-  s.e_ok = e >= 0 && e < m;
-  s.e = s.e_ok ? e : 0;
-  s.cnt = counts[s.e];
-  s.base = offsets[s.e];
-  return s;
+  return ps;
 }
 
 // ---------------------------------------------------------------------------
@@ -214,16 +186,18 @@ __device__ __forceinline__ Segment weighted_segment(int w, int w_hi, int n_act, 
 
 struct GuWave {
   __amdgpu_buffer_rsrc_t w, hh, hl;
-  const uint16_t* xs;  // LDS activations [kNT][H + kPad]
+  const uint16_t* xs;  // LDS activations [rows][stride]
   int H, I, nsteps, cpt, lane, r, kg, wave;
-  int seg_lo, seg_hi, a, tpe, p0, cnt, nbn;
+  int seg_lo, seg_hi, a, tpe, p0, cnt, nbn, cps, stride;
 };
 
-// Weight chunk q of this wave's tiles.  Row-major: lane (r, kg) reads 16 B
-// of weight row r at 64-byte K steps.  Tiled: the tile's fragments are
-// contiguous, so the wave reads 1 KiB per load (non-temporal: read once).
+// Weight chunk q (tile j = q / cpt of this wave, chunk c) of the segment.
+// Row-major: lane (r, kg) reads 16 B of weight row r at 64-byte K steps.
+// Tiled: the tile's fragments are contiguous, so the wave reads 1 KiB per
+// load (non-temporal: read once).  Chunks of tiles this wave does not have
+// read out of range.
 template <bool kTiled>
-__device__ __forceinline__ void gu_issue(const GuWave& g, int q, int Q, u32x4 (&A)[kKC]) {
+__device__ __forceinline__ void gu_issue(const GuWave& g, int q, u32x4 (&A)[kKC]) {
   const int j = q / g.cpt, c = q - j * g.cpt;
   const int tile = g.seg_lo + g.wave + j * kWv;
   const int ib = tile - g.a * g.tpe;
@@ -236,31 +210,41 @@ __device__ __forceinline__ void gu_issue(const GuWave& g, int q, int Q, u32x4 (&
     row = (uint32_t)wrow * g.H * 2u + g.kg * 16u;
     stride = 64u;
   }
+  const bool live = tile < g.seg_hi;
 #pragma unroll
   for (int s = 0; s < kKC; ++s) {
     const int step = c * kKC + s;
-    const uint32_t off = (q < Q && step < g.nsteps) ? row + (uint32_t)step * stride : kOutOfRange;
+    const uint32_t off = (live && step < g.nsteps) ? row + (uint32_t)step * stride : kOutOfRange;
     A[s] = kTiled ? buf_ld128_stream(g.w, off) : buf_ld128(g.w, off);
   }
 }
 
+// MFMAs of chunk q for the pass's column blocks (NB at most), and on the
+// tile's last chunk the SwiGLU epilogue.  The NB pairs of h stores are
+// issued on every chunk (out of range unless they hold a result), so every
+// chunk issues the same memory operations.
+template <int NB>
 __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (&A)[kKC],
-                                           f32x4 (&acc)[kNBk]) {
+                                           f32x4 (&acc)[NB]) {
   const int j = q / g.cpt, c = q - j * g.cpt;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const bool have = tile < g.seg_hi;  // false: no tile of this wave in the group
   if (c == 0) {
 #pragma unroll
-    for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // column of a K step inside the staged slice
+  const int step0 = (c / g.cps) * g.cps * kKC;
 #pragma unroll
-  for (int nb = 0; nb < kNBk; ++nb) {
-    if (nb < g.nbn) {
-      const uint16_t* row = g.xs + (nb * 16 + g.r) * (g.H + kPad) + g.kg * 8;
+  for (int nb = 0; nb < NB; ++nb) {
+    if (have && nb < g.nbn) {
+      const uint16_t* row = g.xs + (nb * 16 + g.r) * g.stride + g.kg * 8;
       u32x4 B[kKC];
 #pragma unroll
       for (int s = 0; s < kKC; ++s) {
         const int step = c * kKC + s;
         const bool ok = step < g.nsteps;
-        const u32x4 v = *reinterpret_cast<const u32x4*>(row + (ok ? step * 32 : 0));
+        const u32x4 v = *reinterpret_cast<const u32x4*>(row + (ok ? (step - step0) * 32 : 0));
         B[s] = ok ? v : zero4();
       }
 #pragma unroll
@@ -269,11 +253,10 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
   }
   // epilogue on the tile's last chunk: SwiGLU of the 8 (gate, up) row pairs
   // for every token column; lanes 0-31 own the results
-  const bool last = c == g.cpt - 1;
-  const int tile = g.seg_lo + g.wave + j * kWv;
+  const bool last = have && c == g.cpt - 1;
   const int ib = tile - g.a * g.tpe;
 #pragma unroll
-  for (int nb = 0; nb < kNBk; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     uint32_t off = kOutOfRange;
     u32x2 hw = {0u, 0u}, lw = {0u, 0u};
     if (last && nb < g.nbn) {
@@ -300,22 +283,50 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
   }
 }
 
-// kBalance: the batch has more tokens than one pass holds, so an expert
-// may need several passes and the blocks may switch to the weighted walk.
+// The chunk loop of one pass.  Chunk q lives in A[q % kDepth]; the issue
+// for q + kDepth - 1 goes out before the compute of q.  A sliced pass
+// stages slice c / cps before chunk c of each tile group: after a barrier
+// (every wave is done with the previous slice) the slice's loads go out,
+// then the chunk kDepth - 1 ahead, then a wait that leaves exactly that
+// chunk's kKC loads outstanding, and a barrier.  Q is the same on every
+// wave of a sliced pass, so every wave meets every barrier.
+template <bool kTiled, int D, int NB, typename Stage>
+__device__ __forceinline__ void gu_run(const GuWave& g, u32x4 (&A)[D][kKC], int Q, bool sliced,
+                                       Stage&& stage) {
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < Q; q += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int qd = q + d;
+      const bool restage = sliced && qd < Q && (qd % g.cpt) % g.cps == 0;
+      if (restage) {
+        slice_barrier_before();
+        stage((qd % g.cpt) / g.cps);
+        __builtin_amdgcn_sched_barrier(0);  // the slice's loads, then the weights
+      }
+      gu_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
+      if (restage) slice_barrier_after<kKC>();
+      if (d == 0 || qd < Q) gu_compute<NB>(g, qd, A[d], acc);
+    }
+  }
+}
+
 // kSpeculate: guess n_active == m and issue the first weight chunks before
 // n_active arrives (a wrong guess redoes the first segment).
-template <bool kTiled, bool kBalance, bool kSpeculate>
+// kNbMax: column blocks of the largest pass (16 kNbMax tokens); a batch of
+// at most kNT tokens needs 2, a larger one takes 8.
+template <bool kTiled, bool kSpeculate, int kNbMax, int kDepth>
 __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
     const int* __restrict__ counts, const int* __restrict__ offsets,
     const int* __restrict__ perm, const int* __restrict__ active,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
-  __shared__ __attribute__((aligned(16))) uint16_t xs[kNT * (kMaxStreamH + kPad)];
-  __shared__ int pid[kNT];
-  __shared__ int wp[kMaxExperts + 1];
-  __shared__ uint32_t scan[34];
-  __shared__ int verdict[kWv];
+  constexpr int kPmax = 16 * kNbMax;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[kStage];
+  __shared__ int pid[kPmax];
   const int tpe = I / 8;
   const int n_act = *n_active_p;
   const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
@@ -333,18 +344,15 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   g.tpe = tpe;
 
   u32x4 A[kDepth][kKC];
-  int Q = 0;
   // weight resource of the segment's expert and its first kDepth - 1 chunks
+  // (tile 0 of this wave: the same chunks in a whole-K and a sliced pass)
   auto begin_segment = [&](const Segment& sg) {
     g.seg_lo = sg.lo;
     g.seg_hi = sg.hi;
     g.a = sg.a;
     g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.e_ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
-    // this wave's tiles of the segment: seg_lo + wave, + kWv, ...
-    const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
-    Q = ntw * g.cpt;
 #pragma unroll
-    for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
+    for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, A[d]);
   };
 
   // Speculate a fully active pool (n_active == m, the usual saturated decode
@@ -352,7 +360,6 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   // alone, so that segment's plan loads and weight chunks go out together
   // with the n_active load.  A wrong guess redoes the first segment.
   // (Without kSpeculate the first segment waits for n_active instead.)
-  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
   int r_lo = 0, r_hi = 0;
   Segment sg;
   if constexpr (kSpeculate) {
@@ -361,121 +368,74 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     begin_segment(sg);
   }
   if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
-  if constexpr (!kSpeculate) block_range(n_act * tpe, &r_lo, &r_hi);
   const bool all = n_act == m;
-  // With kBalance, whether some expert needs several token passes is
-  // decided once, by the first barrier of the block's first pass (so that
-  // pass's pair-id loads are already out); a block without such a barrier
-  // decides it here.  With several passes the block switches to its range
-  // of the weighted walk.
-  bool checked = !kBalance, weighted = false;
-  int w_hi = 0;
-  auto go_weighted = [&]() {
-    weighted = true;
-    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, wp, scan);
-    block_range(wp[n_act], &r_lo, &w_hi);
-    if (r_lo >= w_hi) return false;
-    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+  if (!kSpeculate || !all) {
+    block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo >= r_hi) return;
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
     begin_segment(sg);
-    return true;
-  };
-  if constexpr (!kBalance) {
-    if (!all) {
-      block_range(n_act * tpe, &r_lo, &r_hi);
-      if (r_lo >= r_hi) return;
-      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
-      begin_segment(sg);
-    } else if (r_lo >= r_hi) {
-      return;
-    }
-  } else {
-    if (kSpeculate && !all) block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo < r_hi && (!kSpeculate || !all)) {
-      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
-      begin_segment(sg);
-    }
-    if (r_lo >= r_hi) {
-      checked = true;
-      if (!some_expert_needs_passes(pc, verdict) || !go_weighted()) return;
-    }
+  } else if (r_lo >= r_hi) {
+    return;
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
-    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
-      checked = true;
-      if (some_expert_needs_passes(pc, verdict)) {
-        if (!go_weighted()) return;
-        continue;
-      }
-    }
     g.cnt = sg.cnt;
     const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
     g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
     g.hl = make_rsrc(h_lo + (size_t)sg.base * I, hbytes);
-    // one pass per segment on the weighted walk, every pass otherwise
-    const int p_end = weighted ? min(sg.cnt, sg.p0 + kNT) : sg.cnt;
-    bool restart = false;
-    for (int p0 = sg.p0; p0 < p_end; p0 += kNT) {
-      if (p0 > sg.p0) {
-#pragma unroll
-        for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, Q, A[d]);
-      }
+    const int per_pass = sg.cnt > 0 ? pass_tokens(sg.cnt, kPmax) : 1;
+    // this wave's tiles of the segment (seg_lo + wave, + kWv, ...), and the
+    // tile groups every wave walks on a sliced pass
+    const int seg_n = sg.hi - sg.lo;
+    const int ntw = seg_n > g.wave ? (seg_n - g.wave + kWv - 1) / kWv : 0;
+    const int ngroups = (seg_n + kWv - 1) / kWv;
+    for (int p0 = 0; p0 < sg.cnt; p0 += per_pass) {
+      const PassShape ps = pass_shape(min(per_pass, sg.cnt - p0), H, g.cpt, 1);
       g.p0 = p0;
-      g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
-      // stage this pass's token rows of x in LDS (the pair ids are loaded
-      // before the barrier that waits for the previous pass's readers)
+      g.nbn = ps.nbn;
+      g.cps = ps.cps;
+      g.stride = ps.stride;
+      const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
+      if (p0 > 0) {
+#pragma unroll
+        for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, A[d]);
+      }
+      // the pass's pair ids (loaded before the barrier that waits for the
+      // previous pass's readers of pid and xs)
       int pv = -1;
-      if ((int)threadIdx.x < kNT) {
-        const int slot = p0 + threadIdx.x;
-        const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
+      if ((int)threadIdx.x < ps.n) {
+        const int p = perm[sg.base + p0 + (int)threadIdx.x];
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
-      if (!checked) post_passes_verdict(pc, verdict);
       __syncthreads();
-      if (!checked) {
-        checked = true;
-        if (read_passes_verdict(verdict)) {
-          restart = true;
-          break;
+      if ((int)threadIdx.x < kPmax) pid[threadIdx.x] = pv;
+      __syncthreads();
+      // K slice `sl` (all of K on a whole-K pass) of the pass's token rows
+      // of x, straight into LDS: wave w stages rows w, w + kWv, ... (rows
+      // without a pair read zeros)
+      auto stage = [&](int sl) {
+        const int col0 = sl * g.cps * kChunkCols;
+        const int bytes = 2 * min(g.cps * kChunkCols, H - col0);
+        for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
+          const int p = pid[tok];
+          stage_row(xr, p >= 0 ? ((uint32_t)(p / k) * (uint32_t)H + (uint32_t)col0) * 2u
+                               : kOutOfRange,
+                    xs + tok * g.stride, bytes, g.lane);
         }
+      };
+      if (!ps.sliced) {
+        stage(0);
+        __builtin_amdgcn_s_waitcnt(kVmcntZero);
+        __syncthreads();
       }
-      if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
-      __syncthreads();
-      // the pass's token rows of x, straight into LDS: wave w stages rows
-      // w, w + kWv, ... (rows without a pair read zeros), then one wait
-      for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
-        const int p = pid[tok];
-        stage_row(xr, p >= 0 ? (uint32_t)(p / k) * (uint32_t)H * 2u : kOutOfRange,
-                  xs + tok * (H + kPad), 2 * H, g.lane);
-      }
-      __builtin_amdgcn_s_waitcnt(kVmcntZero);
-      __syncthreads();
-
-      f32x4 acc[kNBk];
-#pragma unroll
-      for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      // chunk q lives in A[q % kDepth]; the issue for q + kDepth - 1 goes
-      // out before the compute of q
-      for (int q = 0; q < Q; q += kDepth) {
-#pragma unroll
-        for (int d = 0; d < kDepth; ++d) {
-          gu_issue<kTiled>(g, q + d + kDepth - 1, Q, A[(d + kDepth - 1) % kDepth]);
-          if (d == 0 || q + d < Q) gu_compute(g, q + d, A[d], acc);
-        }
-      }
+      if (kNbMax == 2 || ps.nbn <= 2)
+        gu_run<kTiled, kDepth, 2>(g, A, Q, ps.sliced, stage);
+      else
+        gu_run<kTiled, kDepth, kNbMax>(g, A, Q, ps.sliced, stage);
     }
-    if (restart) {
-      if (!go_weighted()) return;
-      continue;
-    }
-    if (weighted) {
-      if (sg.w_end >= w_hi) break;
-      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
-    } else {
-      if (sg.hi >= r_hi) break;
-      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
-    }
+    if (sg.hi >= r_hi) break;
+    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
     begin_segment(sg);
   }
 }
@@ -485,14 +445,14 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
 
 struct DnWave {
   __amdgpu_buffer_rsrc_t w, y;
-  const uint16_t* hs;  // LDS h hi rows [kNT][I + kPad], then the lo rows
+  const uint16_t* hs;  // LDS h hi rows [rows][stride], then the lo rows
   const int* pid;      // LDS pair ids of the pass
   int H, I, nsteps, cpt, lane, r, kg, wave;
-  int seg_lo, a, tpe, nbn;
+  int seg_lo, seg_hi, a, tpe, nbn, cps, stride, lo_off;
 };
 
 template <bool kTiled>
-__device__ __forceinline__ void dn_issue(const DnWave& g, int q, int Q, u32x4 (&A)[kKC]) {
+__device__ __forceinline__ void dn_issue(const DnWave& g, int q, u32x4 (&A)[kKC]) {
   const int j = q / g.cpt, c = q - j * g.cpt;
   const int tile = g.seg_lo + g.wave + j * kWv;
   const int ob = tile - g.a * g.tpe;
@@ -505,44 +465,47 @@ __device__ __forceinline__ void dn_issue(const DnWave& g, int q, int Q, u32x4 (&
     row = (uint32_t)o * g.I * 2u + g.kg * 16u;
     stride = 64u;
   }
+  const bool live = tile < g.seg_hi;
 #pragma unroll
   for (int s = 0; s < kKC; ++s) {
     const int step = c * kKC + s;
-    const bool ok = q < Q && step < g.nsteps && o < g.H;
+    const bool ok = live && step < g.nsteps && o < g.H;
     const uint32_t off = ok ? row + (uint32_t)step * stride : kOutOfRange;
     A[s] = kTiled ? buf_ld128_stream(g.w, off) : buf_ld128(g.w, off);
   }
 }
 
+template <int NB>
 __device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (&A)[kKC],
-                                           f32x4 (&acc)[kNBk]) {
+                                           f32x4 (&acc)[NB]) {
   const int j = q / g.cpt, c = q - j * g.cpt;
+  const int tile = g.seg_lo + g.wave + j * kWv;
+  const bool have = tile < g.seg_hi;
   if (c == 0) {
 #pragma unroll
-    for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int lo_rows = kNT * (g.I + kPad);
+  const int step0 = (c / g.cps) * g.cps * kKC;
 #pragma unroll
-  for (int nb = 0; nb < kNBk; ++nb) {
-    if (nb < g.nbn) {
-      const uint16_t* row = g.hs + (nb * 16 + g.r) * (g.I + kPad) + g.kg * 8;
+  for (int nb = 0; nb < NB; ++nb) {
+    if (have && nb < g.nbn) {
+      const uint16_t* row = g.hs + (nb * 16 + g.r) * g.stride + g.kg * 8;
 #pragma unroll
       for (int s = 0; s < kKC; ++s) {
         const int step = c * kKC + s;
         const bool ok = step < g.nsteps;
-        const int col = ok ? step * 32 : 0;
+        const int col = ok ? (step - step0) * 32 : 0;
         const u32x4 bh = *reinterpret_cast<const u32x4*>(row + col);
-        const u32x4 bl = *reinterpret_cast<const u32x4*>(row + lo_rows + col);
+        const u32x4 bl = *reinterpret_cast<const u32x4*>(row + g.lo_off + col);
         acc[nb] = mfma_16x16x32(A[s], ok ? bh : zero4(), acc[nb]);
         acc[nb] = mfma_16x16x32(A[s], ok ? bl : zero4(), acc[nb]);
       }
     }
   }
-  const bool last = c == g.cpt - 1;
-  const int tile = g.seg_lo + g.wave + j * kWv;
+  const bool last = have && c == g.cpt - 1;
   const int o = (tile - g.a * g.tpe) * 16 + g.kg * 4;
 #pragma unroll
-  for (int nb = 0; nb < kNBk; ++nb) {
+  for (int nb = 0; nb < NB; ++nb) {
     uint32_t off = kOutOfRange;
     if (last && nb < g.nbn) {
       const int p = g.pid[nb * 16 + g.r];
@@ -552,18 +515,39 @@ __device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (
   }
 }
 
-template <bool kTiled, bool kBalance, bool kSpeculate>
+template <bool kTiled, int D, int NB, typename Stage>
+__device__ __forceinline__ void dn_run(const DnWave& g, u32x4 (&A)[D][kKC], int Q, bool sliced,
+                                       Stage&& stage) {
+  f32x4 acc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int q = 0; q < Q; q += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int qd = q + d;
+      const bool restage = sliced && qd < Q && (qd % g.cpt) % g.cps == 0;
+      if (restage) {
+        slice_barrier_before();
+        stage((qd % g.cpt) / g.cps);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      dn_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
+      if (restage) slice_barrier_after<kKC>();
+      if (d == 0 || qd < Q) dn_compute<NB>(g, qd, A[d], acc);
+    }
+  }
+}
+
+template <bool kTiled, bool kSpeculate, int kNbMax, int kDepth>
 __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     const uint16_t* __restrict__ h_hi, const uint16_t* __restrict__ h_lo,
     const uint16_t* __restrict__ w2, const int* __restrict__ counts,
     const int* __restrict__ offsets, const int* __restrict__ perm,
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
     int H, int I, int m, int n_pairs) {
-  __shared__ __attribute__((aligned(16))) uint16_t hs[2 * kNT * (kMaxStreamI + kPad)];
-  __shared__ int pid[kNT];
-  __shared__ int wp[kMaxExperts + 1];
-  __shared__ uint32_t scan[34];
-  __shared__ int verdict[kWv];
+  constexpr int kPmax = 16 * kNbMax;
+  __shared__ __attribute__((aligned(16))) uint16_t hs[kStage];
+  __shared__ int pid[kPmax];
   const int tpe = (H + 15) / 16;
   const int n_act = *n_active_p;
 
@@ -580,26 +564,21 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   g.r = g.lane & 15;
   g.kg = g.lane >> 4;
   g.tpe = tpe;
-  const int lo_rows = kNT * (I + kPad);
   const uint32_t hbytes = 2u * (uint32_t)n_pairs * (uint32_t)I;
   const auto hhr = make_rsrc(h_hi, hbytes);
   const auto hlr = make_rsrc(h_lo, hbytes);
 
   u32x4 A[kDepth][kKC];
-  int Q = 0;
   auto begin_segment = [&](const Segment& sg) {
     g.seg_lo = sg.lo;
+    g.seg_hi = sg.hi;
     g.a = sg.a;
     g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.e_ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
-    const int ntw = sg.hi - sg.lo > g.wave ? (sg.hi - sg.lo - g.wave + kWv - 1) / kWv : 0;
-    Q = ntw * g.cpt;
 #pragma unroll
-    for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
+    for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, A[d]);
   };
 
   // Speculate a fully active pool, as in gate_up_wave_kernel.
-  // (Without kSpeculate the first segment waits for n_active instead.)
-  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
   int r_lo = 0, r_hi = 0;
   Segment sg;
   if constexpr (kSpeculate) {
@@ -608,114 +587,67 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     begin_segment(sg);
   }
   if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
-  if constexpr (!kSpeculate) block_range(n_act * tpe, &r_lo, &r_hi);
   const bool all = n_act == m;
-  // With kBalance, whether some expert needs several token passes is
-  // decided once, by the first barrier of the block's first pass (so that
-  // pass's pair-id loads are already out); a block without such a barrier
-  // decides it here.  With several passes the block switches to its range
-  // of the weighted walk.
-  bool checked = !kBalance, weighted = false;
-  int w_hi = 0;
-  auto go_weighted = [&]() {
-    weighted = true;
-    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, wp, scan);
-    block_range(wp[n_act], &r_lo, &w_hi);
-    if (r_lo >= w_hi) return false;
-    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+  if (!kSpeculate || !all) {
+    block_range(n_act * tpe, &r_lo, &r_hi);
+    if (r_lo >= r_hi) return;
+    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
     begin_segment(sg);
-    return true;
-  };
-  if constexpr (!kBalance) {
-    if (!all) {
-      block_range(n_act * tpe, &r_lo, &r_hi);
-      if (r_lo >= r_hi) return;
-      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, false);
-      begin_segment(sg);
-    } else if (r_lo >= r_hi) {
-      return;
-    }
-  } else {
-    if (kSpeculate && !all) block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo < r_hi && (!kSpeculate || !all)) {
-      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
-      begin_segment(sg);
-    }
-    if (r_lo >= r_hi) {
-      checked = true;
-      if (!some_expert_needs_passes(pc, verdict) || !go_weighted()) return;
-    }
+  } else if (r_lo >= r_hi) {
+    return;
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
-    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
-      checked = true;
-      if (some_expert_needs_passes(pc, verdict)) {
-        if (!go_weighted()) return;
-        continue;
-      }
-    }
-    const int p_end = weighted ? min(sg.cnt, sg.p0 + kNT) : sg.cnt;
-    bool restart = false;
-    for (int p0 = sg.p0; p0 < p_end; p0 += kNT) {
-      if (p0 > sg.p0) {
+    const int per_pass = sg.cnt > 0 ? pass_tokens(sg.cnt, kPmax) : 1;
+    const int seg_n = sg.hi - sg.lo;
+    const int ntw = seg_n > g.wave ? (seg_n - g.wave + kWv - 1) / kWv : 0;
+    const int ngroups = (seg_n + kWv - 1) / kWv;
+    for (int p0 = 0; p0 < sg.cnt; p0 += per_pass) {
+      const PassShape ps = pass_shape(min(per_pass, sg.cnt - p0), I, g.cpt, 2);
+      g.nbn = ps.nbn;
+      g.cps = ps.cps;
+      g.stride = ps.stride;
+      g.lo_off = ps.nbn * 16 * ps.stride;
+      const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
+      if (p0 > 0) {
 #pragma unroll
-        for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, Q, A[d]);
+        for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, A[d]);
       }
-      g.nbn = (min(kNT, sg.cnt - p0) + 15) >> 4;
-      // the pass's pair ids (for the y rows) and its h rows, which are
-      // contiguous in dispatch-slot order
+      // the pass's pair ids (for the y rows); its h rows are contiguous in
+      // dispatch-slot order
       int pv = -1;
-      if ((int)threadIdx.x < kNT) {
-        const int slot = p0 + threadIdx.x;
-        const int p = slot < sg.cnt ? perm[sg.base + slot] : -1;
+      if ((int)threadIdx.x < ps.n) {
+        const int p = perm[sg.base + p0 + (int)threadIdx.x];
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
-      if (!checked) post_passes_verdict(pc, verdict);
       __syncthreads();  // the previous pass's readers of hs and pid are done
-      if (!checked) {
-        checked = true;
-        if (read_passes_verdict(verdict)) {
-          restart = true;
-          break;
+      if ((int)threadIdx.x < kPmax) pid[threadIdx.x] = pv;
+      // K slice `sl` of the pass's h rows (hi, then lo), straight into LDS:
+      // wave w stages rows w, w + kWv, ... of both halves
+      auto stage = [&](int sl) {
+        const int col0 = sl * g.cps * kChunkCols;
+        const int bytes = 2 * min(g.cps * kChunkCols, I - col0);
+        for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
+          const uint32_t src =
+              tok < ps.n ? ((uint32_t)(sg.base + p0 + tok) * (uint32_t)I + (uint32_t)col0) * 2u
+                         : kOutOfRange;
+          stage_row(hhr, src, hs + tok * g.stride, bytes, g.lane);
+          stage_row(hlr, src, hs + g.lo_off + tok * g.stride, bytes, g.lane);
         }
+      };
+      if (!ps.sliced) {
+        stage(0);
+        __builtin_amdgcn_s_waitcnt(kVmcntZero);
       }
-      if ((int)threadIdx.x < kNT) pid[threadIdx.x] = pv;
-      // the pass's h rows (hi, then lo), straight into LDS: wave w stages
-      // rows w, w + kWv, ... of both halves, then one wait
-      for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
-        const int slot = p0 + tok;
-        const uint32_t src =
-            slot < sg.cnt ? (uint32_t)(sg.base + slot) * (uint32_t)I * 2u : kOutOfRange;
-        stage_row(hhr, src, hs + tok * (I + kPad), 2 * I, g.lane);
-        stage_row(hlr, src, hs + lo_rows + tok * (I + kPad), 2 * I, g.lane);
-      }
-      __builtin_amdgcn_s_waitcnt(kVmcntZero);
-      __syncthreads();
-
-      f32x4 acc[kNBk];
-#pragma unroll
-      for (int nb = 0; nb < kNBk; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int q = 0; q < Q; q += kDepth) {
-#pragma unroll
-        for (int d = 0; d < kDepth; ++d) {
-          dn_issue<kTiled>(g, q + d + kDepth - 1, Q, A[(d + kDepth - 1) % kDepth]);
-          if (d == 0 || q + d < Q) dn_compute(g, q + d, A[d], acc);
-        }
-      }
+      __syncthreads();  // pid (and a whole-K pass's rows) visible to every wave
+      if (kNbMax == 2 || ps.nbn <= 2)
+        dn_run<kTiled, kDepth, 2>(g, A, Q, ps.sliced, stage);
+      else
+        dn_run<kTiled, kDepth, kNbMax>(g, A, Q, ps.sliced, stage);
     }
-    if (restart) {
-      if (!go_weighted()) return;
-      continue;
-    }
-    if (weighted) {
-      if (sg.w_end >= w_hi) break;
-      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
-    } else {
-      if (sg.hi >= r_hi) break;
-      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
-    }
+    if (sg.hi >= r_hi) break;
+    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
     begin_segment(sg);
   }
 }
@@ -756,23 +688,22 @@ __global__ __launch_bounds__(256) void pack_w2_kernel(const uint16_t* __restrict
   *reinterpret_cast<u32x4*>(dst + f * 8) = ld128(src + e * H * I + (size_t)row * I + col);
 }
 
-// Variant of a launch.  An expert receives at most one pair per token of a
-// routed batch, so a batch of T tokens gives an expert at most ceil(T / kNT)
-// passes; the weighted walk (and the check that selects it, which costs a
-// little on every launch) is compiled in once that bound exceeds two, where
-// one popular expert could otherwise make a few blocks take three or more
-// times as long as the rest.  Guessing a fully active pool pays when the
-// expected number of idle experts, m (1 - k/m)^T, is well below one.
-struct WaveMode {
-  bool balance, speculate;
-};
+// Variant of a launch: the largest pass (column blocks) and the weight
+// pipeline depth.  An expert receives at most one pair per token of a routed
+// batch, so a batch of T tokens needs passes of T tokens for one stream per
+// expert: 2 column blocks up to 32 tokens, 4 up to 64, then the most that
+// fit the registers with no spill -- 8 (128 tokens) for gate/up with two
+// chunks in flight, 6 (96 tokens) for down with three.  An expert with more
+// pairs (only a larger batch, or an unrouted plan, gives one) takes further
+// passes.  Guessing a fully active pool pays when the expected number of
+// idle experts, m (1 - k/m)^T, is well below one (always assumed for
+// batches of up to 64 tokens, where a wrong guess costs one segment).
+int gate_up_column_blocks(int T) { return T <= kNT ? 2 : T <= 2 * kNT ? 4 : 8; }
+int down_column_blocks(int T) { return T <= kNT ? 2 : 6; }
 
-WaveMode wave_mode(int T, int m, int k) {
-  WaveMode md;
-  md.balance = T > 2 * kNT;
+bool speculate_full_pool(int T, int m, int k) {
   const double idle = m * std::pow(1.0 - (double)k / m, (double)T);
-  md.speculate = !md.balance || idle < 0.25;
-  return md;
+  return T <= 2 * kNT || idle < 0.25;
 }
 
 int stream_grid() {
@@ -794,16 +725,19 @@ hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bo
                                const int* counts, const int* offsets, const int* perm,
                                const int* active, const int* n_active, int H, int I, int m, int k,
                                uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
-  const WaveMode md = wave_mode(T, m, k);
-#define SW_GU(TI, BA, SP)                                                                      \
-  gate_up_wave_kernel<TI, BA, SP><<<stream_grid(), kBlk, 0, stream>>>(                          \
+  const int nb = gate_up_column_blocks(T);
+  const bool sp = speculate_full_pool(T, m, k);
+#define SW_GU(TI, SP, NB, D)                                                                   \
+  gate_up_wave_kernel<TI, SP, NB, D><<<stream_grid(), kBlk, 0, stream>>>(                       \
       x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k)
-  if (!md.balance) {
-    if (tiled) SW_GU(true, false, true); else SW_GU(false, false, true);
-  } else if (md.speculate) {
-    if (tiled) SW_GU(true, true, true); else SW_GU(false, true, true);
+  if (nb == 2) {
+    if (tiled) SW_GU(true, true, 2, 3); else SW_GU(false, true, 2, 3);
+  } else if (nb == 4) {
+    if (tiled) SW_GU(true, true, 4, 3); else SW_GU(false, true, 4, 3);
+  } else if (sp) {
+    if (tiled) SW_GU(true, true, 8, 2); else SW_GU(false, true, 8, 2);
   } else {
-    if (tiled) SW_GU(true, true, false); else SW_GU(false, true, false);
+    if (tiled) SW_GU(true, false, 8, 2); else SW_GU(false, false, 8, 2);
   }
 #undef SW_GU
   return hipGetLastError();
@@ -813,16 +747,17 @@ hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* co
                             const int* offsets, const int* perm, const int* active,
                             const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
                             const uint16_t* h_lo, float* y, hipStream_t stream) {
-  const WaveMode md = wave_mode(T, m, k);
-#define SW_DN(TI, BA, SP)                                                                      \
-  down_wave_kernel<TI, BA, SP><<<stream_grid(), kBlk, 0, stream>>>(                             \
+  const int nb = down_column_blocks(T);
+  const bool sp = speculate_full_pool(T, m, k);
+#define SW_DN(TI, SP, NB)                                                                      \
+  down_wave_kernel<TI, SP, NB, 3><<<stream_grid(), kBlk, 0, stream>>>(                          \
       h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k)
-  if (!md.balance) {
-    if (tiled) SW_DN(true, false, true); else SW_DN(false, false, true);
-  } else if (md.speculate) {
-    if (tiled) SW_DN(true, true, true); else SW_DN(false, true, true);
+  if (nb == 2) {
+    if (tiled) SW_DN(true, true, 2); else SW_DN(false, true, 2);
+  } else if (sp) {
+    if (tiled) SW_DN(true, true, 6); else SW_DN(false, true, 6);
   } else {
-    if (tiled) SW_DN(true, true, false); else SW_DN(false, true, false);
+    if (tiled) SW_DN(true, false, 6); else SW_DN(false, false, 6);
   }
 #undef SW_DN
   return hipGetLastError();

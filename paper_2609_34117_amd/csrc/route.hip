@@ -205,16 +205,25 @@ __global__ __launch_bounds__(256) void route_logits_wide_kernel(const uint16_t* 
 
 constexpr int kMaxSplit = 4;  // slices of H per logit tile
 
+// Columns of a routing call: the m experts the top-k selects from, whose
+// partial logits sit in rows of ld >= m columns (ld = m + 1 when the last
+// column is the shared expert's gate logit), the k routed slots and the S
+// slots of the shared expert's parts after them (ids m .. m + S - 1).
+struct Cols {
+  int m, ld, k, S;
+};
+
 // Order key of token t's logit for expert e: z = sum of the KS partials in
 // slice order, plus the bias; 0 marks an ineligible expert (the one logit
 // whose key is 0, a NaN, is nudged to 1).  All partial loads are issued
 // before the first add.
 __device__ __forceinline__ uint32_t logit_key(const float* __restrict__ part, int KS, int T,
-                                              int m, int t, int e, const float* __restrict__ bias,
+                                              const Cols& c, int t, int e,
+                                              const float* __restrict__ bias,
                                               const uint8_t* __restrict__ keep_mask) {
-  if (e >= m || (keep_mask != nullptr && keep_mask[e] == 0)) return 0u;
-  const float* p = part + (size_t)t * m + e;
-  const size_t plane = (size_t)T * m;
+  if (e >= c.m || (keep_mask != nullptr && keep_mask[e] == 0)) return 0u;
+  const float* p = part + (size_t)t * c.ld + e;
+  const size_t plane = (size_t)T * c.ld;
   float zp[kMaxSplit];
 #pragma unroll
   for (int ks = 0; ks < kMaxSplit; ++ks) zp[ks] = ks < KS ? p[ks * plane] : 0.f;
@@ -224,6 +233,23 @@ __device__ __forceinline__ uint32_t logit_key(const float* __restrict__ part, in
     if (ks < KS) z += zp[ks];
   if (bias != nullptr) z += bias[e];
   return max(f32_order_key(z), 1u);
+}
+
+// Gate of the shared expert for token t (Section 3.3): the sigmoid of its
+// gate logit, the partials of column m summed in slice order like every
+// other logit.
+__device__ __forceinline__ float shared_gate(const float* __restrict__ part, int KS, int T,
+                                             const Cols& c, int t) {
+  const float* p = part + (size_t)t * c.ld + c.m;
+  const size_t plane = (size_t)T * c.ld;
+  float zp[kMaxSplit];
+#pragma unroll
+  for (int ks = 0; ks < kMaxSplit; ++ks) zp[ks] = ks < KS ? p[ks * plane] : 0.f;
+  float z = zp[0];
+#pragma unroll
+  for (int ks = 1; ks < kMaxSplit; ++ks)
+    if (ks < KS) z += zp[ks];
+  return 1.0f / (1.0f + expf(-z));
 }
 
 // Reductions inside one 16-lane row (quad swaps, then the half-row and row
@@ -309,7 +335,7 @@ __device__ __forceinline__ uint32_t fadd_bits(uint32_t a, uint32_t b) {
 // variant's first four steps; the other rows only add +0 there, so both
 // variants give identical gates.
 template <int KPL>
-__device__ __forceinline__ Selection select_row(const float* part, int KS, int T, int m, int k,
+__device__ __forceinline__ Selection select_row(const float* part, int KS, int T, const Cols& c,
                                                 int t, const float* bias,
                                                 const uint8_t* keep_mask) {
   const int r = threadIdx.x & 15;
@@ -318,17 +344,17 @@ __device__ __forceinline__ Selection select_row(const float* part, int KS, int T
 #pragma unroll
   for (int q = 0; q < KPL; ++q) {
     eid[q] = q * 16 + r;
-    key[q] = t < T ? logit_key(part, KS, T, m, t, eid[q], bias, keep_mask) : 0u;
+    key[q] = t < T ? logit_key(part, KS, T, c, t, eid[q], bias, keep_mask) : 0u;
   }
   return select_topk<KPL>(
-      key, eid, k, r, [](uint32_t v) { return row_reduce_u32(v, 0u, umax); },
+      key, eid, c.k, r, [](uint32_t v) { return row_reduce_u32(v, 0u, umax); },
       [](uint32_t v) { return row_reduce_u32(v, 0xffffffffu, umin); },
       [](float v) { return __uint_as_float(row_reduce_u32(__float_as_uint(v), 0u, fadd_bits)); });
 }
 
 // Top-k of one token per wave: lane l holds the keys of experts q * 64 + l.
 template <int KPL>
-__device__ __forceinline__ Selection select_wave(const float* part, int KS, int T, int m, int k,
+__device__ __forceinline__ Selection select_wave(const float* part, int KS, int T, const Cols& c,
                                                  int t, const float* bias,
                                                  const uint8_t* keep_mask) {
   const int lane = threadIdx.x & 63;
@@ -337,20 +363,27 @@ __device__ __forceinline__ Selection select_wave(const float* part, int KS, int 
 #pragma unroll
   for (int q = 0; q < KPL; ++q) {
     eid[q] = q * 64 + lane;
-    key[q] = logit_key(part, KS, T, m, t, eid[q], bias, keep_mask);
+    key[q] = logit_key(part, KS, T, c, t, eid[q], bias, keep_mask);
   }
   return select_topk<KPL>(
-      key, eid, k, lane, [](uint32_t v) { return wave_max_u32(v); },
+      key, eid, c.k, lane, [](uint32_t v) { return wave_max_u32(v); },
       [](uint32_t v) { return wave_min_u32(v); }, [](float v) { return wave_sum_f32(v); });
 }
 
-__device__ __forceinline__ void store_selection(const Selection& s, int t, int k, int slot,
-                                                int* __restrict__ topk_ids,
+// Slot `slot` of token t: a routed slot (slot < k) takes the selection,
+// a shared slot k + s the shared expert's part m + s with the shared gate.
+__device__ __forceinline__ int slot_id(const Selection& s, const Cols& c, int slot) {
+  return slot < c.k ? s.id : c.m + slot - c.k;
+}
+
+__device__ __forceinline__ void store_selection(const Selection& s, int t, const Cols& c, int slot,
+                                                float sgate, int* __restrict__ topk_ids,
                                                 float* __restrict__ topk_w,
                                                 float* __restrict__ gap) {
-  if (slot < k) {
-    topk_ids[(size_t)t * k + slot] = s.id;
-    topk_w[(size_t)t * k + slot] = s.gate;
+  const int kout = c.k + c.S;
+  if (slot < kout) {
+    topk_ids[(size_t)t * kout + slot] = slot_id(s, c, slot);
+    topk_w[(size_t)t * kout + slot] = slot < c.k ? s.gate : sgate;
   }
   if (gap != nullptr && slot == 0) gap[t] = s.gap;
 }
@@ -361,19 +394,21 @@ template <int KPL, bool ROW>
 __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict__ part, int KS,
                                                         const float* __restrict__ bias,
                                                         const uint8_t* __restrict__ keep_mask,
-                                                        int T, int m, int k,
+                                                        int T, Cols c,
                                                         int* __restrict__ topk_ids,
                                                         float* __restrict__ topk_w,
                                                         float* __restrict__ gap) {
   if (ROW) {
     const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
-    const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
-    if (t < T) store_selection(s, t, k, threadIdx.x & 15, topk_ids, topk_w, gap);
+    const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
+    const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
+    if (t < T) store_selection(s, t, c, threadIdx.x & 15, sg, topk_ids, topk_w, gap);
   } else {
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;  // wave-uniform
-    const Selection s = select_wave<KPL>(part, KS, T, m, k, t, bias, keep_mask);
-    store_selection(s, t, k, threadIdx.x & 63, topk_ids, topk_w, gap);
+    const Selection s = select_wave<KPL>(part, KS, T, c, t, bias, keep_mask);
+    const float sg = c.S > 0 ? shared_gate(part, KS, T, c, t) : 0.f;
+    store_selection(s, t, c, threadIdx.x & 63, sg, topk_ids, topk_w, gap);
   }
 }
 
@@ -384,7 +419,9 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
 // from them (512 threads measured 0.4 us a step faster at one token than
 // 1024: the plan's barriers and LDS clearing cover half the waves).  Larger
 // batches take the multi-block top-k kernel and the dispatch kernel: one
-// block's SIMDs would serialise their selections.
+// block would serialise their selections and plan (a 1024-thread block for
+// 33-64 tokens measured 8.9 us at 64 tokens over 64 experts and 11.3 us
+// over 128, against 9.2 us for the two kernels).
 constexpr int kFusedThreads = 512;
 constexpr int kFusedMaxPool = 256;
 constexpr int kFusedMaxTokens = 32;
@@ -394,7 +431,7 @@ constexpr int kWaveFusedTokens = 4;  // one wave: 4 rows of 16 lanes, <= 64 pair
 template <int KPL>
 __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
     const float* __restrict__ part, int KS, const float* __restrict__ bias,
-    const uint8_t* __restrict__ keep_mask, int T, int m, int k, int* __restrict__ topk_ids,
+    const uint8_t* __restrict__ keep_mask, int T, Cols c, int* __restrict__ topk_ids,
     float* __restrict__ topk_w, float* __restrict__ gap, int* __restrict__ counts,
     int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
     int* __restrict__ n_active) {
@@ -405,16 +442,18 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
   __shared__ uint32_t scan_scratch[34];
   __shared__ int bad;
   const int t = threadIdx.x >> 4, r = threadIdx.x & 15;
+  const int kout = c.k + c.S;
   if ((threadIdx.x >> 6) * 4 < T) {  // wave-uniform
-    const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
+    const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
+    const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
     if (t < T) {
-      store_selection(s, t, k, r, topk_ids, topk_w, gap);
-      if (r < k) ids_s[t * k + r] = s.id;
+      store_selection(s, t, c, r, sg, topk_ids, topk_w, gap);
+      if (r < kout) ids_s[t * kout + r] = slot_id(s, c, r);
     }
   }
   __syncthreads();
   const DispatchLds lds{cursor, wave_base, wave_cnt, scan_scratch, &bad};
-  dispatch_block(ids_s, T * k, m, lds, counts, offsets, perm, active, n_active);
+  dispatch_block(ids_s, T * kout, c.m + c.S, lds, counts, offsets, perm, active, n_active);
 }
 
 // Route + dispatch of at most 4 tokens (at most 64 pairs) in one wave: the
@@ -425,17 +464,21 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
 template <int KPL>
 __global__ __launch_bounds__(64) void route_select_dispatch_wave_kernel(
     const float* __restrict__ part, int KS, const float* __restrict__ bias,
-    const uint8_t* __restrict__ keep_mask, int T, int m, int k, int* __restrict__ topk_ids,
+    const uint8_t* __restrict__ keep_mask, int T, Cols c, int* __restrict__ topk_ids,
     float* __restrict__ topk_w, float* __restrict__ gap, int* __restrict__ counts,
     int* __restrict__ offsets, int* __restrict__ perm, int* __restrict__ active,
     int* __restrict__ n_active) {
   const int lane = threadIdx.x, t = lane >> 4, r = lane & 15;
-  const Selection s = select_row<KPL>(part, KS, T, m, k, t, bias, keep_mask);
-  if (t < T) store_selection(s, t, k, r, topk_ids, topk_w, gap);
-  // pair q = t' * k + j was selected by lane 16 t' + j
-  const int n_pairs = T * k;
+  const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
+  const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
+  if (t < T) store_selection(s, t, c, r, sg, topk_ids, topk_w, gap);
+  // the plan covers the m selectable experts and the S shared parts (<= 256
+  // in all), kout slots a token; pair q = t' * kout + j is slot j of lane
+  // 16 t' + j
+  const int kout = c.k + c.S, m = c.m + c.S;
+  const int n_pairs = T * kout;
   const bool valid = lane < n_pairs;
-  const int e = __shfl(s.id, valid ? (lane / k) * 16 + lane % k : 0);
+  const int e = __shfl(slot_id(s, c, r), valid ? (lane / kout) * 16 + lane % kout : 0);
   if (__ballot(valid && (e < 0 || e >= m)) != 0) {  // the flagged plan
     for (int i = lane; i <= m; i += 64) {
       if (i < m) counts[i] = 0;
@@ -529,39 +572,39 @@ hipError_t launch_logits(const uint16_t* x, int T, const float* wr, int H, int m
 
 template <int KPL, bool ROW>
 void launch_topk_t(const float* part, int KS, const float* bias, const uint8_t* keep_mask, int T,
-                   int m, int k, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
+                   const Cols& c, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
   const int per_block = ROW ? 16 : 4;
   route_topk_kernel<KPL, ROW><<<(T + per_block - 1) / per_block, 256, 0, stream>>>(
-      part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap);
+      part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap);
 }
 
 void launch_topk(const float* part, int KS, const float* bias, const uint8_t* keep_mask, int T,
-                 int m, int k, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
+                 const Cols& c, int* topk_ids, float* topk_w, float* gap, hipStream_t stream) {
   // one token per 16-lane row for small batches; from 64 tokens on, one token
   // per wave (more waves in flight) measured faster: 8.3 against 12.5 us at
   // 4096 tokens, 2-3% of a 40-layer batch-256 step, 2 us of a batch-64 step
   // over 128 experts
-  if (k <= 16 && m <= 256 && T < 64) {
-    const int kpl = (m + 15) / 16;
+  if (c.k + c.S <= 16 && c.m <= 256 && T < 64) {
+    const int kpl = (c.m + 15) / 16;
     if (kpl <= 4)
-      launch_topk_t<4, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+      launch_topk_t<4, true>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
     else if (kpl <= 8)
-      launch_topk_t<8, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+      launch_topk_t<8, true>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
     else
-      launch_topk_t<16, true>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+      launch_topk_t<16, true>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
     return;
   }
-  const int kpl = (m + 63) / 64;
+  const int kpl = (c.m + 63) / 64;
   if (kpl <= 1)
-    launch_topk_t<1, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    launch_topk_t<1, false>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
   else if (kpl <= 2)
-    launch_topk_t<2, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    launch_topk_t<2, false>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
   else if (kpl <= 4)
-    launch_topk_t<4, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    launch_topk_t<4, false>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
   else if (kpl <= 8)
-    launch_topk_t<8, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    launch_topk_t<8, false>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
   else
-    launch_topk_t<16, false>(part, KS, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
+    launch_topk_t<16, false>(part, KS, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -693,43 +736,64 @@ size_t route_workspace_bytes(int T, int H, int m, int k) {
   return part_bytes(T, H, m) + dispatch_workspace_bytes(T * k, m);
 }
 
+size_t route_shared_workspace_bytes(int T, int H, int m, int k, int S) {
+  if (T <= 0) return 0;
+  return part_bytes(T, H, m + 1) + dispatch_workspace_bytes(T * (k + S), m + S);
+}
+
+namespace {
+
+// Logits of the c.ld router rows, then the top-k over the first c.m.
+hipError_t route_cols(const uint16_t* x, int T, const float* wr, const float* bias,
+                      const uint8_t* keep_mask, int H, const Cols& c, int* topk_ids,
+                      float* topk_w, float* gap, void* workspace, hipStream_t stream) {
+  float* part = static_cast<float*>(workspace);
+  const LogitsSplit sp = logits_split(T, H, c.ld);
+  hipError_t err = launch_logits(x, T, wr, H, c.ld, part, sp, stream);
+  if (err != hipSuccess) return err;
+  launch_topk(part, sp.ks, bias, keep_mask, T, c, topk_ids, topk_w, gap, stream);
+  return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* bias,
                         const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                         float* topk_w, float* gap, void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  float* part = static_cast<float*>(workspace);
-  const LogitsSplit sp = logits_split(T, H, m);
-  hipError_t err = launch_logits(x, T, wr, H, m, part, sp, stream);
-  if (err != hipSuccess) return err;
-  launch_topk(part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, stream);
-  return hipGetLastError();
+  return route_cols(x, T, wr, bias, keep_mask, H, Cols{m, m, k, 0}, topk_ids, topk_w, gap,
+                    workspace, stream);
 }
 
-bool fused_route_dispatch_supported(int T, int m, int k) {
-  return T > 0 && T <= kFusedMaxTokens && m <= kFusedMaxPool && k <= kFusedMaxK;
+bool fused_route_dispatch_supported(int T, int m, int k, int S) {
+  return T > 0 && T <= kFusedMaxTokens && m + S <= kFusedMaxPool && k + S <= kFusedMaxK;
 }
 
 hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
                                  const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                                  float* topk_w, float* gap, int* counts, int* offsets, int* perm,
-                                 int* active, int* n_active, void* workspace,
-                                 hipStream_t stream) {
-  if (!fused_route_dispatch_supported(T, m, k)) {
-    hipError_t err = launch_route(x, T, wr, bias, keep_mask, H, m, k, topk_ids, topk_w, gap,
+                                 int* active, int* n_active, void* workspace, hipStream_t stream,
+                                 int n_shared) {
+  const Cols c{m, n_shared > 0 ? m + 1 : m, k, n_shared};
+  const int kout = k + n_shared, m_plan = m + n_shared;
+  if (!fused_route_dispatch_supported(T, m, k, n_shared)) {
+    if (T > 0) {
+      hipError_t err = route_cols(x, T, wr, bias, keep_mask, H, c, topk_ids, topk_w, gap,
                                   workspace, stream);
-    if (err != hipSuccess) return err;
-    return launch_dispatch(topk_ids, T * k, m, counts, offsets, perm, active, n_active, stream,
-                           static_cast<char*>(workspace) + part_bytes(T, H, m));
+      if (err != hipSuccess) return err;
+    }
+    return launch_dispatch(topk_ids, T * kout, m_plan, counts, offsets, perm, active, n_active,
+                           stream, static_cast<char*>(workspace) + part_bytes(T, H, c.ld));
   }
   float* part = static_cast<float*>(workspace);
-  const LogitsSplit sp = logits_split(T, H, m);
-  hipError_t err = launch_logits(x, T, wr, H, m, part, sp, stream);
+  const LogitsSplit sp = logits_split(T, H, c.ld);
+  hipError_t err = launch_logits(x, T, wr, H, c.ld, part, sp, stream);
   if (err != hipSuccess) return err;
   const int kpl = (m + 15) / 16;
   if (T <= kWaveFusedTokens) {
 #define SW_WF(KPL)                                                                             \
-  route_select_dispatch_wave_kernel<KPL><<<1, 64, 0, stream>>>(part, sp.ks, bias, keep_mask, T, m, \
-                                                               k, topk_ids, topk_w, gap, counts,   \
+  route_select_dispatch_wave_kernel<KPL><<<1, 64, 0, stream>>>(part, sp.ks, bias, keep_mask, T, c, \
+                                                               topk_ids, topk_w, gap, counts,      \
                                                                offsets, perm, active, n_active)
     if (kpl <= 4)
       SW_WF(4);
@@ -740,18 +804,17 @@ hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, cons
 #undef SW_WF
     return hipGetLastError();
   }
+#define SW_FD(KPL)                                                                             \
+  route_select_dispatch_kernel<KPL><<<1, kFusedThreads, 0, stream>>>(                             \
+      part, sp.ks, bias, keep_mask, T, c, topk_ids, topk_w, gap, counts, offsets, perm, active,   \
+      n_active)
   if (kpl <= 4)
-    route_select_dispatch_kernel<4><<<1, kFusedThreads, 0, stream>>>(
-        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
-        active, n_active);
+    SW_FD(4);
   else if (kpl <= 8)
-    route_select_dispatch_kernel<8><<<1, kFusedThreads, 0, stream>>>(
-        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
-        active, n_active);
+    SW_FD(8);
   else
-    route_select_dispatch_kernel<16><<<1, kFusedThreads, 0, stream>>>(
-        part, sp.ks, bias, keep_mask, T, m, k, topk_ids, topk_w, gap, counts, offsets, perm,
-        active, n_active);
+    SW_FD(16);
+#undef SW_FD
   return hipGetLastError();
 }
 

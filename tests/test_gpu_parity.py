@@ -400,6 +400,42 @@ def test_weighted_walk_over_popular_experts(sw, hidden, n_experts, top_k, inter,
     assert all(int(counts[e]) == tokens for e in popular)
 
 
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
+    (2048, 64, 4, 512, 64, (3,)),      # 64-token batch: gate/up passes of 64 tokens, x in 2 K slices
+    (1056, 48, 4, 384, 80, (2,)),      # H 1056 (5 chunks, the last one K step): slices of 3 + 2 chunks
+    (2048, 32, 4, 1024, 120, (0, 1)),  # 120 pairs: gate/up 4 slices of 2 chunks; down 2 passes of
+                                       # 60 tokens over 2 h slices (I 1024)
+    (2048, 48, 4, 768, 100, (5,)),     # gate/up 4 slices; down 2 passes of 50 tokens, h slices of
+                                       # 2 + 1 chunks
+])
+@pytest.mark.parametrize("tiled", [False, True])
+def test_sliced_passes_stream_each_tile_once(sw, hidden, n_experts, top_k, inter, tokens, popular,
+                                             tiled):
+    # experts whose tokens do not fit in LDS with the whole contraction take
+    # sliced passes (K in slices, every token staged per slice); each output
+    # still accumulates over K in the same order, so it equals the same
+    # tokens run in small batches (whole-K passes) bit for bit
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=17)
+    bias = np.zeros(n_experts, np.float32)
+    bias[list(popular)] = 50.0
+    layout = sw.ROW_MAJOR
+    if tiled:
+        D = dict(D)
+        D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+        layout = sw.TILED
+    d = sw.dims(hidden, inter, n_experts, top_k)
+    assert sw.sw_moe_forward_kernels(d, tokens, layout) == ("wave", "wave")
+    # reference batches that divide the tokens and run whole-K passes of the
+    # same kernels (a ragged last batch could take the split-K kernels)
+    nb = next(b for b in (16, 20, 24, 30) if tokens % b == 0)
+    assert sw.sw_moe_forward_kernels(d, nb, layout) == ("wave", "wave")
+    s = check_layer(sw, cfg, L, D, None, bias=bias, layout=layout,
+                    what=f"sliced H={hidden} I={inter} T={tokens}")
+    assert all(int(s["counts"][e]) == tokens for e in popular)
+    small = _layer_in_batches(sw, D, top_k, nb, layout, bias=dev(bias))
+    assert torch.equal(s["gpu"]["out"], small)
+
+
 def test_bias_and_mask_together(sw):
     cfg = I.CONFIGS["skewed_stack"]
     small = I.MoEConfig("skew_small", cfg.config_id, hidden=256, n_experts=cfg.n_experts,
@@ -621,7 +657,9 @@ def _assert_same_route_dispatch(a, b):
     (512, 256, 1, 3, False, False),       # k = 1 on the one-wave path
     (256, 16, 2, 5, False, False),        # 5 tokens: the 512-thread block again
     (2048, 256, 16, 32, True, True),      # largest fused k
-    (2048, 128, 8, 64, False, False),     # 64 tokens: multi-block top-k, then dispatch
+    (2048, 128, 8, 33, True, False),      # 33 tokens: row-form multi-block top-k, then dispatch
+    (2048, 128, 8, 64, False, False),     # 64 tokens: wave-form top-k, then dispatch
+    (2048, 64, 16, 64, True, True),       # 1024 pairs, k = 16
     (2048, 256, 8, 256, False, True),     # 2048 pairs: the largest one-block dispatch
     (1024, 200, 16, 100, True, False),    # k = 16, ragged last top-k block
     (2048, 256, 8, 600, False, False),    # 4800 pairs: chunked multi-block dispatch
@@ -660,12 +698,14 @@ def test_route_dispatch_in_band_errors_and_empty_batch(sw):
     b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
     _assert_same_route_dispatch(a, b)
     assert int(b[3].n_active.item()) == -1      # the missing third choice flags the batch
-    # the same flag after the multi-block top-k (40 tokens, 120 pairs)
-    cfg, L, D = small_layer(64, 8, 3, 32, 40, seed=5)
-    a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
-    b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
-    _assert_same_route_dispatch(a, b)
-    assert int(b[3].n_active.item()) == -1
+    # the same flag after the multi-block top-k, row form (40 tokens) and
+    # wave form (70 tokens, 210 pairs)
+    for tokens in (40, 70):
+        cfg, L, D = small_layer(64, 8, 3, 32, tokens, seed=5)
+        a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
+        b = sw.sw_moe_route_dispatch(D["x"], D["wr"], 3, keep_mask=dev(mask))
+        _assert_same_route_dispatch(a, b)
+        assert int(b[3].n_active.item()) == -1
     # the same in-band flag from the chunked dispatch (3000 pairs)
     cfg, L, D = small_layer(64, 8, 3, 32, 1000, seed=4)
     a = _route_then_dispatch(sw, D["x"], D["wr"], 3, 8, keep_mask=dev(mask))
@@ -720,6 +760,97 @@ def test_shared_expert_zero_initialised_se2_is_se1_bit_for_bit(sw):
     merged = dev(base)
     sw.sw_moe_shared_expert(dev(x), dev(w13[None]), dev(w2[None]), dev(gate), merged)
     assert torch.equal(one, merged)
+
+
+def _shared_parts(w13s, w2s, inter, n_shared):
+    """The shared expert of width n_shared * I as n_shared experts of width I
+    in the pool layout: part s = the gate and up rows of its intermediate
+    units s*I .. (s+1)*I - 1, and the matching columns of its down
+    projection."""
+    isz = n_shared * inter
+    p13 = np.stack([np.concatenate([w13s[s * inter:(s + 1) * inter],
+                                    w13s[isz + s * inter:isz + (s + 1) * inter]])
+                    for s in range(n_shared)])
+    p2 = np.stack([np.ascontiguousarray(w2s[:, s * inter:(s + 1) * inter]) for s in range(n_shared)])
+    return p13, p2
+
+
+def _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled):
+    inter = L["w2"].shape[2]
+    p13, p2 = _shared_parts(w13s, w2s, inter, n_shared)
+    w13 = dev(np.concatenate([L["w13"], p13]))
+    w2 = dev(np.concatenate([L["w2"], p2]))
+    layout = sw.ROW_MAJOR
+    if tiled:
+        w13, w2 = sw.sw_moe_pack_experts(w13, w2)
+        layout = sw.TILED
+    wr = dev(np.concatenate([L["wr"], gate[None]]))
+    ids, w, gap, plan = sw.sw_moe_route_dispatch_shared(
+        dev(L["x"]), wr, top_k, n_shared, keep_mask=None if mask is None else dev(mask))
+    out = sw.sw_moe_forward(dev(L["x"]), w13, w2, w, plan, layout=layout)
+    return ids, w, gap, plan, out
+
+
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,n_shared,masked,tiled", [
+    (2048, 64, 8, 512, 64, 2, False, True),    # batch 64: the 1024-thread route + plan block
+    (2048, 128, 8, 512, 1, 2, True, False),    # one token: the one-wave route + plan
+    (2048, 64, 8, 768, 17, 1, False, False),   # 17 tokens: the 512-thread block, one part
+    (2048, 256, 8, 512, 100, 2, False, True),  # 100 tokens: the wave-form top-k, then dispatch
+    (1024, 200, 14, 256, 40, 2, True, False),  # k + parts = 16: the row form at its limit
+    (2048, 96, 6, 512, 200, 4, False, False),  # 4 parts: 200-token parts over gate/up passes
+])
+def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter, tokens, n_shared,
+                                            masked, tiled):
+    # Section 3.3: the always-on shared expert behind a sigmoid gate, run as
+    # n_shared extra experts every token routes to
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=23)
+    g = np.random.default_rng([401, hidden, tokens])
+    isz = n_shared * inter
+    w13s = I.to_bf16_bits(0.02 * g.standard_normal((2 * isz, hidden), dtype=np.float32))
+    w2s = I.to_bf16_bits(0.02 * g.standard_normal((hidden, isz), dtype=np.float32))
+    gate = (0.05 * g.standard_normal(hidden)).astype(np.float32)
+    mask = mask_for(cfg, L, 0.5) if masked else None
+    ids, w, gap, plan, out = _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled)
+    ids, w, gap = host(ids), host(w), host(gap)
+    m, k = n_experts, top_k
+    # routed slots: the oracle's routing rule; shared slots: every part, with
+    # the sigmoid of the gate logit
+    o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], k, keep_mask=mask, want_logits=True)
+    compare_routing(ids[:, :k], w[:, :k], o_ids, o_w, o_z, mask, k, g_gap=gap, o_gap=o_gap,
+                    what=f"folded shared T={tokens}")
+    xf = I.bf16_bits_to_f32(L["x"]).astype(np.float64)
+    sig = 1.0 / (1.0 + np.exp(-(xf @ gate.astype(np.float64))))
+    for s in range(n_shared):
+        assert np.all(ids[:, k + s] == m + s)
+        np.testing.assert_allclose(w[:, k + s], sig, rtol=0, atol=1e-6)
+    counts, offsets, perm, active, n_active = oracle.dispatch(ids, m + n_shared)
+    np.testing.assert_array_equal(host(plan.counts), counts)
+    np.testing.assert_array_equal(host(plan.offsets), offsets)
+    np.testing.assert_array_equal(host(plan.perm)[: ids.size], perm)
+    assert int(host(plan.n_active)[0]) == n_active
+    np.testing.assert_array_equal(host(plan.active)[:n_active], active)
+    # output: the routed layer plus the shared expert, as the oracle defines it
+    o_out = oracle_forward_rows(oracle.forward, L["x"], L["w13"], L["w2"],
+                                np.ascontiguousarray(ids[:, :k]), np.ascontiguousarray(w[:, :k]))
+    o_out = oracle.shared_expert(L["x"], w13s, w2s, gate, out=o_out)
+    err, rel = compare_out(host(out), o_out)
+    print(f"folded shared H={hidden} m={m} k={k} I={inter} T={tokens} parts={n_shared}: "
+          f"max|err|={err:.3g} rel={rel:.3g}")
+
+
+def test_folded_shared_expert_zero_se2_is_se1_bit_for_bit(sw):
+    # SE2's down projection starts at zero (Section 3.3): its part adds +0 to
+    # every output, so the folded SE1 + SE2 equals the folded SE1 alone
+    cfg, L, D = small_layer(2048, 64, 8, 512, 48, seed=29)
+    g = np.random.default_rng(31)
+    w13s = I.to_bf16_bits(0.02 * g.standard_normal((2 * 1024, 2048), dtype=np.float32))
+    w2s = I.to_bf16_bits(0.02 * g.standard_normal((2048, 1024), dtype=np.float32))
+    w2s[:, 512:] = 0
+    gate = (0.05 * g.standard_normal(2048)).astype(np.float32)
+    se1_13 = np.concatenate([w13s[:512], w13s[1024:1536]])
+    two = _folded_layer(sw, L, w13s, w2s, gate, 8, 2, None, True)
+    one = _folded_layer(sw, L, se1_13, np.ascontiguousarray(w2s[:, :512]), gate, 8, 1, None, True)
+    assert torch.equal(two[4], one[4])
 
 
 # --------------------------------------------------------------------------
