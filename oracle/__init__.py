@@ -4,6 +4,7 @@ Only the tests, the smoke check and the benchmark's CPU-baseline leg may use
 this package.  It shares no code with the HIP library.
 """
 from .oracle import (  # noqa: F401
+    CFLAGS,
     build,
     dispatch,
     forward,
