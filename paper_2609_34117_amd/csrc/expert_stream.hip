@@ -6,7 +6,10 @@
 //   - A persistent grid of one 8-wave block per compute unit.  The tiles of
 //     all active experts form one list; block b owns the contiguous,
 //     equal-sized range b*per .. (b+1)*per of it, which crosses at most a few
-//     expert boundaries ("segments").
+//     expert boundaries ("segments").  When some expert has more tokens than
+//     a whole-K pass holds, the blocks instead own equal runs of estimated
+//     cost (the cost-weighted walk below), so that the tiles of popular
+//     experts, which cost more each, are spread over more blocks.
 //   - Each wave owns whole tiles (16 weight rows over the full K) and
 //     streams them as 8 KiB chunks through a kDepth-deep register pipeline
 //     (3, or 2 where a wide pass needs the registers for its accumulators):
@@ -22,9 +25,11 @@
 //     into slices of whole chunks that fit for all of the tokens: the block
 //     takes one tile per wave at a time, and for each slice stages that
 //     slice of every token row, then each wave streams its tile's chunks of
-//     the slice into accumulators that live across the slices.  A popular
-//     expert thus costs the same weight bytes as any other; its tokens are
-//     re-read from L2 once per group of 8 tiles.
+//     the slice into accumulators that live across the slices.  Where two
+//     slices fit, they alternate between two LDS buffers and each is staged
+//     a whole slice ahead of its use.  A popular expert thus costs the same
+//     weight bytes as any other; its tokens are re-read from L2 once per
+//     group of 8 tiles.
 //   - Every step issues the same memory operations (out-of-range offsets
 //     for missing chunks and for epilogue stores on non-final chunks), so
 //     the compiler's wait counts are exact and the pipeline never drains on
@@ -48,6 +53,7 @@ constexpr int kKC = 8;            // 32-wide K steps per streamed chunk
 constexpr int kChunkCols = 32 * kKC;
 constexpr int kNT = 32;           // tokens of the whole-K pass of a small batch
 constexpr int kPad = 8;           // bf16 elements of padding per staged row
+constexpr int kMaxExperts = 1024;  // pool size limit of the library (routed + shared parts)
 // LDS of the staged activations (bf16 elements): 32 whole rows of the
 // largest H, or of both h planes at the largest I, with room to spare for
 // the sliced passes' larger token counts
@@ -104,9 +110,33 @@ __device__ __forceinline__ void slice_barrier_after() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
+// A double-buffered slice's wait: every staging load of this wave issued
+// before the last `after` vector-memory operations has landed, and this
+// wave's LDS accesses are done.  `after` (wave-uniform, 0..63) is rounded
+// down to a multiple of 8, which only waits for more.
+__device__ __forceinline__ void wait_staged_before(int after) {
+  switch (after >> 3) {
+    case 0: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(0)); break;
+    case 1: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(8)); break;
+    case 2: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(16)); break;
+    case 3: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(24)); break;
+    case 4: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(32)); break;
+    case 5: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(40)); break;
+    case 6: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(48)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_at_most_lds_done(56)); break;
+  }
+}
+
+// LDS offset (elements) of slice sigma's buffer: the two halves of the
+// staging area alternate on a double-buffered pass.
+__device__ __forceinline__ int slice_buffer(bool dbl, int sigma) {
+  return (dbl && (sigma & 1)) ? kStage / 2 : 0;
+}
+
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
+  int w_end;   // cost position after the segment (cost-weighted walk)
   bool e_ok;   // expert id in range: its weights may be read
 };
 
@@ -127,6 +157,7 @@ __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const
   s.e = s.e_ok ? e : 0;
   s.cnt = counts[s.e];
   s.base = offsets[s.e];
+  s.w_end = 0;
   return s;
 }
 
@@ -148,14 +179,17 @@ __device__ __forceinline__ void block_range(int total, int* r_lo, int* r_hi) {
 
 // How one pass of a segment is staged.  A pass takes up to pmax tokens
 // (passes of a segment are balanced); `planes` staged rows per token (1:
-// x, 2: h hi and lo) of K columns.  Whole-K when all of them fit, else the
-// widest slice of whole chunks that fits.
+// x, 2: h hi and lo) of K columns.  Whole-K when all of them fit.  Else the
+// widest slice of whole chunks of which two fit ("double-buffered": the
+// next slice is staged while the current one is read), or failing that of
+// which one fits.
 struct PassShape {
   int n;       // tokens of the pass
   int nbn;     // 16-token MFMA column blocks
   int cps;     // chunks per K slice (cpt for a whole-K pass)
   int stride;  // LDS elements per staged row
   bool sliced;
+  bool dbl;    // sliced into two LDS buffers (at 0 and kStage / 2)
 };
 
 __device__ __forceinline__ int pass_tokens(int cnt, int pmax) {
@@ -168,17 +202,153 @@ __device__ __forceinline__ PassShape pass_shape(int n, int K, int cpt, int plane
   ps.n = n;
   ps.nbn = (n + 15) >> 4;
   const int rows = ps.nbn * 16 * planes;
+  ps.dbl = false;
   if (rows * (K + kPad) <= kStage) {
     ps.cps = cpt;
     ps.stride = K + kPad;
     ps.sliced = false;
   } else {
-    const int c = (kStage / rows - kPad) / kChunkCols;
+    const int c2 = (kStage / 2 / rows - kPad) / kChunkCols;
+    const int c = c2 >= 1 ? c2 : (kStage / rows - kPad) / kChunkCols;
     ps.cps = max(1, min(c, cpt));
     ps.stride = ps.cps * kChunkCols + kPad;
     ps.sliced = true;
+    ps.dbl = c2 >= 1;
   }
   return ps;
+}
+
+// Cost-weighted walk.  Equal tile ranges balance the blocks when every
+// expert takes one whole-K pass.  A sliced pass costs more per tile: its
+// waves meet at a barrier on every slice, its tokens are staged again for
+// every group of tiles, and its wider passes take more MFMA and LDS work.
+// Per-block timings put a double-buffered sliced tile of 3 to 6 column
+// blocks at 2.9 to 4 times a whole-K tile, and a single-buffered slice
+// (which drains the weight pipeline) at about one whole-K tile.  Every extra
+// pass streams the tile again.  So when some expert needs a sliced pass or
+// several passes, the blocks take equal runs of cost instead: expert slot
+// a's tiles each cost tile_cost(count) units and start at wp[a] + i * cost,
+// and block b owns the tiles whose start lies in its run.  A popular expert
+// is then spread over more blocks instead of lengthening the few that own
+// its tiles.
+constexpr int kCostWholeK = 8;     // one whole-K pass over a tile
+constexpr int kCostSliced = 6;     // added per tile by a double-buffered sliced pass
+constexpr int kCostSlicedNb = 3;   // ... and per 16-token column block of it
+constexpr int kCostSlice1 = 8;     // added per K slice of a single-buffered pass
+
+__device__ __forceinline__ int pass_cost(int n, int K, int cpt, int planes) {
+  const PassShape ps = pass_shape(n, K, cpt, planes);
+  if (!ps.sliced) return kCostWholeK;
+  if (ps.dbl) return kCostWholeK + kCostSliced + kCostSlicedNb * ps.nbn;
+  return kCostWholeK + kCostSlice1 * ((cpt + ps.cps - 1) / ps.cps);
+}
+
+// Cost of one tile of an expert with n pairs, in passes of at most pmax.
+__device__ __forceinline__ int tile_cost(int n, int pmax, int K, int cpt, int planes) {
+  if (n <= 0) return 0;
+  const int np = (n + pmax - 1) / pmax, per = (n + np - 1) / np;
+  return (np - 1) * pass_cost(per, K, cpt, planes) + pass_cost(n - (np - 1) * per, K, cpt, planes);
+}
+
+// Tokens of the largest whole-K pass.
+__device__ __forceinline__ int whole_k_tokens(int pmax, int K, int planes) {
+  return min(pmax, 16 * (kStage / (16 * planes * (K + kPad))));
+}
+
+// Offsets of experts 2t .. 2t + 2 (thread t): one round of independent
+// loads at the kernel's start, with indices clamped to offsets[m] (past m
+// the differences are 0).
+struct PairCounts {
+  int o0, o1, o2;
+};
+
+__device__ __forceinline__ PairCounts load_pair_counts(const int* offsets, int m) {
+  const int e0 = 2 * (int)threadIdx.x;
+  return PairCounts{offsets[min(e0, m)], offsets[min(e0 + 1, m)], offsets[min(e0 + 2, m)]};
+}
+
+// Whether some expert has more pairs than a whole-K pass holds (a garbage
+// plan can only make this true, which takes the checked weighted walk):
+// each wave posts its verdict to its own LDS slot before a barrier the
+// kernel has anyway, and every thread reads the eight slots after it.
+// m <= 2 * kBlk.
+__device__ __forceinline__ void post_heavy_verdict(const PairCounts& c, int light, int* verdict) {
+  const bool big = c.o1 - c.o0 > light || c.o2 - c.o1 > light;
+  const bool any = __ballot(big) != 0;
+  if ((threadIdx.x & 63) == 0) verdict[threadIdx.x >> 6] = any ? 1 : 0;
+}
+
+__device__ __forceinline__ bool read_heavy_verdict(const int* verdict) {
+  int v = 0;
+#pragma unroll
+  for (int w = 0; w < kWv; ++w) v |= verdict[w];
+  return v != 0;
+}
+
+// The same with a barrier of its own.  Every thread of the block calls it.
+__device__ __forceinline__ bool some_expert_is_heavy(const PairCounts& c, int light,
+                                                     int* verdict) {
+  post_heavy_verdict(c, light, verdict);
+  __syncthreads();
+  return read_heavy_verdict(verdict);
+}
+
+// wp[a] = cost before active slot a's tiles, wp[n_act] = the total.  Every
+// thread of the block calls it; n_act <= 2 * kBlk.
+__device__ void weighted_work(int n_act, int tpe, const int* active, const int* counts,
+                              const int* offsets, int m, int n_pairs, int pmax, int K, int cpt,
+                              int planes, int* wp, uint32_t* scan) {
+  auto cost = [&](int a) {
+    if (a >= n_act) return 0;
+    const int e = active[a];
+    if (e < 0 || e >= m) return 0;
+    const int c = counts[e], b = offsets[e];
+    if (c <= 0 || b < 0 || c > n_pairs - b) return 0;
+    return tpe * tile_cost(c, pmax, K, cpt, planes);
+  };
+  const int a0 = 2 * (int)threadIdx.x;
+  const int c0 = cost(a0), c1 = cost(a0 + 1);
+  uint32_t off, unused, total, unused_t;
+  block_exclusive_scan2((uint32_t)(c0 + c1), 0u, scan, &off, &unused, &total, &unused_t);
+  if (a0 < n_act) wp[a0] = (int)off;
+  if (a0 + 1 < n_act) wp[a0 + 1] = (int)off + c0;
+  if (threadIdx.x == 0) wp[n_act] = (int)total;
+  __syncthreads();
+}
+
+// Segment of the weighted walk from cost position w: the first tile whose
+// start is at or after w, and the following tiles of its expert whose starts
+// lie before w_hi.  s.lo == s.hi when no tile starts in [w, w_hi).
+__device__ __forceinline__ Segment weighted_segment(int w, int w_hi, int n_act, const int* wp,
+                                                    int tpe, const int* active,
+                                                    const int* counts, const int* offsets,
+                                                    int m) {
+  int a = 0, hi = n_act - 1;  // the last slot a with wp[a] <= w
+  while (a < hi) {
+    const int mid = (a + hi + 1) >> 1;
+    if (wp[mid] <= w)
+      a = mid;
+    else
+      hi = mid - 1;
+  }
+  Segment s;
+  int c = (wp[a + 1] - wp[a]) / tpe, i0 = c > 0 ? (w - wp[a] + c - 1) / c : tpe;
+  while (i0 >= tpe && a + 1 < n_act && wp[a + 1] < w_hi) {  // the next expert's first tile
+    ++a;
+    c = (wp[a + 1] - wp[a]) / tpe;
+    i0 = c > 0 ? 0 : tpe;
+  }
+  const int i1 = c > 0 ? min(tpe, (w_hi - wp[a] + c - 1) / c) : 0;
+  s.a = a;
+  s.lo = a * tpe + min(i0, tpe);
+  s.hi = a * tpe + max(min(i0, tpe), i1);
+  s.w_end = i1 >= tpe ? wp[a + 1] : w_hi;
+  const int e = active[a];
+  s.e_ok = e >= 0 && e < m;
+  s.e = s.e_ok ? e : 0;
+  s.cnt = counts[s.e];
+  s.base = offsets[s.e];
+  return s;
 }
 
 // ---------------------------------------------------------------------------
@@ -189,6 +359,8 @@ struct GuWave {
   const uint16_t* xs;  // LDS activations [rows][stride]
   int H, I, nsteps, cpt, lane, r, kg, wave;
   int seg_lo, seg_hi, a, tpe, p0, cnt, nbn, cps, stride;
+  int nsl;   // K slices per tile (1 on a whole-K pass)
+  bool dbl;  // double-buffered slices
 };
 
 // Weight chunk q (tile j = q / cpt of this wave, chunk c) of the segment.
@@ -233,12 +405,14 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  // column of a K step inside the staged slice
-  const int step0 = (c / g.cps) * g.cps * kKC;
+  // column of a K step inside the staged slice, and the slice's buffer
+  const int sl = c / g.cps;
+  const int step0 = sl * g.cps * kKC;
+  const uint16_t* xb = g.xs + slice_buffer(g.dbl, j * g.nsl + sl);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     if (have && nb < g.nbn) {
-      const uint16_t* row = g.xs + (nb * 16 + g.r) * g.stride + g.kg * 8;
+      const uint16_t* row = xb + (nb * 16 + g.r) * g.stride + g.kg * 8;
       u32x4 B[kKC];
 #pragma unroll
       for (int s = 0; s < kKC; ++s) {
@@ -283,16 +457,31 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
   }
 }
 
-// The chunk loop of one pass.  Chunk q lives in A[q % kDepth]; the issue
-// for q + kDepth - 1 goes out before the compute of q.  A sliced pass
-// stages slice c / cps before chunk c of each tile group: after a barrier
-// (every wave is done with the previous slice) the slice's loads go out,
-// then the chunk kDepth - 1 ahead, then a wait that leaves exactly that
-// chunk's kKC loads outstanding, and a barrier.  Q is the same on every
-// wave of a sliced pass, so every wave meets every barrier.
+// The chunk loop of one pass.  Chunk q lives in A[q % D]; the issue for
+// q + D - 1 goes out before the compute of q.  Q is the same on every wave
+// of a sliced pass, so every wave meets every barrier.
+//   Single-buffered slices: slice c / cps is staged before chunk c of each
+//     tile group: after a barrier (every wave is done with the previous
+//     slice) its loads go out, then the chunk D - 1 ahead, then a wait that
+//     leaves exactly that chunk's kKC loads outstanding, and a barrier.
+//   Double-buffered slices: the slices of the pass (sigma = 0, 1, ... over
+//     the tile groups) alternate between the two buffers.  At the first
+//     step of slice sigma a wait lands sigma's staging (issued a whole
+//     slice earlier) without waiting for the weight chunks issued after it,
+//     then a barrier; after it every wave is done with slice sigma - 1, so
+//     slice sigma + 1 is staged into that buffer at once, a whole slice of
+//     steps before it is read.  The first slice, staged before the loop,
+//     waits for everything.
 template <bool kTiled, int D, int NB, typename Stage>
 __device__ __forceinline__ void gu_run(const GuWave& g, u32x4 (&A)[D][kKC], int Q, bool sliced,
                                        Stage&& stage) {
+  // vector-memory operations of one step (its weight chunk and its stores),
+  // and those issued after a slice's staging before the slice is read (at
+  // least one slice of steps)
+  constexpr int kStepOps = kKC + 2 * NB;
+  const int min_len = min(g.cps, g.cpt - (g.nsl - 1) * g.cps);
+  const int after = min(63, min_len * kStepOps);
+  const int n_slices = g.nsl * (Q / g.cpt);
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -300,14 +489,25 @@ __device__ __forceinline__ void gu_run(const GuWave& g, u32x4 (&A)[D][kKC], int 
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int qd = q + d;
-      const bool restage = sliced && qd < Q && (qd % g.cpt) % g.cps == 0;
-      if (restage) {
+      const int j = qd / g.cpt, c = qd - j * g.cpt, sl = c / g.cps;
+      const bool first = sliced && qd < Q && c == sl * g.cps;
+      if (first && !g.dbl) {
         slice_barrier_before();
-        stage((qd % g.cpt) / g.cps);
+        stage(sl, 0);
         __builtin_amdgcn_sched_barrier(0);  // the slice's loads, then the weights
       }
+      if (first && g.dbl) {
+        const int sigma = j * g.nsl + sl;
+        wait_staged_before(sigma == 0 ? 0 : after);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        if (sigma + 1 < n_slices) {
+          stage(sl + 1 < g.nsl ? sl + 1 : 0, slice_buffer(true, sigma + 1));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
       gu_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
-      if (restage) slice_barrier_after<kKC>();
+      if (first && !g.dbl) slice_barrier_after<kKC>();
       if (d == 0 || qd < Q) gu_compute<NB>(g, qd, A[d], acc);
     }
   }
@@ -325,8 +525,14 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
   constexpr int kPmax = 16 * kNbMax;
+  // batches of more than 32 tokens can give an expert more pairs than a
+  // whole-K pass holds: the cost-weighted walk is compiled in
+  constexpr bool kBalance = kNbMax > 2;
   __shared__ __attribute__((aligned(16))) uint16_t xs[kStage];
   __shared__ int pid[kPmax];
+  __shared__ int wp[kBalance ? kMaxExperts + 1 : 1];
+  __shared__ uint32_t scan[34];
+  __shared__ int verdict[kWv];
   const int tpe = I / 8;
   const int n_act = *n_active_p;
   const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
@@ -360,6 +566,8 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   // alone, so that segment's plan loads and weight chunks go out together
   // with the n_active load.  A wrong guess redoes the first segment.
   // (Without kSpeculate the first segment waits for n_active instead.)
+  const int light = whole_k_tokens(kPmax, H, 1);
+  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
   int r_lo = 0, r_hi = 0;
   Segment sg;
   if constexpr (kSpeculate) {
@@ -369,17 +577,45 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   }
   if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
   const bool all = n_act == m;
+  // With kBalance, whether some expert needs a sliced pass or several passes
+  // is decided once, at the first barrier of the block's first pass (its
+  // pair-id loads are already out then); a block without such a barrier
+  // decides it on a barrier of its own.  If one does, the block switches to
+  // its run of the cost-weighted walk.
+  bool checked = !kBalance, weighted = false;
+  int w_hi = 0;
+  auto go_weighted = [&]() {
+    weighted = true;
+    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, kPmax, H, g.cpt, 1, wp, scan);
+    block_range(wp[n_act], &r_lo, &w_hi);
+    if (r_lo >= w_hi) return false;
+    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    if (sg.lo >= sg.hi) return false;
+    begin_segment(sg);
+    return true;
+  };
   if (!kSpeculate || !all) {
     block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo >= r_hi) return;
-    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
-    begin_segment(sg);
-  } else if (r_lo >= r_hi) {
-    return;
+    if (r_lo < r_hi) {
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
+      begin_segment(sg);
+    }
+  }
+  if (r_lo >= r_hi) {
+    if (!kBalance) return;
+    checked = true;
+    if (!some_expert_is_heavy(pc, light, verdict) || !go_weighted()) return;
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
+    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
+      checked = true;
+      if (some_expert_is_heavy(pc, light, verdict)) {
+        if (!go_weighted()) return;
+        continue;
+      }
+    }
     g.cnt = sg.cnt;
     const uint32_t hbytes = 2u * (uint32_t)sg.cnt * (uint32_t)I;
     g.hh = make_rsrc(h_hi + (size_t)sg.base * I, hbytes);
@@ -390,12 +626,15 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const int seg_n = sg.hi - sg.lo;
     const int ntw = seg_n > g.wave ? (seg_n - g.wave + kWv - 1) / kWv : 0;
     const int ngroups = (seg_n + kWv - 1) / kWv;
+    bool restart = false;
     for (int p0 = 0; p0 < sg.cnt; p0 += per_pass) {
       const PassShape ps = pass_shape(min(per_pass, sg.cnt - p0), H, g.cpt, 1);
       g.p0 = p0;
       g.nbn = ps.nbn;
       g.cps = ps.cps;
       g.stride = ps.stride;
+      g.nsl = (g.cpt + ps.cps - 1) / ps.cps;
+      g.dbl = ps.dbl;
       const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
       if (p0 > 0) {
 #pragma unroll
@@ -408,34 +647,54 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
         const int p = perm[sg.base + p0 + (int)threadIdx.x];
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
+      if (!checked) post_heavy_verdict(pc, light, verdict);
       __syncthreads();
+      if (!checked) {
+        checked = true;
+        if (read_heavy_verdict(verdict)) {
+          restart = true;
+          break;
+        }
+      }
       if ((int)threadIdx.x < kPmax) pid[threadIdx.x] = pv;
       __syncthreads();
       // K slice `sl` (all of K on a whole-K pass) of the pass's token rows
-      // of x, straight into LDS: wave w stages rows w, w + kWv, ... (rows
-      // without a pair read zeros)
-      auto stage = [&](int sl) {
+      // of x, straight into the LDS buffer at element `boff`: wave w stages
+      // rows w, w + kWv, ... (rows without a pair read zeros)
+      auto stage = [&](int sl, int boff) {
         const int col0 = sl * g.cps * kChunkCols;
         const int bytes = 2 * min(g.cps * kChunkCols, H - col0);
         for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
           const int p = pid[tok];
           stage_row(xr, p >= 0 ? ((uint32_t)(p / k) * (uint32_t)H + (uint32_t)col0) * 2u
                                : kOutOfRange,
-                    xs + tok * g.stride, bytes, g.lane);
+                    xs + boff + tok * g.stride, bytes, g.lane);
         }
       };
       if (!ps.sliced) {
-        stage(0);
+        stage(0, 0);
         __builtin_amdgcn_s_waitcnt(kVmcntZero);
         __syncthreads();
+      } else if (ps.dbl) {
+        stage(0, 0);  // landed by the wait at the loop's first step
       }
       if (kNbMax == 2 || ps.nbn <= 2)
         gu_run<kTiled, kDepth, 2>(g, A, Q, ps.sliced, stage);
       else
         gu_run<kTiled, kDepth, kNbMax>(g, A, Q, ps.sliced, stage);
     }
-    if (sg.hi >= r_hi) break;
-    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    if (restart) {
+      if (!go_weighted()) return;
+      continue;
+    }
+    if (weighted) {
+      if (sg.w_end >= w_hi) break;
+      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+      if (sg.lo >= sg.hi) break;
+    } else {
+      if (sg.hi >= r_hi) break;
+      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    }
     begin_segment(sg);
   }
 }
@@ -449,6 +708,8 @@ struct DnWave {
   const int* pid;      // LDS pair ids of the pass
   int H, I, nsteps, cpt, lane, r, kg, wave;
   int seg_lo, seg_hi, a, tpe, nbn, cps, stride, lo_off;
+  int nsl;   // K slices per tile (1 on a whole-K pass)
+  bool dbl;  // double-buffered slices
 };
 
 template <bool kTiled>
@@ -485,11 +746,13 @@ __device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int step0 = (c / g.cps) * g.cps * kKC;
+  const int sl = c / g.cps;
+  const int step0 = sl * g.cps * kKC;
+  const uint16_t* hb = g.hs + slice_buffer(g.dbl, j * g.nsl + sl);
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     if (have && nb < g.nbn) {
-      const uint16_t* row = g.hs + (nb * 16 + g.r) * g.stride + g.kg * 8;
+      const uint16_t* row = hb + (nb * 16 + g.r) * g.stride + g.kg * 8;
 #pragma unroll
       for (int s = 0; s < kKC; ++s) {
         const int step = c * kKC + s;
@@ -515,9 +778,14 @@ __device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (
   }
 }
 
+// As gu_run; a down step stores one y fragment per column block.
 template <bool kTiled, int D, int NB, typename Stage>
 __device__ __forceinline__ void dn_run(const DnWave& g, u32x4 (&A)[D][kKC], int Q, bool sliced,
                                        Stage&& stage) {
+  constexpr int kStepOps = kKC + NB;
+  const int min_len = min(g.cps, g.cpt - (g.nsl - 1) * g.cps);
+  const int after = min(63, min_len * kStepOps);
+  const int n_slices = g.nsl * (Q / g.cpt);
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -525,14 +793,25 @@ __device__ __forceinline__ void dn_run(const DnWave& g, u32x4 (&A)[D][kKC], int 
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int qd = q + d;
-      const bool restage = sliced && qd < Q && (qd % g.cpt) % g.cps == 0;
-      if (restage) {
+      const int j = qd / g.cpt, c = qd - j * g.cpt, sl = c / g.cps;
+      const bool first = sliced && qd < Q && c == sl * g.cps;
+      if (first && !g.dbl) {
         slice_barrier_before();
-        stage((qd % g.cpt) / g.cps);
+        stage(sl, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
+      if (first && g.dbl) {
+        const int sigma = j * g.nsl + sl;
+        wait_staged_before(sigma == 0 ? 0 : after);
+        __builtin_amdgcn_s_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+        if (sigma + 1 < n_slices) {
+          stage(sl + 1 < g.nsl ? sl + 1 : 0, slice_buffer(true, sigma + 1));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
       dn_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
-      if (restage) slice_barrier_after<kKC>();
+      if (first && !g.dbl) slice_barrier_after<kKC>();
       if (d == 0 || qd < Q) dn_compute<NB>(g, qd, A[d], acc);
     }
   }
@@ -546,8 +825,12 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     const int* __restrict__ active, const int* __restrict__ n_active_p, float* __restrict__ y,
     int H, int I, int m, int n_pairs) {
   constexpr int kPmax = 16 * kNbMax;
+  constexpr bool kBalance = kNbMax > 2;  // as in gate_up_wave_kernel
   __shared__ __attribute__((aligned(16))) uint16_t hs[kStage];
   __shared__ int pid[kPmax];
+  __shared__ int wp[kBalance ? kMaxExperts + 1 : 1];
+  __shared__ uint32_t scan[34];
+  __shared__ int verdict[kWv];
   const int tpe = (H + 15) / 16;
   const int n_act = *n_active_p;
 
@@ -578,7 +861,10 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, A[d]);
   };
 
-  // Speculate a fully active pool, as in gate_up_wave_kernel.
+  // Speculate a fully active pool, and walk by cost when some expert needs
+  // a sliced pass or several passes, as in gate_up_wave_kernel.
+  const int light = whole_k_tokens(kPmax, I, 2);
+  const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
   int r_lo = 0, r_hi = 0;
   Segment sg;
   if constexpr (kSpeculate) {
@@ -588,27 +874,53 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
   }
   if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
   const bool all = n_act == m;
+  bool checked = !kBalance, weighted = false;
+  int w_hi = 0;
+  auto go_weighted = [&]() {
+    weighted = true;
+    weighted_work(n_act, tpe, active, counts, offsets, m, n_pairs, kPmax, I, g.cpt, 2, wp, scan);
+    block_range(wp[n_act], &r_lo, &w_hi);
+    if (r_lo >= w_hi) return false;
+    sg = weighted_segment(r_lo, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+    if (sg.lo >= sg.hi) return false;
+    begin_segment(sg);
+    return true;
+  };
   if (!kSpeculate || !all) {
     block_range(n_act * tpe, &r_lo, &r_hi);
-    if (r_lo >= r_hi) return;
-    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
-    begin_segment(sg);
-  } else if (r_lo >= r_hi) {
-    return;
+    if (r_lo < r_hi) {
+      sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, all);
+      begin_segment(sg);
+    }
+  }
+  if (r_lo >= r_hi) {
+    if (!kBalance) return;
+    checked = true;
+    if (!some_expert_is_heavy(pc, light, verdict) || !go_weighted()) return;
   }
 
   for (;;) {
     finish_segment(sg, n_pairs);
+    if (!checked && sg.cnt == 0) {  // no pass (hence no barrier) in this segment
+      checked = true;
+      if (some_expert_is_heavy(pc, light, verdict)) {
+        if (!go_weighted()) return;
+        continue;
+      }
+    }
     const int per_pass = sg.cnt > 0 ? pass_tokens(sg.cnt, kPmax) : 1;
     const int seg_n = sg.hi - sg.lo;
     const int ntw = seg_n > g.wave ? (seg_n - g.wave + kWv - 1) / kWv : 0;
     const int ngroups = (seg_n + kWv - 1) / kWv;
+    bool restart = false;
     for (int p0 = 0; p0 < sg.cnt; p0 += per_pass) {
       const PassShape ps = pass_shape(min(per_pass, sg.cnt - p0), I, g.cpt, 2);
       g.nbn = ps.nbn;
       g.cps = ps.cps;
       g.stride = ps.stride;
       g.lo_off = ps.nbn * 16 * ps.stride;
+      g.nsl = (g.cpt + ps.cps - 1) / ps.cps;
+      g.dbl = ps.dbl;
       const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
       if (p0 > 0) {
 #pragma unroll
@@ -621,24 +933,35 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
         const int p = perm[sg.base + p0 + (int)threadIdx.x];
         pv = (p >= 0 && p < n_pairs) ? p : -1;
       }
+      if (!checked) post_heavy_verdict(pc, light, verdict);
       __syncthreads();  // the previous pass's readers of hs and pid are done
+      if (!checked) {
+        checked = true;
+        if (read_heavy_verdict(verdict)) {
+          restart = true;
+          break;
+        }
+      }
       if ((int)threadIdx.x < kPmax) pid[threadIdx.x] = pv;
-      // K slice `sl` of the pass's h rows (hi, then lo), straight into LDS:
-      // wave w stages rows w, w + kWv, ... of both halves
-      auto stage = [&](int sl) {
+      // K slice `sl` of the pass's h rows (hi, then lo), straight into the
+      // LDS buffer at element `boff`: wave w stages rows w, w + kWv, ... of
+      // both halves
+      auto stage = [&](int sl, int boff) {
         const int col0 = sl * g.cps * kChunkCols;
         const int bytes = 2 * min(g.cps * kChunkCols, I - col0);
         for (int tok = g.wave; tok < g.nbn * 16; tok += kWv) {
           const uint32_t src =
               tok < ps.n ? ((uint32_t)(sg.base + p0 + tok) * (uint32_t)I + (uint32_t)col0) * 2u
                          : kOutOfRange;
-          stage_row(hhr, src, hs + tok * g.stride, bytes, g.lane);
-          stage_row(hlr, src, hs + g.lo_off + tok * g.stride, bytes, g.lane);
+          stage_row(hhr, src, hs + boff + tok * g.stride, bytes, g.lane);
+          stage_row(hlr, src, hs + boff + g.lo_off + tok * g.stride, bytes, g.lane);
         }
       };
       if (!ps.sliced) {
-        stage(0);
+        stage(0, 0);
         __builtin_amdgcn_s_waitcnt(kVmcntZero);
+      } else if (ps.dbl) {
+        stage(0, 0);  // landed by the wait at the loop's first step
       }
       __syncthreads();  // pid (and a whole-K pass's rows) visible to every wave
       if (kNbMax == 2 || ps.nbn <= 2)
@@ -646,8 +969,18 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
       else
         dn_run<kTiled, kDepth, kNbMax>(g, A, Q, ps.sliced, stage);
     }
-    if (sg.hi >= r_hi) break;
-    sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    if (restart) {
+      if (!go_weighted()) return;
+      continue;
+    }
+    if (weighted) {
+      if (sg.w_end >= w_hi) break;
+      sg = weighted_segment(sg.w_end, w_hi, n_act, wp, tpe, active, counts, offsets, m);
+      if (sg.lo >= sg.hi) break;
+    } else {
+      if (sg.hi >= r_hi) break;
+      sg = next_segment(sg.hi, r_hi, tpe, active, counts, offsets, m, all);
+    }
     begin_segment(sg);
   }
 }

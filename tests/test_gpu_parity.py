@@ -401,12 +401,15 @@ def test_weighted_walk_over_popular_experts(sw, hidden, n_experts, top_k, inter,
 
 
 @pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
-    (2048, 64, 4, 512, 64, (3,)),      # 64-token batch: gate/up passes of 64 tokens, x in 2 K slices
-    (1056, 48, 4, 384, 80, (2,)),      # H 1056 (5 chunks, the last one K step): slices of 3 + 2 chunks
-    (2048, 32, 4, 1024, 120, (0, 1)),  # 120 pairs: gate/up 4 slices of 2 chunks; down 2 passes of
-                                       # 60 tokens over 2 h slices (I 1024)
-    (2048, 48, 4, 768, 100, (5,)),     # gate/up 4 slices; down 2 passes of 50 tokens, h slices of
-                                       # 2 + 1 chunks
+    (2048, 64, 4, 512, 64, (3,)),      # 64-token batch: gate/up passes of 64 tokens, x in 4 K
+                                       # slices of 2 chunks through two LDS buffers
+    (1056, 48, 4, 384, 80, (2,)),      # H 1056 (5 chunks, the last one K step): one-chunk slices
+    (2048, 32, 4, 1024, 120, (0, 1)),  # 120 pairs: gate/up 8 one-chunk slices; down 2 passes of
+                                       # 60 tokens over 4 h slices (I 1024)
+    (2048, 48, 4, 768, 100, (5,)),     # gate/up 8 one-chunk slices; down 2 passes of 50 tokens,
+                                       # h slices of one chunk
+    (2048, 40, 4, 512, 90, (7,)),      # down: 90 tokens, one LDS buffer (two do not fit): h slices
+                                       # of one chunk staged at each slice's start
 ])
 @pytest.mark.parametrize("tiled", [False, True])
 def test_sliced_passes_stream_each_tile_once(sw, hidden, n_experts, top_k, inter, tokens, popular,
