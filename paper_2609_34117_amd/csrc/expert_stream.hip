@@ -238,7 +238,10 @@ constexpr int kCostSlice1 = 8;     // added per K slice of a single-buffered pas
 
 __device__ __forceinline__ int pass_cost(int n, int K, int cpt, int planes) {
   const PassShape ps = pass_shape(n, K, cpt, planes);
-  if (!ps.sliced) return kCostWholeK;
+  // a whole-K pass costs more with its column blocks too: per-block timings
+  // put each further block of 16 tokens at about 6% of a tile for gate/up
+  // and 12% for down (two h planes)
+  if (!ps.sliced) return kCostWholeK + (ps.nbn - 1) * planes / 2;
   if (ps.dbl) return kCostWholeK + kCostSliced + kCostSlicedNb * ps.nbn;
   return kCostWholeK + kCostSlice1 * ((cpt + ps.cps - 1) / ps.cps);
 }

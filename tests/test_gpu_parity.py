@@ -664,11 +664,13 @@ def _assert_same_route_dispatch(a, b):
     (2048, 128, 8, 64, False, False),     # 64 tokens: wave-form top-k, then dispatch
     (2048, 64, 16, 64, True, True),       # 1024 pairs, k = 16
     (2048, 256, 8, 256, False, True),     # 2048 pairs: the largest one-block dispatch
+    (2048, 512, 8, 256, False, False),    # 2048 pairs over 512 experts, wave top-k (8 per lane)
     (1024, 200, 16, 100, True, False),    # k = 16, ragged last top-k block
     (2048, 256, 8, 600, False, False),    # 4800 pairs: chunked multi-block dispatch
     (2048, 256, 8, 4096, True, False),    # prefill: wide logit tiles, 32 dispatch chunks
     (1536, 100, 6, 700, False, True),     # wide logit tiles with ragged token and expert tiles
     (512, 300, 8, 40, False, False),      # m > 256: separate kernels, wave top-k
+    (1024, 600, 4, 40, False, False),     # m > 512: 10 experts per lane of the wave top-k
     (256, 64, 17, 20, False, False),      # k > 16: separate kernels, wave top-k
     (520, 12, 4, 70, True, False),        # ragged H
 ])
