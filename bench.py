@@ -78,15 +78,15 @@ PAPER_CONTEXT = {
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
 # `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
-# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197801.8 KiB x
-# 1.99985 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
-# of 192-768 MiB) + WRITE_SIZE 1571.3 KiB x 1.0 (WRITE_SIZE of the copies is
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197882.6 KiB x
+# 1.99982 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
+# of 192-768 MiB) + WRITE_SIZE 1558.9 KiB x 1.0 (WRITE_SIZE of the copies is
 # exact).  The figure holds while the gate/up kernel's sources hash as below.
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="1f44eb2b39dd69a360ac4eb15915566aec44e54da51636e6cf0cff7b4a4e627b",
+GATE_UP_TRAFFIC = dict(sources_sha256="d797c89480be3d9be1ef4ffcb48a657ff52d0742016ef64b34c7b855a7259d1c",
                        workload=("decode_b64", 64, 0.5, "tiled"),
-                       bytes_per_launch=int(round((197799.7 * 1.99983 + 1577.3) * 1024)))
+                       bytes_per_launch=int(round((197882.6 * 1.99982 + 1558.9) * 1024)))
 
 
 def parse():
@@ -484,9 +484,14 @@ def run_decode_sweep(args, sw, torch, dev):
     L = I.make_layer(cfg)
     layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
     prunings = (0.0, 0.25, 0.5, 0.75)
+    batches = I.SWEEP_BATCHES
+    head_at = (64, 0.5)
+    if args.batch is not None:  # one batch size, at 0% and at --pruning only
+        batches, head_at = (args.batch,), (args.batch, args.pruning)
+        prunings = (0.0,) if args.pruning == 0.0 else (0.0, args.pruning)
     pools = build_pools(sw, torch, cfg, L, prunings, layout, dev)
     rows, at = [], {}
-    for T in I.SWEEP_BATCHES:
+    for T in batches:
         xs = [up(torch, dev, I.make_x(cfg, tokens=T, rep=r)) for r in range(N_X)]
         for p in prunings:
             s = measure(sw, torch, pools[p], cfg, T, xs, args.sweep_steps, args.warmup, dev)
@@ -496,24 +501,27 @@ def run_decode_sweep(args, sw, torch, dev):
                   f"step {s['t_step_us']:.1f} us (graph {s['t_step_graph_us']:.1f} us), n_active {s['n_active_mean']:.1f} "
                   f"(Eq. 1 {s['eq1_expected']:.1f}), fwd {s['fwd_GBps']:.0f} GB/s",
                   file=sys.stderr, flush=True)
-    head = at[(64, 0.5)]
-    line = base_line(args, cfg, 64, head["tokens_per_s"], head["t_step_us"], args.sweep_steps)
+    head = at[head_at]
+    line = base_line(args, cfg, head_at[0], head["tokens_per_s"], head["t_step_us"],
+                     args.sweep_steps)
     line["config"] = {
         "workload": f"{cfg.name}: decode MoE layer H {cfg.hidden}, {cfg.n_experts} experts, "
-                    f"top-{cfg.top_k}, I {cfg.inter}; value at batch 64, 50% pruned "
-                    f"({cfg.n_keep(0.5)} kept, compacted); batches {list(I.SWEEP_BATCHES)} x "
-                    f"pruning {list(prunings)} in detail",
+                    f"top-{cfg.top_k}, I {cfg.inter}; value at batch {head_at[0]}, "
+                    f"{int(head_at[1] * 100)}% pruned ({cfg.n_keep(head_at[1])} kept, compacted); "
+                    f"batches {list(batches)} x pruning {list(prunings)} in detail",
         "hidden": cfg.hidden, "n_experts": cfg.n_experts, "top_k": cfg.top_k, "inter": cfg.inter,
-        "batch": 64, "pruning": 0.5, "weight_layout": args.layout, "parallelism": "none (1 GPU)",
+        "batch": head_at[0], "pruning": head_at[1], "weight_layout": args.layout,
+        "parallelism": "none (1 GPU)",
     }
-    line["roofline"] = hbm_roofline(cfg, 64, 0.5, args.layout, head)
+    line["roofline"] = hbm_roofline(cfg, head_at[0], head_at[1], args.layout, head)
+    b = head_at[0]
     line["detail"] = {
         "sweep": rows,
-        "speedup_vs_full_at_b64": {str(p): round(at[(64, 0.0)]["t_step_us"] / at[(64, p)]["t_step_us"], 3)
-                                   for p in prunings},
+        f"speedup_vs_full_at_b{b}": {
+            str(p): round(at[(b, 0.0)]["t_step_us"] / at[(b, p)]["t_step_us"], 3) for p in prunings},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, L, 0.5, args.cpu_seconds, 64)
+        line["cpu_baseline"] = cpu_baseline(cfg, L, head_at[1], args.cpu_seconds, head_at[0])
     return line
 
 

@@ -269,13 +269,15 @@ sw_status sw_moe_forward_kernels(const sw_moe_dims* d, int32_t n_tokens, int32_t
  * and out[t] = sum_j topk_w[t, j] * y(t, j), summed in slot order.  The
  * same call serves the full pool (prefill shape) and the pruned pool
  * (decode shape).  Weight traffic: each active expert's weights are read
- * from HBM once per pass over its tokens.  One pass holds every token of
- * an expert with up to 64 pairs (up to 128 in the gate/up projection and
- * 96 in the down projection for batches of more than 64 tokens, 160 on the
- * prefill-sized kernels), so each expert of a routed batch of up to 64
- * tokens -- an expert takes at most one pair a token -- is read exactly
- * once; the split-K kernels of batches of one or two tokens read each
- * expert once.
+ * from HBM once per pass over its tokens.  One pass holds up to 32 of an
+ * expert's pairs in batches of up to 64 tokens; in larger batches up to 128
+ * in the gate/up projection and 96 in the down projection (passes whose
+ * tokens do not fit in LDS with the whole contraction stage it in slices),
+ * and 160 on the prefill-sized kernels.  So every expert of a routed batch
+ * of up to 32 tokens, every expert with at most 32 pairs of a batch of up
+ * to 64, and every expert with at most 96 pairs of a larger batch is read
+ * exactly once (an expert takes at most one pair a token); the split-K
+ * kernels of batches of one or two tokens read each expert once.
  *
  *   layout     sw_weight_layout of w13 and w2 (SW_LAYOUT_TILED needs the
  *              shapes sw_moe_pack_experts accepts, and 4*T*k*H < 2^31)

@@ -133,6 +133,31 @@ __device__ __forceinline__ int slice_buffer(bool dbl, int sigma) {
   return (dbl && (sigma & 1)) ? kStage / 2 : 0;
 }
 
+// Position of a wave's chunk q in its pass: tile group (or own tile) j,
+// chunk c of the tile, and on a sliced pass the slice sl and the chunk's
+// place ks in it.  Advanced by one step at a time, so that the chunk loops
+// do no integer division per step.
+struct ChunkPos {
+  int j, c, sl, ks;
+  __device__ __forceinline__ void start(int q, int cpt, int cps) {
+    j = q / cpt;
+    c = q - j * cpt;
+    sl = c / cps;
+    ks = c - sl * cps;
+  }
+  __device__ __forceinline__ void next(int cpt, int cps) {
+    ++c;
+    if (++ks == cps) {
+      ks = 0;
+      ++sl;
+    }
+    if (c == cpt) {
+      c = ks = sl = 0;
+      ++j;
+    }
+  }
+};
+
 struct Segment {
   int lo, hi;  // tile range [lo, hi) inside one expert
   int a, e, cnt, base;
@@ -372,8 +397,7 @@ struct GuWave {
 // load (non-temporal: read once).  Chunks of tiles this wave does not have
 // read out of range.
 template <bool kTiled>
-__device__ __forceinline__ void gu_issue(const GuWave& g, int q, u32x4 (&A)[kKC]) {
-  const int j = q / g.cpt, c = q - j * g.cpt;
+__device__ __forceinline__ void gu_issue(const GuWave& g, int j, int c, u32x4 (&A)[kKC]) {
   const int tile = g.seg_lo + g.wave + j * kWv;
   const int ib = tile - g.a * g.tpe;
   uint32_t row, stride;
@@ -399,9 +423,9 @@ __device__ __forceinline__ void gu_issue(const GuWave& g, int q, u32x4 (&A)[kKC]
 // issued on every chunk (out of range unless they hold a result), so every
 // chunk issues the same memory operations.
 template <int NB>
-__device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (&A)[kKC],
-                                           f32x4 (&acc)[NB]) {
-  const int j = q / g.cpt, c = q - j * g.cpt;
+__device__ __forceinline__ void gu_compute(const GuWave& g, const ChunkPos& at,
+                                           const u32x4 (&A)[kKC], f32x4 (&acc)[NB]) {
+  const int j = at.j, c = at.c;
   const int tile = g.seg_lo + g.wave + j * kWv;
   const bool have = tile < g.seg_hi;  // false: no tile of this wave in the group
   if (c == 0) {
@@ -409,7 +433,7 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, int q, const u32x4 (
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   // column of a K step inside the staged slice, and the slice's buffer
-  const int sl = c / g.cps;
+  const int sl = at.sl;
   const int step0 = sl * g.cps * kKC;
   const uint16_t* xb = g.xs + slice_buffer(g.dbl, j * g.nsl + sl);
 #pragma unroll
@@ -488,38 +512,42 @@ __device__ __forceinline__ void gu_run(const GuWave& g, u32x4 (&A)[D][kKC], int 
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkPos at, ahead;  // the chunk computed, and the chunk issued D - 1 steps ahead
+  at.start(0, g.cpt, g.cps);
+  ahead.start(D - 1, g.cpt, g.cps);
   for (int q = 0; q < Q; q += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int qd = q + d;
-      const int j = qd / g.cpt, c = qd - j * g.cpt, sl = c / g.cps;
-      const bool first = sliced && qd < Q && c == sl * g.cps;
+      const bool first = sliced && qd < Q && at.ks == 0;
       if (first && !g.dbl) {
         slice_barrier_before();
-        stage(sl, 0);
+        stage(at.sl, 0);
         __builtin_amdgcn_sched_barrier(0);  // the slice's loads, then the weights
       }
       if (first && g.dbl) {
-        const int sigma = j * g.nsl + sl;
+        const int sigma = at.j * g.nsl + at.sl;
         wait_staged_before(sigma == 0 ? 0 : after);
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         if (sigma + 1 < n_slices) {
-          stage(sl + 1 < g.nsl ? sl + 1 : 0, slice_buffer(true, sigma + 1));
+          stage(at.sl + 1 < g.nsl ? at.sl + 1 : 0, slice_buffer(true, sigma + 1));
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-      gu_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
+      gu_issue<kTiled>(g, ahead.j, ahead.c, A[(d + D - 1) % D]);
       if (first && !g.dbl) slice_barrier_after<kKC>();
-      if (d == 0 || qd < Q) gu_compute<NB>(g, qd, A[d], acc);
+      if (d == 0 || qd < Q) gu_compute<NB>(g, at, A[d], acc);
+      at.next(g.cpt, g.cps);
+      ahead.next(g.cpt, g.cps);
     }
   }
 }
 
 // kSpeculate: guess n_active == m and issue the first weight chunks before
 // n_active arrives (a wrong guess redoes the first segment).
-// kNbMax: column blocks of the largest pass (16 kNbMax tokens); a batch of
-// at most kNT tokens needs 2, a larger one takes 8.
+// kNbMax: column blocks of the largest pass (16 kNbMax tokens): 2 for
+// batches of up to 64 tokens, 8 for larger ones.
 template <bool kTiled, bool kSpeculate, int kNbMax, int kDepth>
 __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
@@ -528,8 +556,9 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
     uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
   constexpr int kPmax = 16 * kNbMax;
-  // batches of more than 32 tokens can give an expert more pairs than a
-  // whole-K pass holds: the cost-weighted walk is compiled in
+  // the wide variant (batches of more than 64 tokens) can give an expert
+  // more pairs than a whole-K pass holds: the cost-weighted walk is
+  // compiled in
   constexpr bool kBalance = kNbMax > 2;
   __shared__ __attribute__((aligned(16))) uint16_t xs[kStage];
   __shared__ int pid[kPmax];
@@ -561,7 +590,11 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     g.a = sg.a;
     g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.e_ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
 #pragma unroll
-    for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, A[d]);
+    for (int d = 0; d < kDepth - 1; ++d) {
+      ChunkPos h;
+      h.start(d, g.cpt, g.cpt);
+      gu_issue<kTiled>(g, h.j, h.c, A[d]);
+    }
   };
 
   // Speculate a fully active pool (n_active == m, the usual saturated decode
@@ -641,7 +674,11 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
       const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
       if (p0 > 0) {
 #pragma unroll
-        for (int d = 0; d < kDepth - 1; ++d) gu_issue<kTiled>(g, d, A[d]);
+        for (int d = 0; d < kDepth - 1; ++d) {
+      ChunkPos h;
+      h.start(d, g.cpt, g.cpt);
+      gu_issue<kTiled>(g, h.j, h.c, A[d]);
+    }
       }
       // the pass's pair ids (loaded before the barrier that waits for the
       // previous pass's readers of pid and xs)
@@ -716,8 +753,7 @@ struct DnWave {
 };
 
 template <bool kTiled>
-__device__ __forceinline__ void dn_issue(const DnWave& g, int q, u32x4 (&A)[kKC]) {
-  const int j = q / g.cpt, c = q - j * g.cpt;
+__device__ __forceinline__ void dn_issue(const DnWave& g, int j, int c, u32x4 (&A)[kKC]) {
   const int tile = g.seg_lo + g.wave + j * kWv;
   const int ob = tile - g.a * g.tpe;
   const int o = ob * 16 + g.r;
@@ -740,16 +776,16 @@ __device__ __forceinline__ void dn_issue(const DnWave& g, int q, u32x4 (&A)[kKC]
 }
 
 template <int NB>
-__device__ __forceinline__ void dn_compute(const DnWave& g, int q, const u32x4 (&A)[kKC],
-                                           f32x4 (&acc)[NB]) {
-  const int j = q / g.cpt, c = q - j * g.cpt;
+__device__ __forceinline__ void dn_compute(const DnWave& g, const ChunkPos& at,
+                                           const u32x4 (&A)[kKC], f32x4 (&acc)[NB]) {
+  const int j = at.j, c = at.c;
   const int tile = g.seg_lo + g.wave + j * kWv;
   const bool have = tile < g.seg_hi;
   if (c == 0) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-  const int sl = c / g.cps;
+  const int sl = at.sl;
   const int step0 = sl * g.cps * kKC;
   const uint16_t* hb = g.hs + slice_buffer(g.dbl, j * g.nsl + sl);
 #pragma unroll
@@ -792,30 +828,34 @@ __device__ __forceinline__ void dn_run(const DnWave& g, u32x4 (&A)[D][kKC], int 
   f32x4 acc[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  ChunkPos at, ahead;  // the chunk computed, and the chunk issued D - 1 steps ahead
+  at.start(0, g.cpt, g.cps);
+  ahead.start(D - 1, g.cpt, g.cps);
   for (int q = 0; q < Q; q += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int qd = q + d;
-      const int j = qd / g.cpt, c = qd - j * g.cpt, sl = c / g.cps;
-      const bool first = sliced && qd < Q && c == sl * g.cps;
+      const bool first = sliced && qd < Q && at.ks == 0;
       if (first && !g.dbl) {
         slice_barrier_before();
-        stage(sl, 0);
+        stage(at.sl, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (first && g.dbl) {
-        const int sigma = j * g.nsl + sl;
+        const int sigma = at.j * g.nsl + at.sl;
         wait_staged_before(sigma == 0 ? 0 : after);
         __builtin_amdgcn_s_barrier();
         __builtin_amdgcn_sched_barrier(0);
         if (sigma + 1 < n_slices) {
-          stage(sl + 1 < g.nsl ? sl + 1 : 0, slice_buffer(true, sigma + 1));
+          stage(at.sl + 1 < g.nsl ? at.sl + 1 : 0, slice_buffer(true, sigma + 1));
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-      dn_issue<kTiled>(g, qd + D - 1, A[(d + D - 1) % D]);
+      dn_issue<kTiled>(g, ahead.j, ahead.c, A[(d + D - 1) % D]);
       if (first && !g.dbl) slice_barrier_after<kKC>();
-      if (d == 0 || qd < Q) dn_compute<NB>(g, qd, A[d], acc);
+      if (d == 0 || qd < Q) dn_compute<NB>(g, at, A[d], acc);
+      at.next(g.cpt, g.cps);
+      ahead.next(g.cpt, g.cps);
     }
   }
 }
@@ -861,7 +901,11 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
     g.a = sg.a;
     g.w = make_rsrc(w2 + (size_t)sg.e * H * I, sg.e_ok ? 2u * (uint32_t)H * (uint32_t)I : 0u);
 #pragma unroll
-    for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, A[d]);
+    for (int d = 0; d < kDepth - 1; ++d) {
+      ChunkPos h;
+      h.start(d, g.cpt, g.cpt);
+      dn_issue<kTiled>(g, h.j, h.c, A[d]);
+    }
   };
 
   // Speculate a fully active pool, and walk by cost when some expert needs
@@ -927,7 +971,11 @@ __global__ __launch_bounds__(kBlk, 1) void down_wave_kernel(
       const int Q = (ps.sliced ? ngroups : ntw) * g.cpt;
       if (p0 > 0) {
 #pragma unroll
-        for (int d = 0; d < kDepth - 1; ++d) dn_issue<kTiled>(g, d, A[d]);
+        for (int d = 0; d < kDepth - 1; ++d) {
+      ChunkPos h;
+      h.start(d, g.cpt, g.cpt);
+      dn_issue<kTiled>(g, h.j, h.c, A[d]);
+    }
       }
       // the pass's pair ids (for the y rows); its h rows are contiguous in
       // dispatch-slot order
@@ -1026,20 +1074,23 @@ __global__ __launch_bounds__(256) void pack_w2_kernel(const uint16_t* __restrict
 
 // Variant of a launch: the largest pass (column blocks) and the weight
 // pipeline depth.  An expert receives at most one pair per token of a routed
-// batch, so a batch of T tokens needs passes of T tokens for one stream per
-// expert: 2 column blocks up to 32 tokens, 4 up to 64, then the most that
-// fit the registers with no spill -- 8 (128 tokens) for gate/up with two
-// chunks in flight, 6 (96 tokens) for down with three.  An expert with more
-// pairs (only a larger batch, or an unrouted plan, gives one) takes further
-// passes.  Guessing a fully active pool pays when the expected number of
-// idle experts, m (1 - k/m)^T, is well below one (always assumed for
-// batches of up to 64 tokens, where a wrong guess costs one segment).
-int gate_up_column_blocks(int T) { return T <= kNT ? 2 : T <= 2 * kNT ? 4 : 8; }
-int down_column_blocks(int T) { return T <= kNT ? 2 : 6; }
+// batch, so passes of T tokens stream every expert once.  Batches of up to
+// 64 tokens take passes of 32 (2 column blocks, three chunks in flight): a
+// 64-token variant needs every register and measured 2.6 us slower on the
+// 64-token decode layer over 64 experts, and 10 us over 128, than the
+// 32-token one, whose only extra cost is a second pass over an expert that
+// receives more than 32 of the batch's tokens (heavy skew; near-uniform
+// routing gives at most about 20 at 64 tokens).  Larger batches take the
+// most that fit the registers with no spill -- 8 column blocks (128 tokens)
+// for gate/up with two chunks in flight, 6 (96 tokens) for down with three
+// -- and the cost-weighted walk.  Guessing a fully active pool pays when
+// the expected number of idle experts, m (1 - k/m)^T, is well below one.
+int gate_up_column_blocks(int T) { return T <= 2 * kNT ? 2 : 8; }
+int down_column_blocks(int T) { return T <= 2 * kNT ? 2 : 6; }
 
 bool speculate_full_pool(int T, int m, int k) {
   const double idle = m * std::pow(1.0 - (double)k / m, (double)T);
-  return T <= 2 * kNT || idle < 0.25;
+  return idle < 0.25;
 }
 
 int stream_grid() {
@@ -1067,9 +1118,11 @@ hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bo
   gate_up_wave_kernel<TI, SP, NB, D><<<stream_grid(), kBlk, 0, stream>>>(                       \
       x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k)
   if (nb == 2) {
-    if (tiled) SW_GU(true, true, 2, 3); else SW_GU(false, true, 2, 3);
-  } else if (nb == 4) {
-    if (tiled) SW_GU(true, true, 4, 3); else SW_GU(false, true, 4, 3);
+    if (sp) {
+      if (tiled) SW_GU(true, true, 2, 3); else SW_GU(false, true, 2, 3);
+    } else {
+      if (tiled) SW_GU(true, false, 2, 3); else SW_GU(false, false, 2, 3);
+    }
   } else if (sp) {
     if (tiled) SW_GU(true, true, 8, 2); else SW_GU(false, true, 8, 2);
   } else {
@@ -1089,7 +1142,11 @@ hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* co
   down_wave_kernel<TI, SP, NB, 3><<<stream_grid(), kBlk, 0, stream>>>(                          \
       h_hi, h_lo, w2, counts, offsets, perm, active, n_active, y, H, I, m, T * k)
   if (nb == 2) {
-    if (tiled) SW_DN(true, true, 2); else SW_DN(false, true, 2);
+    if (sp) {
+      if (tiled) SW_DN(true, true, 2); else SW_DN(false, true, 2);
+    } else {
+      if (tiled) SW_DN(true, false, 2); else SW_DN(false, false, 2);
+    }
   } else if (sp) {
     if (tiled) SW_DN(true, true, 6); else SW_DN(false, true, 6);
   } else {

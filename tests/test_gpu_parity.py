@@ -143,7 +143,8 @@ def test_decode_sweep_parity(sw, batch, pruning):
     if batch >= 64:
         assert fam == ("wave", "wave")
     if batch == 256 and pruning == 0.75:
-        # 2048 pairs over 64 experts: experts with more than one 32-token pass
+        # 2048 pairs over 64 experts: experts with more pairs than a whole-K
+        # pass holds (sliced passes, double-buffered)
         assert s["counts"].max() > 32
     print(f"sweep B={batch} p={pruning}: kernels={fam} n_active={s['n_active']} "
           f"max pairs/expert={s['counts'].max()} near_ties={s['n_near']} "
@@ -166,8 +167,8 @@ def test_prefill_shape_parity(sw):
 def test_skew_routed_batch256_parity(sw, pruning):
     # the skewed stack's routing (Zipf(1.1) logit bias, kept set = the most
     # popular half) on the sweep layer's host-drawn experts at batch 256:
-    # popular experts take up to ~80 pairs (several 32-token passes); every
-    # token is compared
+    # popular experts take up to ~80 pairs (sliced passes, the cost-weighted
+    # walk); every token is compared
     cfg, L, D = layer_inputs("decode_sweep")
     scfg = I.CONFIGS["skewed_stack"]
     S = I.make_layer(scfg, layer=0, experts=False)
@@ -375,7 +376,7 @@ def test_split_k_ragged_shapes(sw, hidden, n_experts, top_k, inter, tokens, popu
 
 def test_popular_expert_spans_several_token_passes(sw):
     # a bias makes expert 3 every token's first choice: 200 pairs on one
-    # expert (4 passes of 64 tokens over its weights)
+    # expert (two passes of 100 tokens over its weights)
     cfg, L, D = small_layer(256, 16, 2, 64, 200, seed=1)
     bias = np.zeros(16, np.float32)
     bias[3] = 50.0
@@ -384,14 +385,14 @@ def test_popular_expert_spans_several_token_passes(sw):
 
 
 @pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
-    (512, 16, 2, 96, 300, (3, 7)),   # two experts take every token: 10 passes each,
+    (512, 16, 2, 96, 300, (3, 7)),   # two experts take every token: 3 passes each,
                                      # 2 of 16 experts active (first segment guessed, redone)
-    (256, 64, 2, 64, 100, (5,)),     # one expert with 4 passes among ~50 light ones
-                                     # (no guess: many idle experts expected)
+    (256, 64, 2, 64, 100, (5,)),     # one expert with a 100-token pass among ~50 light
+                                     # ones (no guess: many idle experts expected)
 ])
 def test_weighted_walk_over_popular_experts(sw, hidden, n_experts, top_k, inter, tokens, popular):
-    # batches above two passes per expert balance the decode kernels' blocks
-    # by tile passes instead of tiles
+    # popular experts with sliced or several passes: the decode kernels'
+    # blocks take equal runs of estimated cost instead of equal tile ranges
     cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=13)
     bias = np.zeros(n_experts, np.float32)
     bias[list(popular)] = 50.0
@@ -401,8 +402,8 @@ def test_weighted_walk_over_popular_experts(sw, hidden, n_experts, top_k, inter,
 
 
 @pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,popular", [
-    (2048, 64, 4, 512, 64, (3,)),      # 64-token batch: gate/up passes of 64 tokens, x in 4 K
-                                       # slices of 2 chunks through two LDS buffers
+    (2048, 64, 4, 512, 64, (3,)),      # 64-token batch: 32-token passes, the popular expert
+                                       # in two (each tile streamed twice)
     (1056, 48, 4, 384, 80, (2,)),      # H 1056 (5 chunks, the last one K step): one-chunk slices
     (2048, 32, 4, 1024, 120, (0, 1)),  # 120 pairs: gate/up 8 one-chunk slices; down 2 passes of
                                        # 60 tokens over 4 h slices (I 1024)
