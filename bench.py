@@ -110,16 +110,17 @@ def parse():
 class Pool:
     """One expert pool (full or compacted) resident on the device, N_COPIES times."""
 
-    def __init__(self, w13, w2, wr, layout, bias=None, shared=None, n_shared=0):
+    def __init__(self, w13, w2, wr, layout, bias=None, shared=None, n_shared=0, n_groups=1):
         self.w13 = [w13] + [w13.clone() for _ in range(N_COPIES - 1)]
         self.w2 = [w2] + [w2.clone() for _ in range(N_COPIES - 1)]
         self.wr = wr
         self.bias = bias
         self.layout = layout
-        # n_shared > 0: the shared expert folded into the plan -- its parts
-        # follow the routed experts in w13 / w2 and its gate row follows the
-        # router rows in wr
+        # n_shared > 0: the shared expert folded into the plan -- n_groups
+        # copies of its parts follow the routed experts in w13 / w2 and its
+        # gate row follows the router rows in wr
         self.n_shared = n_shared
+        self.n_groups = n_groups
         self.m = wr.shape[0] - (1 if n_shared else 0)  # routed experts
         self.shared = shared  # (w13_s, w2_s, gate_w) run by the separate call, or None
         self.keep_mask = None  # router mask over this pool (colocated decode), or None
@@ -132,14 +133,15 @@ class Runner:
         self.sw, self.torch, self.pool, self.cfg, self.T = sw, torch, pool, cfg, T
         k, H, Iw = cfg.top_k, cfg.hidden, cfg.inter
         S = pool.n_shared
-        self.kout, self.m_plan = k + S, pool.m + S  # slots a token, experts of the plan
+        # slots a token, experts of the plan
+        self.kout, self.m_plan = k + S, pool.m + pool.n_groups * S
         self.ids = torch.empty((T, self.kout), dtype=torch.int32, device=dev)
         self.w = torch.empty((T, self.kout), dtype=torch.float32, device=dev)
         self.gap = torch.empty(T, dtype=torch.float32, device=dev)
         self.plan = sw.alloc_plan(T, self.m_plan, self.kout, dev)
         self.out = torch.empty((T, H), dtype=torch.float32, device=dev)
         d = sw.dims(H, Iw, pool.m, k)
-        rbytes = (sw.sw_moe_route_shared_workspace_bytes(d, T, S) if S else
+        rbytes = (sw.sw_moe_route_shared_workspace_bytes(d, T, S, pool.n_groups) if S else
                   sw.sw_moe_route_workspace_bytes(d, T))
         self.rws = sw.workspace(rbytes, dev)
         self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(
@@ -152,7 +154,8 @@ class Runner:
     def route(self, x, plan):
         sw, p = self.sw, self.pool
         if p.n_shared:
-            sw.sw_moe_route_dispatch_shared(x, p.wr, self.cfg.top_k, p.n_shared, bias=p.bias,
+            sw.sw_moe_route_dispatch_shared(x, p.wr, self.cfg.top_k, p.n_shared,
+                                            n_groups=p.n_groups, bias=p.bias,
                                             keep_mask=p.keep_mask,
                                             out=(self.ids, self.w, self.gap), plan=plan,
                                             ws=self.rws)
@@ -397,7 +400,7 @@ def measure(sw, torch, pool, cfg, T, xs, steps, warmup, dev):
                 t_step_graph_us=kern["graph_step"] * 1e6, tokens_per_s_graph=T / kern["graph_step"],
                 t_gate_up_us=t_gu * 1e6, t_down_us=t_dn * 1e6, t_combine_us=t_cb * 1e6,
                 n_active_mean=n_mean,
-                eq1_expected=float(m * (1 - (1 - k / m) ** T)) + pool.n_shared,
+                eq1_expected=float(m * (1 - (1 - k / m) ** T)) + pool.n_shared * pool.n_groups,
                 unique_MiB_per_step=float(U.mean() / 2 ** 20),
                 gate_up_launch_us=kern["gate_up"] * 1e6, down_launch_us=kern["down"] * 1e6,
                 gate_up_GBps=n_mean * 2 * H * Iw * 2 / kern["gate_up"] / 1e9,
@@ -569,6 +572,10 @@ def run_decode_shared(args, sw, torch, dev):
     T, H, Iw = 64, cfg.hidden, cfg.inter
     S = 2
     Is = S * Iw  # the distilled decoder's shared expert: twice the original width
+    # token groups of the folded parts: at most 32 tokens a copy, so that each
+    # part is a one-pass expert of the decode kernels (every further copy
+    # streams the shared weights once more)
+    groups = (T + 31) // 32
     L = I.make_layer(cfg)
     layout = sw.TILED if args.layout == "tiled" else sw.ROW_MAJOR
     pools = build_pools(sw, torch, cfg, L, (0.5, 0.0), layout, dev)
@@ -593,10 +600,12 @@ def run_decode_shared(args, sw, torch, dev):
     for p in (0.5, 0.0):
         base = pools[p]
         res[(p, "none")] = measure(sw, torch, base, cfg, T, xs, args.steps, args.warmup, dev)
-        folded = Pool(torch.cat([base.w13[0], p13_d]), torch.cat([base.w2[0], p2_d]),
-                      torch.cat([base.wr, gate_d[None]]), layout, n_shared=S)
-        res[(p, "folded")] = measure(sw, torch, folded, cfg, T, xs, args.steps, args.warmup, dev)
-        del folded
+        for how, G in (("folded", groups), ("folded, one copy", 1)):
+            folded = Pool(torch.cat([base.w13[0]] + [p13_d] * G),
+                          torch.cat([base.w2[0]] + [p2_d] * G),
+                          torch.cat([base.wr, gate_d[None]]), layout, n_shared=S, n_groups=G)
+            res[(p, how)] = measure(sw, torch, folded, cfg, T, xs, args.steps, args.warmup, dev)
+            del folded
         separate = copy.copy(base)
         separate.shared = (w13s_d, w2s_d, gate_d)
         res[(p, "separate")] = measure(sw, torch, separate, cfg, T, xs, args.steps, args.warmup, dev)
@@ -605,20 +614,22 @@ def run_decode_shared(args, sw, torch, dev):
     line["config"] = {
         "workload": f"decode_shared: decode MoE layer H {H}, {cfg.n_experts} experts, top-{cfg.top_k}, "
                     f"I {Iw}, batch {T}, 50% pruned ({cfg.n_keep(0.5)} kept, compacted) plus a shared "
-                    f"expert of width {Is} behind a sigmoid gate, folded into the plan as {S} parts",
+                    f"expert of width {Is} behind a sigmoid gate, folded into the plan as {S} parts "
+                    f"in {groups} token groups",
         "hidden": H, "n_experts": cfg.n_experts, "n_kept": cfg.n_keep(0.5), "top_k": cfg.top_k,
-        "inter": Iw, "shared_inter": Is, "shared_parts": S, "batch": T, "pruning": 0.5,
+        "inter": Iw, "shared_inter": Is, "shared_parts": S, "shared_groups": groups, "batch": T,
+        "pruning": 0.5,
         "weight_layout": args.layout, "parallelism": "none (1 GPU)",
     }
     line["roofline"] = hbm_roofline(cfg, T, 0.5, args.layout, head)
     line["detail"] = {f"{int(p * 100)}% {how}": rounded(v) for (p, how), v in res.items()}
     line["detail"]["shared_expert_us"] = {
         f"{int(p * 100)}% {how}": round(res[(p, how)]["t_step_us"] - res[(p, "none")]["t_step_us"], 3)
-        for p in (0.5, 0.0) for how in ("folded", "separate")}
+        for p in (0.5, 0.0) for how in ("folded", "folded, one copy", "separate")}
     line["detail"]["shared_expert_us_graph"] = {
         f"{int(p * 100)}% {how}": round(res[(p, how)]["t_step_graph_us"]
                                        - res[(p, "none")]["t_step_graph_us"], 3)
-        for p in (0.5, 0.0) for how in ("folded", "separate")}
+        for p in (0.5, 0.0) for how in ("folded", "folded, one copy", "separate")}
     line["detail"]["shared_expert_MiB"] = 3 * H * Is * 2 / 2 ** 20
     line["detail"]["speedup_pruned_vs_full_with_shared"] = round(
         res[(0.0, "folded")]["t_step_us"] / res[(0.5, "folded")]["t_step_us"], 3)

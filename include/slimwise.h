@@ -87,7 +87,7 @@ typedef enum {
 } sw_kernel_family;
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 8
+#define SW_ABI_VERSION 9
 int32_t sw_abi_version(void);
 
 /*
@@ -185,7 +185,7 @@ sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t
 /* Workspace bytes sw_moe_route_dispatch_shared needs (0 on invalid
  * arguments). */
 size_t sw_moe_route_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens,
-                                           int32_t n_shared);
+                                           int32_t n_shared, int32_t n_groups);
 
 /*
  * Route + dispatch with the always-on shared expert folded into the plan
@@ -193,37 +193,49 @@ size_t sw_moe_route_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_token
  * the frozen SE1 plus the added SE2, behind one sigmoid gate).  The shared
  * expert's SwiGLU is separable over its intermediate units, so a shared
  * expert of width n_shared * I is n_shared experts of the routed width I
- * whose down projections add.  This call gives every token, after its k
- * routed slots, n_shared more slots naming those parts, each with the gate
- * sigmoid(wr[m] . x_t):
- *   topk_ids[t, k + s] = m + s,   topk_w[t, k + s] = sigmoid(wr[m] . x_t),
- * and builds the plan over the m + n_shared experts.  sw_moe_forward with
- * dims {H, I, m + n_shared, k + n_shared} on a pool that holds the m routed
- * experts followed by the n_shared parts (part s: the gate and up rows of
- * the shared expert's intermediate units s*I .. (s+1)*I - 1, and the
- * matching I columns of its down projection) then adds
+ * whose down projections add.  The pool holds n_groups copies of those
+ * parts after the m routed experts, and token t of the batch uses copy
+ * g(t) = t * n_groups / T (contiguous runs of about T / n_groups tokens).
+ * This call gives every token, after its k routed slots, n_shared more
+ * slots naming its copy's parts, each with the gate sigmoid(wr[m] . x_t):
+ *   topk_ids[t, k + s] = m + g(t) * n_shared + s,
+ *   topk_w[t, k + s]   = sigmoid(wr[m] . x_t),
+ * and builds the plan over the m + n_groups * n_shared experts.
+ * sw_moe_forward with dims {H, I, m + n_groups * n_shared, k + n_shared} on
+ * that pool (part s of every copy: the gate and up rows of the shared
+ * expert's intermediate units s*I .. (s+1)*I - 1, and the matching I
+ * columns of its down projection) then adds
  *   sigmoid(wr[m] . x_t) * W2s (silu(W1s x_t) * W3s x_t)
- * to each token's output on the routed experts' launches.
+ * to each token's output on the routed experts' launches, bit for bit the
+ * same for every n_groups.  n_groups trades weight bytes for pass shape:
+ * each copy's parts receive one pair per token of their group, so with
+ * groups of at most 32 tokens every part is a one-pass expert, where one
+ * copy of a batch of more than 32 tokens gives parts with every token
+ * (two passes, or sliced ones); each further copy streams the parts' weights
+ * once more.
  *
  *   d          the routed dims: n_experts = m, top_k = k
  *   wr         fp32 [m + 1, H]: the router rows, then the shared gate row
  *   bias, keep_mask  as for sw_moe_route (over the m routed experts)
- *   n_shared   parts of the shared expert, >= 1; m + n_shared <= 1024 and
- *              k + n_shared <= 32 (else SW_ERR_UNSUPPORTED)
+ *   n_shared   parts of the shared expert, >= 1; k + n_shared <= 32
+ *   n_groups   copies of the parts in the pool, >= 1; m + n_groups * n_shared
+ *              <= 1024 (else SW_ERR_UNSUPPORTED)
  *   topk_ids, topk_w  out [T, k + n_shared]
  *   gap        nullable out fp32 [T], of the routed selection
- *   counts, active  out int32 [m + n_shared]; offsets [m + n_shared + 1];
- *              perm [T (k + n_shared)]; n_active [1]
- *   workspace  >= sw_moe_route_shared_workspace_bytes(d, T, n_shared) bytes
+ *   counts, active  out int32 [m + n_groups * n_shared]; offsets
+ *              [m + n_groups * n_shared + 1]; perm [T (k + n_shared)];
+ *              n_active [1]
+ *   workspace  >= sw_moe_route_shared_workspace_bytes(d, T, n_shared, n_groups)
+ *              bytes
  * In-band errors as sw_moe_route_dispatch.
  */
 sw_status sw_moe_route_dispatch_shared(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
                                        const float* wr, const float* bias,
                                        const uint8_t* keep_mask, int32_t n_shared,
-                                       int32_t* topk_ids, float* topk_w, float* gap,
-                                       int32_t* counts, int32_t* offsets, int32_t* perm,
-                                       int32_t* active, int32_t* n_active, void* workspace,
-                                       size_t workspace_bytes, void* stream);
+                                       int32_t n_groups, int32_t* topk_ids, float* topk_w,
+                                       float* gap, int32_t* counts, int32_t* offsets,
+                                       int32_t* perm, int32_t* active, int32_t* n_active,
+                                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Re-lay an expert pool out for streaming (offline, once per pool; a device

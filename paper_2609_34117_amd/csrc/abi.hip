@@ -122,12 +122,13 @@ sw_status check_forward_operands(const sw_moe_dims* d, const uint16_t* x, int32_
   return SW_OK;
 }
 
-// Routed dims plus n_shared parts of a shared expert: the extended pool
-// and slots must stay within the kernels' limits, and so must the router
-// with its gate row.
-sw_status check_shared(const sw_moe_dims* d, int32_t n_shared) {
-  if (n_shared < 1) return SW_ERR_SHAPE;
-  if (d->n_experts + n_shared > kMaxExperts || d->top_k + n_shared > kMaxTopK)
+// Routed dims plus n_groups copies of n_shared parts of a shared expert: the
+// extended pool and slots must stay within the kernels' limits, and so must
+// the router with its gate row.
+sw_status check_shared(const sw_moe_dims* d, int32_t n_shared, int32_t n_groups) {
+  if (n_shared < 1 || n_groups < 1) return SW_ERR_SHAPE;
+  if ((int64_t)d->n_experts + (int64_t)n_groups * n_shared > kMaxExperts ||
+      d->top_k + n_shared > kMaxTopK)
     return SW_ERR_UNSUPPORTED;
   if (4 * ((int64_t)d->n_experts + 1) * d->hidden >= kMaxBufferBytes) return SW_ERR_UNSUPPORTED;
   return SW_OK;
@@ -274,23 +275,25 @@ sw_status sw_moe_route_dispatch(const sw_moe_dims* d, const uint16_t* x, int32_t
 }
 
 size_t sw_moe_route_shared_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens,
-                                           int32_t n_shared) {
+                                           int32_t n_shared, int32_t n_groups) {
   if (check_dims(d) != SW_OK || check_tokens(d, n_tokens) != SW_OK ||
-      check_shared(d, n_shared) != SW_OK)
+      check_shared(d, n_shared, n_groups) != SW_OK)
     return 0;
-  return sw::route_shared_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k, n_shared);
+  return sw::route_shared_workspace_bytes(n_tokens, d->hidden, d->n_experts, d->top_k, n_shared,
+                                          n_groups);
 }
 
 sw_status sw_moe_route_dispatch_shared(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
                                        const float* wr, const float* bias,
                                        const uint8_t* keep_mask, int32_t n_shared,
-                                       int32_t* topk_ids, float* topk_w, float* gap,
-                                       int32_t* counts, int32_t* offsets, int32_t* perm,
-                                       int32_t* active, int32_t* n_active, void* workspace,
-                                       size_t workspace_bytes, void* stream) {
+                                       int32_t n_groups, int32_t* topk_ids, float* topk_w,
+                                       float* gap, int32_t* counts, int32_t* offsets,
+                                       int32_t* perm, int32_t* active, int32_t* n_active,
+                                       void* workspace, size_t workspace_bytes, void* stream) {
   SW_TRY(check_dims(d));
-  SW_TRY(check_shared(d, n_shared));
-  const sw_moe_dims ext{d->hidden, d->inter, d->n_experts + n_shared, d->top_k + n_shared};
+  SW_TRY(check_shared(d, n_shared, n_groups));
+  const sw_moe_dims ext{d->hidden, d->inter, d->n_experts + n_groups * n_shared,
+                        d->top_k + n_shared};
   SW_TRY(check_tokens(&ext, n_tokens));
   if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
   if (!aligned4(counts) || !aligned4(offsets) || !aligned4(active) || !aligned4(n_active))
@@ -306,13 +309,13 @@ sw_status sw_moe_route_dispatch_shared(const sw_moe_dims* d, const uint16_t* x, 
       (bias && !aligned4(bias)))
     return SW_ERR_ALIGN;
   if (workspace_bytes < sw::route_shared_workspace_bytes(n_tokens, d->hidden, d->n_experts,
-                                                         d->top_k, n_shared))
+                                                         d->top_k, n_shared, n_groups))
     return SW_ERR_WORKSPACE;
   (void)hipGetLastError();
   return launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, d->hidden,
                                             d->n_experts, d->top_k, topk_ids, topk_w, gap, counts,
                                             offsets, perm, active, n_active, workspace,
-                                            as_stream(stream), n_shared));
+                                            as_stream(stream), n_shared, n_groups));
 }
 
 size_t sw_moe_forward_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {

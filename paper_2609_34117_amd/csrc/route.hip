@@ -211,7 +211,14 @@ constexpr int kMaxSplit = 4;  // slices of H per logit tile
 // slots of the shared expert's parts after them (ids m .. m + S - 1).
 struct Cols {
   int m, ld, k, S;
+  int R;  // token groups of the shared parts: the pool holds R copies of the S parts
+  __device__ __host__ int plan_m() const { return m + R * S; }
 };
+
+// Token t's group of shared-part copies: R contiguous runs of the batch.
+__device__ __forceinline__ int token_group(const Cols& c, int t, int T) {
+  return c.R > 1 ? (int)((long long)t * c.R / T) : 0;
+}
 
 // Order key of token t's logit for expert e: z = sum of the KS partials in
 // slice order, plus the bias; 0 marks an ineligible expert (the one logit
@@ -372,17 +379,18 @@ __device__ __forceinline__ Selection select_wave(const float* part, int KS, int 
 
 // Slot `slot` of token t: a routed slot (slot < k) takes the selection,
 // a shared slot k + s the shared expert's part m + s with the shared gate.
-__device__ __forceinline__ int slot_id(const Selection& s, const Cols& c, int slot) {
-  return slot < c.k ? s.id : c.m + slot - c.k;
+__device__ __forceinline__ int slot_id(const Selection& s, const Cols& c, int slot, int t, int T) {
+  return slot < c.k ? s.id : c.m + token_group(c, t, T) * c.S + slot - c.k;
 }
 
-__device__ __forceinline__ void store_selection(const Selection& s, int t, const Cols& c, int slot,
-                                                float sgate, int* __restrict__ topk_ids,
+__device__ __forceinline__ void store_selection(const Selection& s, int t, int T, const Cols& c,
+                                                int slot, float sgate,
+                                                int* __restrict__ topk_ids,
                                                 float* __restrict__ topk_w,
                                                 float* __restrict__ gap) {
   const int kout = c.k + c.S;
   if (slot < kout) {
-    topk_ids[(size_t)t * kout + slot] = slot_id(s, c, slot);
+    topk_ids[(size_t)t * kout + slot] = slot_id(s, c, slot, t, T);
     topk_w[(size_t)t * kout + slot] = slot < c.k ? s.gate : sgate;
   }
   if (gap != nullptr && slot == 0) gap[t] = s.gap;
@@ -402,13 +410,13 @@ __global__ __launch_bounds__(256) void route_topk_kernel(const float* __restrict
     const int t = blockIdx.x * 16 + (threadIdx.x >> 4);
     const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
     const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
-    if (t < T) store_selection(s, t, c, threadIdx.x & 15, sg, topk_ids, topk_w, gap);
+    if (t < T) store_selection(s, t, T, c, threadIdx.x & 15, sg, topk_ids, topk_w, gap);
   } else {
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;  // wave-uniform
     const Selection s = select_wave<KPL>(part, KS, T, c, t, bias, keep_mask);
     const float sg = c.S > 0 ? shared_gate(part, KS, T, c, t) : 0.f;
-    store_selection(s, t, c, threadIdx.x & 63, sg, topk_ids, topk_w, gap);
+    store_selection(s, t, T, c, threadIdx.x & 63, sg, topk_ids, topk_w, gap);
   }
 }
 
@@ -447,13 +455,13 @@ __global__ __launch_bounds__(kFusedThreads) void route_select_dispatch_kernel(
     const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
     const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
     if (t < T) {
-      store_selection(s, t, c, r, sg, topk_ids, topk_w, gap);
-      if (r < kout) ids_s[t * kout + r] = slot_id(s, c, r);
+      store_selection(s, t, T, c, r, sg, topk_ids, topk_w, gap);
+      if (r < kout) ids_s[t * kout + r] = slot_id(s, c, r, t, T);
     }
   }
   __syncthreads();
   const DispatchLds lds{cursor, wave_base, wave_cnt, scan_scratch, &bad};
-  dispatch_block(ids_s, T * kout, c.m + c.S, lds, counts, offsets, perm, active, n_active);
+  dispatch_block(ids_s, T * kout, c.plan_m(), lds, counts, offsets, perm, active, n_active);
 }
 
 // Route + dispatch of at most 4 tokens (at most 64 pairs) in one wave: the
@@ -471,14 +479,14 @@ __global__ __launch_bounds__(64) void route_select_dispatch_wave_kernel(
   const int lane = threadIdx.x, t = lane >> 4, r = lane & 15;
   const Selection s = select_row<KPL>(part, KS, T, c, t, bias, keep_mask);
   const float sg = (c.S > 0 && t < T) ? shared_gate(part, KS, T, c, t) : 0.f;
-  if (t < T) store_selection(s, t, c, r, sg, topk_ids, topk_w, gap);
+  if (t < T) store_selection(s, t, T, c, r, sg, topk_ids, topk_w, gap);
   // the plan covers the m selectable experts and the S shared parts (<= 256
   // in all), kout slots a token; pair q = t' * kout + j is slot j of lane
   // 16 t' + j
-  const int kout = c.k + c.S, m = c.m + c.S;
+  const int kout = c.k + c.S, m = c.plan_m();
   const int n_pairs = T * kout;
   const bool valid = lane < n_pairs;
-  const int e = __shfl(slot_id(s, c, r), valid ? (lane / kout) * 16 + lane % kout : 0);
+  const int e = __shfl(slot_id(s, c, r, t, T), valid ? (lane / kout) * 16 + lane % kout : 0);
   if (__ballot(valid && (e < 0 || e >= m)) != 0) {  // the flagged plan
     for (int i = lane; i <= m; i += 64) {
       if (i < m) counts[i] = 0;
@@ -736,9 +744,9 @@ size_t route_workspace_bytes(int T, int H, int m, int k) {
   return part_bytes(T, H, m) + dispatch_workspace_bytes(T * k, m);
 }
 
-size_t route_shared_workspace_bytes(int T, int H, int m, int k, int S) {
+size_t route_shared_workspace_bytes(int T, int H, int m, int k, int S, int R) {
   if (T <= 0) return 0;
-  return part_bytes(T, H, m + 1) + dispatch_workspace_bytes(T * (k + S), m + S);
+  return part_bytes(T, H, m + 1) + dispatch_workspace_bytes(T * (k + S), m + R * S);
 }
 
 namespace {
@@ -761,22 +769,22 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
                         const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                         float* topk_w, float* gap, void* workspace, hipStream_t stream) {
   if (T == 0) return hipSuccess;
-  return route_cols(x, T, wr, bias, keep_mask, H, Cols{m, m, k, 0}, topk_ids, topk_w, gap,
+  return route_cols(x, T, wr, bias, keep_mask, H, Cols{m, m, k, 0, 1}, topk_ids, topk_w, gap,
                     workspace, stream);
 }
 
-bool fused_route_dispatch_supported(int T, int m, int k, int S) {
-  return T > 0 && T <= kFusedMaxTokens && m + S <= kFusedMaxPool && k + S <= kFusedMaxK;
+bool fused_route_dispatch_supported(int T, int m, int k, int S, int R) {
+  return T > 0 && T <= kFusedMaxTokens && m + R * S <= kFusedMaxPool && k + S <= kFusedMaxK;
 }
 
 hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
                                  const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                                  float* topk_w, float* gap, int* counts, int* offsets, int* perm,
                                  int* active, int* n_active, void* workspace, hipStream_t stream,
-                                 int n_shared) {
-  const Cols c{m, n_shared > 0 ? m + 1 : m, k, n_shared};
-  const int kout = k + n_shared, m_plan = m + n_shared;
-  if (!fused_route_dispatch_supported(T, m, k, n_shared)) {
+                                 int n_shared, int n_groups) {
+  const Cols c{m, n_shared > 0 ? m + 1 : m, k, n_shared, n_shared > 0 ? n_groups : 1};
+  const int kout = k + n_shared, m_plan = c.plan_m();
+  if (!fused_route_dispatch_supported(T, m, k, n_shared, c.R)) {
     if (T > 0) {
       hipError_t err = route_cols(x, T, wr, bias, keep_mask, H, c, topk_ids, topk_w, gap,
                                   workspace, stream);

@@ -51,15 +51,17 @@ hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts,
 // fused_route_dispatch_supported, else the separate kernels.
 // With n_shared > 0 the router has a last row, the shared expert's gate,
 // and every token gets n_shared more slots after its k routed ones: the
-// shared expert's parts, pool ids m .. m + n_shared - 1, with the sigmoid of
-// that gate logit; the plan then covers m + n_shared experts.
-bool fused_route_dispatch_supported(int T, int m, int k, int n_shared = 0);
-size_t route_shared_workspace_bytes(int T, int H, int m, int k, int n_shared);
+// shared expert's parts with the sigmoid of that gate logit.  The pool
+// holds n_groups copies of the parts; token t of T uses copy
+// g = t * n_groups / T, pool ids m + g * n_shared .. + n_shared - 1, and the
+// plan covers m + n_groups * n_shared experts.
+bool fused_route_dispatch_supported(int T, int m, int k, int n_shared = 0, int n_groups = 1);
+size_t route_shared_workspace_bytes(int T, int H, int m, int k, int n_shared, int n_groups);
 hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
                                  const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
                                  float* topk_w, float* gap, int* counts, int* offsets, int* perm,
                                  int* active, int* n_active, void* workspace, hipStream_t stream,
-                                 int n_shared = 0);
+                                 int n_shared = 0, int n_groups = 1);
 
 // Kernel family serving a gate/up or a down call of a shape; the launchers
 // dispatch on it (values as sw_kernel_family in the ABI header).

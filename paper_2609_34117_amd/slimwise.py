@@ -44,8 +44,9 @@ def _load() -> ctypes.CDLL:
         "sw_moe_dispatch": ([D, P, I32, P, P, P, P, P, P], ctypes.c_int),
         "sw_moe_route_dispatch": ([D, P, I32, P, P, P, P, P, P, P, P, P, P, P, P, SZ, P],
                                   ctypes.c_int),
-        "sw_moe_route_shared_workspace_bytes": ([D, I32, I32], SZ),
-        "sw_moe_route_dispatch_shared": ([D, P, I32, P, P, P, I32, P, P, P, P, P, P, P, P, P, SZ, P],
+        "sw_moe_route_shared_workspace_bytes": ([D, I32, I32, I32], SZ),
+        "sw_moe_route_dispatch_shared": ([D, P, I32, P, P, P, I32, I32, P, P, P, P, P, P, P, P, P,
+                                          SZ, P],
                                          ctypes.c_int),
         "sw_moe_forward_workspace_bytes": ([D, I32], SZ),
         "sw_moe_forward_kernels": ([D, I32, I32, P, P], ctypes.c_int),
@@ -69,7 +70,7 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 8
+ABI_VERSION = 9
 NO_ALLOC_SCRATCH_BYTES = 32 << 20
 ROW_MAJOR, TILED = 0, 1
 # sw_kernel_family values
@@ -260,19 +261,22 @@ def sw_moe_route_dispatch(x: torch.Tensor, wr: torch.Tensor, top_k: int, *, keep
     return ids, w, gap, plan
 
 
-def sw_moe_route_shared_workspace_bytes(d: Dims, n_tokens: int, n_shared: int) -> int:
-    return LIB.sw_moe_route_shared_workspace_bytes(ctypes.byref(d), n_tokens, n_shared)
+def sw_moe_route_shared_workspace_bytes(d: Dims, n_tokens: int, n_shared: int,
+                                        n_groups: int = 1) -> int:
+    return LIB.sw_moe_route_shared_workspace_bytes(ctypes.byref(d), n_tokens, n_shared, n_groups)
 
 
 def sw_moe_route_dispatch_shared(x: torch.Tensor, wr: torch.Tensor, top_k: int, n_shared: int, *,
-                                 keep_mask=None, bias=None, want_gap=True, out=None,
-                                 plan: Optional[Plan] = None, ws=None, stream=None):
+                                 n_groups: int = 1, keep_mask=None, bias=None, want_gap=True,
+                                 out=None, plan: Optional[Plan] = None, ws=None, stream=None):
     """Section 3.3: route + dispatch with the shared expert folded into the
     plan.  ``wr`` is [m + 1, H] (the router rows, then the shared gate row);
-    every token gets ``n_shared`` more slots, ids m .. m + n_shared - 1, with
-    the sigmoid of the shared gate logit.
+    the pool holds ``n_groups`` copies of the ``n_shared`` parts, and token
+    t gets ``n_shared`` more slots, ids m + g * n_shared + s with
+    g = t * n_groups // T, with the sigmoid of the shared gate logit.
 
-    Returns ``(topk_ids [T, k + n_shared], topk_w, gap, plan over m + n_shared)``."""
+    Returns ``(topk_ids [T, k + n_shared], topk_w, gap, plan over
+    m + n_groups * n_shared)``."""
     t, hidden = x.shape
     m = wr.shape[0] - 1
     kout = top_k + n_shared
@@ -282,13 +286,13 @@ def sw_moe_route_dispatch_shared(x: torch.Tensor, wr: torch.Tensor, top_k: int, 
                _empty(t, torch.float32, x.device) if want_gap else None)
     ids, w, gap = out
     if plan is None:
-        plan = alloc_plan(t, m + n_shared, kout, x.device)
+        plan = alloc_plan(t, m + n_groups * n_shared, kout, x.device)
     if ws is None:
-        ws = workspace(sw_moe_route_shared_workspace_bytes(d, t, n_shared), x.device)
+        ws = workspace(sw_moe_route_shared_workspace_bytes(d, t, n_shared, n_groups), x.device)
     st = LIB.sw_moe_route_dispatch_shared(
         ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
         _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
-        n_shared, _ptr(ids), _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets),
+        n_shared, n_groups, _ptr(ids), _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets),
         _ptr(plan.perm), _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
         _stream(stream))
     _check(st, "sw_moe_route_dispatch_shared")

@@ -781,34 +781,42 @@ def _shared_parts(w13s, w2s, inter, n_shared):
     return p13, p2
 
 
-def _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled):
+def _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled, n_groups=1):
     inter = L["w2"].shape[2]
     p13, p2 = _shared_parts(w13s, w2s, inter, n_shared)
-    w13 = dev(np.concatenate([L["w13"], p13]))
-    w2 = dev(np.concatenate([L["w2"], p2]))
+    # the pool: the routed experts, then n_groups copies of the parts
+    w13 = dev(np.concatenate([L["w13"]] + [p13] * n_groups))
+    w2 = dev(np.concatenate([L["w2"]] + [p2] * n_groups))
     layout = sw.ROW_MAJOR
     if tiled:
         w13, w2 = sw.sw_moe_pack_experts(w13, w2)
         layout = sw.TILED
     wr = dev(np.concatenate([L["wr"], gate[None]]))
     ids, w, gap, plan = sw.sw_moe_route_dispatch_shared(
-        dev(L["x"]), wr, top_k, n_shared, keep_mask=None if mask is None else dev(mask))
+        dev(L["x"]), wr, top_k, n_shared, n_groups=n_groups,
+        keep_mask=None if mask is None else dev(mask))
     out = sw.sw_moe_forward(dev(L["x"]), w13, w2, w, plan, layout=layout)
     return ids, w, gap, plan, out
 
 
-@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,n_shared,masked,tiled", [
-    (2048, 64, 8, 512, 64, 2, False, True),    # batch 64: the 1024-thread route + plan block
-    (2048, 128, 8, 512, 1, 2, True, False),    # one token: the one-wave route + plan
-    (2048, 64, 8, 768, 17, 1, False, False),   # 17 tokens: the 512-thread block, one part
-    (2048, 256, 8, 512, 100, 2, False, True),  # 100 tokens: the wave-form top-k, then dispatch
-    (1024, 200, 14, 256, 40, 2, True, False),  # k + parts = 16: the row form at its limit
-    (2048, 96, 6, 512, 200, 4, False, False),  # 4 parts: 200-token parts over gate/up passes
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,n_shared,masked,tiled,groups", [
+    (2048, 64, 8, 512, 64, 2, False, True, 1),    # batch 64: wave-form top-k, then dispatch;
+                                                  # parts with every token (two passes)
+    (2048, 64, 8, 512, 64, 2, False, True, 2),    # the same in two groups of 32 tokens
+    (2048, 128, 8, 512, 1, 2, True, False, 1),    # one token: the one-wave route + plan
+    (2048, 128, 8, 512, 3, 2, True, False, 3),    # 3 groups of one token: the one-wave path
+    (2048, 64, 8, 768, 17, 1, False, False, 1),   # 17 tokens: the 512-thread block, one part
+    (2048, 64, 8, 768, 17, 1, False, True, 2),    # the 512-thread block, groups of 8 and 9
+    (2048, 256, 8, 512, 100, 2, False, True, 1),  # 100 tokens: wave-form top-k, then dispatch
+    (2048, 256, 8, 512, 100, 2, False, True, 4),  # four groups of 25 tokens
+    (1024, 200, 14, 256, 40, 2, True, False, 3),  # k + parts = 16: the row form at its limit
+    (2048, 96, 6, 512, 200, 4, False, False, 1),  # 4 parts: 200-token parts over gate/up passes
 ])
 def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter, tokens, n_shared,
-                                            masked, tiled):
+                                            masked, tiled, groups):
     # Section 3.3: the always-on shared expert behind a sigmoid gate, run as
-    # n_shared extra experts every token routes to
+    # n_shared extra experts every token routes to (token t to the parts of
+    # copy t * groups // T)
     cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=23)
     g = np.random.default_rng([401, hidden, tokens])
     isz = n_shared * inter
@@ -816,7 +824,8 @@ def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter,
     w2s = I.to_bf16_bits(0.02 * g.standard_normal((hidden, isz), dtype=np.float32))
     gate = (0.05 * g.standard_normal(hidden)).astype(np.float32)
     mask = mask_for(cfg, L, 0.5) if masked else None
-    ids, w, gap, plan, out = _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled)
+    ids, w, gap, plan, out = _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled,
+                                           n_groups=groups)
     ids, w, gap = host(ids), host(w), host(gap)
     m, k = n_experts, top_k
     # routed slots: the oracle's routing rule; shared slots: every part, with
@@ -826,10 +835,11 @@ def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter,
                     what=f"folded shared T={tokens}")
     xf = I.bf16_bits_to_f32(L["x"]).astype(np.float64)
     sig = 1.0 / (1.0 + np.exp(-(xf @ gate.astype(np.float64))))
+    copy = np.arange(tokens) * groups // tokens
     for s in range(n_shared):
-        assert np.all(ids[:, k + s] == m + s)
+        assert np.all(ids[:, k + s] == m + copy * n_shared + s)
         np.testing.assert_allclose(w[:, k + s], sig, rtol=0, atol=1e-6)
-    counts, offsets, perm, active, n_active = oracle.dispatch(ids, m + n_shared)
+    counts, offsets, perm, active, n_active = oracle.dispatch(ids, m + groups * n_shared)
     np.testing.assert_array_equal(host(plan.counts), counts)
     np.testing.assert_array_equal(host(plan.offsets), offsets)
     np.testing.assert_array_equal(host(plan.perm)[: ids.size], perm)
@@ -840,8 +850,12 @@ def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter,
                                 np.ascontiguousarray(ids[:, :k]), np.ascontiguousarray(w[:, :k]))
     o_out = oracle.shared_expert(L["x"], w13s, w2s, gate, out=o_out)
     err, rel = compare_out(host(out), o_out)
-    print(f"folded shared H={hidden} m={m} k={k} I={inter} T={tokens} parts={n_shared}: "
-          f"max|err|={err:.3g} rel={rel:.3g}")
+    print(f"folded shared H={hidden} m={m} k={k} I={inter} T={tokens} parts={n_shared} "
+          f"groups={groups}: max|err|={err:.3g} rel={rel:.3g}")
+    if groups > 1:
+        # every copy holds the same weights: the output equals one copy's
+        one = _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled)
+        assert torch.equal(out, one[4])
 
 
 def test_folded_shared_expert_zero_se2_is_se1_bit_for_bit(sw):
