@@ -78,15 +78,15 @@ PAPER_CONTEXT = {
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
 # `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
-# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197882.6 KiB x
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197820.45 KiB x
 # 1.99982 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
-# of 192-768 MiB) + WRITE_SIZE 1558.9 KiB x 1.0 (WRITE_SIZE of the copies is
+# of 192-768 MiB) + WRITE_SIZE 1567.95 KiB x 1.0 (WRITE_SIZE of the copies is
 # exact).  The figure holds while the gate/up kernel's sources hash as below.
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="d797c89480be3d9be1ef4ffcb48a657ff52d0742016ef64b34c7b855a7259d1c",
+GATE_UP_TRAFFIC = dict(sources_sha256="24051af7129796e5727f84cf49ce034209f12aeb5af1e64436784b9a23a13c87",
                        workload=("decode_b64", 64, 0.5, "tiled"),
-                       bytes_per_launch=int(round((197882.6 * 1.99982 + 1558.9) * 1024)))
+                       bytes_per_launch=int(round((197820.45 * 1.99982 + 1567.95) * 1024)))
 
 
 def parse():
@@ -638,6 +638,12 @@ def run_decode_shared(args, sw, torch, dev):
     return line
 
 
+def route_phase(s):
+    """Route + dispatch time of a measured point: the eager step minus its
+    forward phases (each timed between events on the launch stream)."""
+    return s["t_step_us"] - s["t_gate_up_us"] - s["t_down_us"] - s["t_combine_us"]
+
+
 def run_colocated(args, sw, torch, dev):
     import copy
 
@@ -670,7 +676,17 @@ def run_colocated(args, sw, torch, dev):
     line["detail"] = {
         "masked_full_pool": rounded(sm), "compacted_pool": rounded(sc), "unmasked_full_pool": rounded(sf),
         "prefill_unmasked_4096": rounded(sp),
-        "mask_overhead_us_per_layer": round(sm["t_step_us"] - sc["t_step_us"], 3),
+        # the mask's cost per layer: masked full pool minus compacted pool, from
+        # graph replay (no host calls in the difference) and per phase; the
+        # eager difference includes host-side noise and is kept for reference
+        "mask_overhead_us_per_layer": round(sm["t_step_graph_us"] - sc["t_step_graph_us"], 3),
+        "mask_overhead_us_per_layer_eager": round(sm["t_step_us"] - sc["t_step_us"], 3),
+        "mask_overhead_us_by_phase": {
+            "route_dispatch": round(route_phase(sm) - route_phase(sc), 3),
+            "gate_up": round(sm["gate_up_launch_us"] - sc["gate_up_launch_us"], 3),
+            "down": round(sm["down_launch_us"] - sc["down_launch_us"], 3),
+            "combine": round(sm["t_combine_us"] - sc["t_combine_us"], 3),
+        },
         "speedup_masked_vs_full": round(sf["t_step_us"] / sm["t_step_us"], 3),
     }
     if not args.no_cpu_baseline:
