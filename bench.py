@@ -144,8 +144,11 @@ class Runner:
         rbytes = (sw.sw_moe_route_shared_workspace_bytes(d, T, S, pool.n_groups) if S else
                   sw.sw_moe_route_workspace_bytes(d, T))
         self.rws = sw.workspace(rbytes, dev)
-        self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(
-            sw.dims(H, Iw, self.m_plan, self.kout), T), dev)
+        fd = sw.dims(H, Iw, self.m_plan, self.kout)
+        self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(fd, T), dev)
+        self.lws = sw.workspace(sw.sw_moe_layer_workspace_bytes(d, T, S, pool.n_groups), dev)
+        # decode batches: the step's gate/up launch builds the plan itself
+        self.builds = sw.sw_moe_gate_up_builds_plan(fd, T, pool.layout)
         self.sws = None
         if pool.shared is not None:
             ds = sw.dims(H, pool.shared[1].shape[-1], 1, 1)
@@ -164,22 +167,44 @@ class Runner:
                                      out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
 
     def plan_for(self, x):
-        """A dispatch plan of its own for batch `x` (route + dispatch)."""
+        """The routed ids and a dispatch plan of their own for batch `x`
+        (route + dispatch)."""
         plan = self.sw.alloc_plan(self.T, self.m_plan, self.kout, x.device)
         self.route(x, plan)
-        return plan
+        return self.ids.clone(), plan
 
     def step(self, x, c, ev=None):
+        """One layer step.  Whole steps (ev None) are one sw_moe_layer call
+        (with a separate shared expert, route + dispatch, the forward and
+        the shared expert's call).  With ev, the same kernels with events
+        between the forward's phases: the routing (and, where the gate/up
+        launch does not build it, the dispatch), then gate/up, down and
+        combine."""
         sw, p = self.sw, self.pool
-        self.route(x, self.plan)
         if ev is None:
+            if p.shared is None:
+                sw.sw_moe_layer(x, p.wr, self.cfg.top_k, p.w13[c], p.w2[c], layout=p.layout,
+                                n_shared=p.n_shared, n_groups=p.n_groups, bias=p.bias,
+                                keep_mask=p.keep_mask, route_out=(self.ids, self.w, self.gap),
+                                plan=self.plan, out=self.out, ws=self.lws)
+                return
+            self.route(x, self.plan)
             sw.sw_moe_forward(x, p.w13[c], p.w2[c], self.w, self.plan, layout=p.layout,
                               out=self.out, ws=self.fws)
-            if p.shared is not None:
-                sw.sw_moe_shared_expert(x, *p.shared, self.out, layout=p.layout, ws=self.sws)
+            sw.sw_moe_shared_expert(x, *p.shared, self.out, layout=p.layout, ws=self.sws)
             return
+        plan_in_gate_up = self.builds and not p.n_shared
+        if plan_in_gate_up:
+            sw.sw_moe_route(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
+                            out=(self.ids, self.w, self.gap), ws=self.rws)
+        else:
+            self.route(x, self.plan)
         ev[0].record()
-        sw.sw_moe_forward_gate_up(x, p.w13[c], self.kout, self.plan, self.fws, layout=p.layout)
+        if plan_in_gate_up:
+            sw.sw_moe_forward_gate_up_plan(x, p.w13[c], self.ids, self.plan, self.fws,
+                                           layout=p.layout)
+        else:
+            sw.sw_moe_forward_gate_up(x, p.w13[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[1].record()
         sw.sw_moe_forward_down(self.T, p.w2[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[2].record()
@@ -250,28 +275,32 @@ def time_graph(torch, r: Runner, xs, reps):
 def time_kernels(torch, r: Runner, xs, steps):
     """Mean launch duration of gate_up and of down: `steps` launches of one
     kernel back to back between two HIP events on the launch stream, rotating
-    the batches (each with its own plan) and the pool copies.  (The small
-    kernels are shorter than a host call, so their durations come from the
-    kernel trace instead.)"""
+    the batches (each with its own ids and plan) and the pool copies.  The
+    gate_up launch is the step's: on decode batches it builds the plan from
+    the ids on the way.  (The small kernels are shorter than a host call, so
+    their durations come from the kernel trace instead.)"""
     sw, p, k = r.sw, r.pool, r.kout
-    plans = [r.plan_for(x) for x in xs]
+    routed = [r.plan_for(x) for x in xs]
     torch.cuda.synchronize()
     out = {}
+
+    def launch(name, s):
+        j, c = s % len(xs), s % N_COPIES
+        ids, plan = routed[j]
+        if name == "down":
+            sw.sw_moe_forward_down(r.T, p.w2[c], k, plan, r.fws, layout=p.layout)
+        elif r.builds and p.shared is None:
+            sw.sw_moe_forward_gate_up_plan(xs[j], p.w13[c], ids, plan, r.fws, layout=p.layout)
+        else:
+            sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plan, r.fws, layout=p.layout)
+
     for name in ("gate_up", "down"):
         for s in range(4):
-            j, c = s % len(xs), s % N_COPIES
-            if name == "gate_up":
-                sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
-            else:
-                sw.sw_moe_forward_down(r.T, p.w2[c], k, plans[j], r.fws, layout=p.layout)
+            launch(name, s)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for s in range(steps):
-            j, c = s % len(xs), s % N_COPIES
-            if name == "gate_up":
-                sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
-            else:
-                sw.sw_moe_forward_down(r.T, p.w2[c], k, plans[j], r.fws, layout=p.layout)
+            launch(name, s)
         e1.record()
         torch.cuda.synchronize()
         out[name] = e0.elapsed_time(e1) / 1e3 / steps
@@ -639,8 +668,9 @@ def run_decode_shared(args, sw, torch, dev):
 
 
 def route_phase(s):
-    """Route + dispatch time of a measured point: the eager step minus its
-    forward phases (each timed between events on the launch stream)."""
+    """Routing time of a measured point (with the dispatch where the gate/up
+    launch does not build the plan): the eager step minus its forward phases
+    (each timed between events on the launch stream)."""
     return s["t_step_us"] - s["t_gate_up_us"] - s["t_down_us"] - s["t_combine_us"]
 
 

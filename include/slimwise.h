@@ -87,7 +87,7 @@ typedef enum {
 } sw_kernel_family;
 
 /* ABI version of this header (bumped on any signature change). */
-#define SW_ABI_VERSION 9
+#define SW_ABI_VERSION 10
 int32_t sw_abi_version(void);
 
 /*
@@ -359,6 +359,74 @@ sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint
 sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const float* topk_w,
                                  const int32_t* n_active, float* out, void* workspace,
                                  size_t workspace_bytes, void* stream);
+
+/*
+ * Whether the gate/up phase builds the dispatch plan itself for T tokens of
+ * this shape and layout (the forward's dims: the pool's m and slots per
+ * token): 1 for decode batches of 3 to 64 tokens that the 32-token streaming
+ * kernels serve, with m <= 512, T*k <= 1024 and 3m + 2 + T*k <= 2464 (the
+ * plan's LDS), else 0 (also on invalid arguments).  Host-side only.
+ */
+int32_t sw_moe_gate_up_builds_plan(const sw_moe_dims* d, int32_t n_tokens, int32_t layout);
+
+/*
+ * The gate/up phase (as sw_moe_forward_gate_up) that builds the dispatch
+ * plan of topk_ids on the way (Section 2.1): every block of the launch builds
+ * the plan in LDS, one of them writes counts, offsets, perm, active and
+ * n_active -- what sw_moe_dispatch writes for the same ids, bit for bit,
+ * in-band flag included -- and the down and combine phases then read them.
+ * sw_moe_layer runs this launch in place of the dispatch kernel.
+ *   topk_ids   int32 [T, k] (k = d->top_k, ids into the pool of d->n_experts)
+ *   counts, offsets, perm, active, n_active  out, as for sw_moe_dispatch
+ * Errors: as sw_moe_forward_gate_up, and SW_ERR_UNSUPPORTED where
+ * sw_moe_gate_up_builds_plan is 0 (T = 0 included).
+ */
+sw_status sw_moe_forward_gate_up_plan(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                      const uint16_t* w13, int32_t layout,
+                                      const int32_t* topk_ids, int32_t* counts, int32_t* offsets,
+                                      int32_t* perm, int32_t* active, int32_t* n_active,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes sw_moe_layer needs (0 on invalid arguments). */
+size_t sw_moe_layer_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens, int32_t n_shared,
+                                    int32_t n_groups);
+
+/*
+ * One MoE layer in one call: routing (Section 3.1, Eq. 2 and the
+ * renormalisation), the dispatch plan (Section 2.1, Eq. 1), the expert FFNs
+ * and the weighted combine.  Every output is bit for bit what
+ * sw_moe_route_dispatch (n_shared = 0) or sw_moe_route_dispatch_shared
+ * (n_shared > 0) followed by sw_moe_forward would write with the same
+ * arguments, the forward taking the dims {H, I, m + n_groups * n_shared,
+ * k + n_shared}.  On decode batches that the 32-token streaming kernels
+ * serve (3 to 64 tokens; at most 512 plan experts and 1024 pairs, within the
+ * kernels' LDS), the plan is built inside the gate/up launch: each of its
+ * blocks builds it in LDS from the selected ids, and one of them writes it
+ * out, which saves the dispatch launch of the step.  Other shapes run the
+ * two calls' kernels.
+ *
+ *   d, x, wr, bias, keep_mask   as for sw_moe_route (n_shared = 0) or
+ *              sw_moe_route_dispatch_shared (n_shared > 0: wr has the shared
+ *              gate row after the m router rows)
+ *   n_shared   parts of a folded shared expert, 0 for none; n_groups their
+ *              copies in the pool (ignored when n_shared = 0; as
+ *              sw_moe_route_dispatch_shared otherwise)
+ *   w13, w2, layout   the pool of m + n_groups * n_shared experts, as for
+ *              sw_moe_forward
+ *   topk_ids, topk_w  out [T, k + n_shared]; gap nullable out fp32 [T]
+ *   counts, offsets, perm, active, n_active  out: the plan, as for
+ *              sw_moe_dispatch over the m + n_groups * n_shared experts
+ *   out        out fp32 [T, H]
+ *   workspace  >= sw_moe_layer_workspace_bytes(d, T, n_shared, n_groups)
+ * In-band errors as the two calls (a flagged plan fills out with NaN).
+ * T = 0 writes the empty plan and nothing else.
+ */
+sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
+                       const float* bias, const uint8_t* keep_mask, int32_t n_shared,
+                       int32_t n_groups, const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                       int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                       int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
+                       float* out, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Workspace bytes sw_moe_routing_mass needs for T tokens (0 if T == 0). */
 size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);

@@ -150,6 +150,39 @@ sw_status launch_forward(const sw_moe_dims* d, const uint16_t* x, int32_t n_toke
   return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, m, k, workspace, s));
 }
 
+// The dims of the pool a layer call's forward runs on: the routed pool, and
+// the shared expert's parts after it.
+sw_moe_dims layer_pool_dims(const sw_moe_dims* d, int32_t n_shared, int32_t n_groups) {
+  if (n_shared == 0) return *d;
+  return sw_moe_dims{d->hidden, d->inter, d->n_experts + n_groups * n_shared,
+                     d->top_k + n_shared};
+}
+
+size_t layer_route_bytes(const sw_moe_dims* d, int32_t T, int32_t n_shared, int32_t n_groups) {
+  if (n_shared == 0) return sw::route_workspace_bytes(T, d->hidden, d->n_experts, d->top_k);
+  return sw::route_shared_workspace_bytes(T, d->hidden, d->n_experts, d->top_k, n_shared,
+                                          n_groups);
+}
+
+// Dims, shared-expert and token arguments of a layer call.
+sw_status check_layer_dims(const sw_moe_dims* d, int32_t n_tokens, int32_t n_shared,
+                           int32_t n_groups) {
+  SW_TRY(check_dims(d));
+  if (n_shared < 0) return SW_ERR_SHAPE;
+  if (n_shared > 0) SW_TRY(check_shared(d, n_shared, n_groups));
+  const sw_moe_dims pool = layer_pool_dims(d, n_shared, n_groups);
+  SW_TRY(check_dims(&pool));
+  return check_tokens(&pool, n_tokens);
+}
+
+size_t layer_workspace_bytes(const sw_moe_dims* d, int32_t T, int32_t n_shared,
+                             int32_t n_groups) {
+  if (T <= 0) return 0;
+  const sw_moe_dims pool = layer_pool_dims(d, n_shared, n_groups);
+  return sw::align_up(layer_route_bytes(d, T, n_shared, n_groups), 256) +
+         sw::forward_workspace_bytes(T, pool.hidden, pool.inter, pool.top_k);
+}
+
 }  // namespace
 
 extern "C" {
@@ -355,6 +388,34 @@ sw_status sw_moe_forward_gate_up(const sw_moe_dims* d, const uint16_t* x, int32_
                                      as_stream(stream)));
 }
 
+int32_t sw_moe_gate_up_builds_plan(const sw_moe_dims* d, int32_t n_tokens, int32_t layout) {
+  if (check_dims(d) != SW_OK || check_tokens(d, n_tokens) != SW_OK || n_tokens == 0 ||
+      check_layout(d, n_tokens, layout) != SW_OK)
+    return 0;
+  return sw::wave_plan_supported(n_tokens, d->hidden, d->inter, d->n_experts, d->top_k,
+                                 layout == SW_LAYOUT_TILED)
+             ? 1
+             : 0;
+}
+
+sw_status sw_moe_forward_gate_up_plan(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens,
+                                      const uint16_t* w13, int32_t layout,
+                                      const int32_t* topk_ids, int32_t* counts, int32_t* offsets,
+                                      int32_t* perm, int32_t* active, int32_t* n_active,
+                                      void* workspace, size_t workspace_bytes, void* stream) {
+  SW_TRY(check_forward_common(d, n_tokens, counts, offsets, perm, active, n_active, workspace,
+                              workspace_bytes));
+  if (n_tokens == 0) return SW_ERR_UNSUPPORTED;
+  SW_TRY(check_layout(d, n_tokens, layout));
+  if (!x || !w13 || !topk_ids) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w13) || !aligned4(topk_ids)) return SW_ERR_ALIGN;
+  if (!sw_moe_gate_up_builds_plan(d, n_tokens, layout)) return SW_ERR_UNSUPPORTED;
+  (void)hipGetLastError();
+  return launched(sw::launch_gate_up_building_plan(
+      x, n_tokens, w13, layout == SW_LAYOUT_TILED, topk_ids, counts, offsets, perm, active,
+      n_active, d->hidden, d->inter, d->n_experts, d->top_k, workspace, as_stream(stream)));
+}
+
 sw_status sw_moe_forward_down(const sw_moe_dims* d, int32_t n_tokens, const uint16_t* w2,
                               int32_t layout, const int32_t* counts, const int32_t* offsets,
                               const int32_t* perm, const int32_t* active, const int32_t* n_active,
@@ -386,6 +447,61 @@ sw_status sw_moe_forward_combine(const sw_moe_dims* d, int32_t n_tokens, const f
   (void)hipGetLastError();
   return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, d->hidden, d->inter,
                                      d->n_experts, d->top_k, workspace, as_stream(stream)));
+}
+
+size_t sw_moe_layer_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens, int32_t n_shared,
+                                    int32_t n_groups) {
+  if (check_layer_dims(d, n_tokens, n_shared, n_groups) != SW_OK) return 0;
+  return layer_workspace_bytes(d, n_tokens, n_shared, n_groups);
+}
+
+sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
+                       const float* bias, const uint8_t* keep_mask, int32_t n_shared,
+                       int32_t n_groups, const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                       int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                       int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
+                       float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  SW_TRY(check_layer_dims(d, n_tokens, n_shared, n_groups));
+  const sw_moe_dims pool = layer_pool_dims(d, n_shared, n_groups);
+  if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
+  if (!aligned4(counts) || !aligned4(offsets) || !aligned4(active) || !aligned4(n_active))
+    return SW_ERR_ALIGN;
+  const hipStream_t s = as_stream(stream);
+  if (n_tokens == 0) {
+    (void)hipGetLastError();
+    return launched(sw::launch_dispatch(nullptr, 0, pool.n_experts, counts, offsets, nullptr,
+                                        active, n_active, s));
+  }
+  if (!x || !wr || !topk_ids || !topk_w || !perm || !workspace) return SW_ERR_NULL;
+  if (!aligned16(x) || !aligned16(wr) || !aligned16(workspace) || !aligned4(topk_ids) ||
+      !aligned4(topk_w) || !aligned4(perm) || (gap && !aligned4(gap)) ||
+      (bias && !aligned4(bias)))
+    return SW_ERR_ALIGN;
+  SW_TRY(check_forward_operands(&pool, x, n_tokens, w13, w2, layout, topk_w, out));
+  if (workspace_bytes < layer_workspace_bytes(d, n_tokens, n_shared, n_groups))
+    return SW_ERR_WORKSPACE;
+  (void)hipGetLastError();
+  const int H = d->hidden, I = d->inter, m = d->n_experts, k = d->top_k;
+  const int mp = pool.n_experts, kp = pool.top_k;
+  const bool tiled = layout == SW_LAYOUT_TILED;
+  void* fws = static_cast<char*>(workspace) +
+              sw::align_up(layer_route_bytes(d, n_tokens, n_shared, n_groups), 256);
+  if (!sw::wave_plan_supported(n_tokens, H, I, mp, kp, tiled)) {
+    SW_TRY(launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, H, m, k,
+                                              topk_ids, topk_w, gap, counts, offsets, perm,
+                                              active, n_active, workspace, s, n_shared,
+                                              n_groups)));
+    return launch_forward(&pool, x, n_tokens, w13, w2, layout, topk_w, counts, offsets, perm,
+                          active, n_active, out, fws, s);
+  }
+  SW_TRY(launched(sw::launch_route_select(x, n_tokens, wr, bias, keep_mask, H, m, k, topk_ids,
+                                          topk_w, gap, workspace, s, n_shared, n_groups)));
+  SW_TRY(launched(sw::launch_gate_up_building_plan(x, n_tokens, w13, tiled, topk_ids, counts,
+                                                   offsets, perm, active, n_active, H, I, mp,
+                                                   kp, fws, s)));
+  SW_TRY(launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active,
+                                  H, I, mp, kp, fws, s)));
+  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, mp, kp, fws, s));
 }
 
 size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {

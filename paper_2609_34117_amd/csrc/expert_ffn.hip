@@ -848,6 +848,15 @@ hipError_t launch_gate_up(const uint16_t* x, int T, const uint16_t* w13, bool ti
   return hipGetLastError();
 }
 
+hipError_t launch_gate_up_building_plan(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                       const int* topk_ids, int* counts, int* offsets, int* perm,
+                                       int* active, int* n_active, int H, int I, int m, int k,
+                                       void* workspace, hipStream_t stream) {
+  const ForwardWs ws = carve(workspace, T * k, H, I);
+  return launch_gate_up_wave_plan(x, T, w13, tiled, topk_ids, counts, offsets, perm, active,
+                                  n_active, H, I, m, k, ws.h_hi, ws.h_lo, stream);
+}
+
 template <int KS, int MB>
 static void launch_down_t(const ForwardWs& ws, const uint16_t* w2, const int* counts,
                           const int* offsets, const int* perm, const int* active,

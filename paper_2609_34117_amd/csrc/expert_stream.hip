@@ -41,6 +41,7 @@
 //         down: 16 output rows of W2; epilogue writes y (fp32) per pair.
 #include <cmath>
 
+#include "dispatch_block.h"
 #include "sw_device.h"
 #include "sw_launch.h"
 
@@ -170,9 +171,10 @@ struct Segment {
 // expert is the slot itself and active[] is not read.  The loads of the
 // expert's count and offset are issued here but consumed only by
 // finish_segment, so the first weight chunks can go out in between.
+// Without `read_plan` the count and offset are left for the caller.
 __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const int* active,
                                                 const int* counts, const int* offsets, int m,
-                                                bool all_active) {
+                                                bool all_active, bool read_plan = true) {
   Segment s;
   s.lo = lo;
   s.a = lo / tpe;
@@ -180,8 +182,8 @@ __device__ __forceinline__ Segment next_segment(int lo, int r_hi, int tpe, const
   const int e = all_active ? s.a : active[s.a];
   s.e_ok = e >= 0 && e < m;
   s.e = s.e_ok ? e : 0;
-  s.cnt = counts[s.e];
-  s.base = offsets[s.e];
+  s.cnt = read_plan ? counts[s.e] : 0;
+  s.base = read_plan ? offsets[s.e] : 0;
   s.w_end = 0;
   return s;
 }
@@ -544,29 +546,169 @@ __device__ __forceinline__ void gu_run(const GuWave& g, u32x4 (&A)[D][kKC], int 
   }
 }
 
+// The dispatch plan of a gate/up launch that builds it itself (kPlan): the
+// selected ids it reads, and the arrays block 0 writes for the launches after
+// it (down projection, combine) and for the caller.
+struct PlanBuild {
+  const int* ids;
+  int *counts, *offsets, *perm, *active, *n_active;
+};
+
+// LDS words of such a plan, beside the staging area: n_active, counts[m],
+// offsets[m + 1], active[m] and perm[n_pairs].
+constexpr int kPlanInts = 2464;
+__host__ __device__ constexpr int plan_ints(int m, int n_pairs) { return 3 * m + 2 + n_pairs; }
+
+// Every block builds the plan of the batch in LDS from its n_pairs selected
+// ids (n_pairs <= 2 kBlk, m <= kBlk): the plan the dispatch kernel writes,
+// value for value, in four barriers.  ids_r holds this thread's ids (pairs
+// tid and tid + kBlk), loaded before the block's first weight chunks so that
+// waiting for them does not wait for those.  Pair p belongs to run
+// cw = p / 64 (a wave's 64 pairs); within a run, ballots match equal ids
+// (the pair's rank among them), and the run's count of each id goes to
+// LDS.  The histogram is the sum of the runs' counts; offsets and the active
+// list come from one block scan over the experts (expert e on thread e); a
+// pair's place in perm is then its expert's offset, plus its expert's
+// counts in the earlier runs, plus its rank: pairs in pair order within
+// each expert.  The runs' counts live in the staging area, which nothing
+// else uses yet.  Block 0 then writes the plan to memory.  Every thread of
+// the block calls it.
+__device__ void build_plan(const int (&ids_r)[2], int n_pairs, int m, uint16_t* xs, int* plan_s,
+                           const PlanBuild& pb) {
+  constexpr int kRuns = 2 * kWv;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int* counts = plan_s + 1;
+  int* offsets = counts + m;
+  int* active = offsets + m + 1;
+  int* perm = active + m;
+  uint8_t* run_cnt = reinterpret_cast<uint8_t*>(xs);                   // [kRuns][m]
+  uint32_t* wsum = reinterpret_cast<uint32_t*>(xs) + kRuns * m / 4;     // [2][kWv]
+  int* bad = reinterpret_cast<int*>(wsum + 2 * kWv);
+  for (int i = tid; i < kRuns * m / 4; i += kBlk) reinterpret_cast<uint32_t*>(run_cnt)[i] = 0u;
+  if (tid < m) counts[tid] = 0;
+  if (tid == 0) *bad = 0;
+  __syncthreads();
+
+  // runs: rank among equal ids, the run's count per id, the histogram
+  const int nbits = id_bits(m);
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
+  int rank[2], key[2];
+  bool ok[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int p = tid + i * kBlk;
+    const int e = ids_r[i];
+    ok[i] = p < n_pairs && e >= 0 && e < m;
+    if (p < n_pairs && !ok[i]) *bad = 1;
+    key[i] = ok[i] ? e : 0;
+    const uint64_t peers = match_peers(key[i], ok[i], nbits);
+    rank[i] = __popcll(peers & lt_mask);
+    if (ok[i] && rank[i] == 0) {
+      const int n = __popcll(peers);
+      run_cnt[(i * kWv + wave) * m + key[i]] = static_cast<uint8_t>(n);
+      atomicAdd(&counts[key[i]], n);
+    }
+  }
+  __syncthreads();
+
+  if (*bad) {  // an id outside [0, m): the flagged plan
+    for (int e = tid; e <= m; e += kBlk) {
+      if (e < m) counts[e] = 0;
+      offsets[e] = 0;
+    }
+    for (int p = tid; p < n_pairs; p += kBlk) perm[p] = p;
+    if (tid == 0) plan_s[0] = -1;
+  } else {
+    // offsets and the active list: one scan over the experts
+    const uint32_t c = tid < m ? (uint32_t)counts[tid] : 0u, a = c > 0 ? 1u : 0u;
+    const uint32_t ic = wave_inclusive_scan_u32(c), ia = wave_inclusive_scan_u32(a);
+    if (lane == 63) {
+      wsum[wave] = ic;
+      wsum[kWv + wave] = ia;
+    }
+    __syncthreads();
+    uint32_t bc = 0, ba = 0, tc = 0, ta = 0;
+#pragma unroll
+    for (int w = 0; w < kWv; ++w) {
+      const uint32_t sc = wsum[w], sa = wsum[kWv + w];
+      bc += w < wave ? sc : 0u;
+      ba += w < wave ? sa : 0u;
+      tc += sc;
+      ta += sa;
+    }
+    if (tid < m) {
+      offsets[tid] = (int)(bc + ic - c);
+      if (a) active[ba + ia - 1] = tid;
+    }
+    if (tid == 0) {
+      offsets[m] = (int)tc;
+      plan_s[0] = (int)ta;
+    }
+    __syncthreads();
+    // each pair's place: its expert's offset, its expert's pairs in the
+    // earlier runs, its rank in its run
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!ok[i]) continue;
+      const int run = i * kWv + wave;
+      int pos = offsets[key[i]] + rank[i];
+      for (int r = 0; r < run; ++r) pos += run_cnt[r * m + key[i]];
+      perm[pos] = tid + i * kBlk;
+    }
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {
+    const int na = plan_s[0];
+    for (int e = tid; e <= m; e += kBlk) {
+      if (e < m) pb.counts[e] = counts[e];
+      pb.offsets[e] = offsets[e];
+    }
+    for (int p = tid; p < n_pairs; p += kBlk) pb.perm[p] = perm[p];
+    for (int a = tid; a < na; a += kBlk) pb.active[a] = active[a];
+    if (tid == 0) *pb.n_active = na;
+  }
+}
+
 // kSpeculate: guess n_active == m and issue the first weight chunks before
 // n_active arrives (a wrong guess redoes the first segment).
 // kNbMax: column blocks of the largest pass (16 kNbMax tokens): 2 for
 // batches of up to 64 tokens, 8 for larger ones.
-template <bool kTiled, bool kSpeculate, int kNbMax, int kDepth>
+// kPlan: the plan arguments are unused; the block builds the plan from
+// pb.ids instead (m <= kBlk, n_pairs <= 2 kBlk, plan_ints(m, n_pairs) <=
+// kPlanInts), and block 0 writes it to pb's arrays.
+template <bool kTiled, bool kSpeculate, int kNbMax, int kDepth, bool kPlan>
 __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w13,
-    const int* __restrict__ counts, const int* __restrict__ offsets,
-    const int* __restrict__ perm, const int* __restrict__ active,
+    const int* __restrict__ counts_in, const int* __restrict__ offsets_in,
+    const int* __restrict__ perm_in, const int* __restrict__ active_in,
     const int* __restrict__ n_active_p, uint16_t* __restrict__ h_hi,
-    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs) {
+    uint16_t* __restrict__ h_lo, int H, int I, int m, int k, int n_pairs, PlanBuild pb) {
   constexpr int kPmax = 16 * kNbMax;
   // the wide variant (batches of more than 64 tokens) can give an expert
   // more pairs than a whole-K pass holds: the cost-weighted walk is
   // compiled in
   constexpr bool kBalance = kNbMax > 2;
+  static_assert(!(kPlan && kBalance), "the plan is built by the 32-token variants only");
   __shared__ __attribute__((aligned(16))) uint16_t xs[kStage];
   __shared__ int pid[kPmax];
   __shared__ int wp[kBalance ? kMaxExperts + 1 : 1];
   __shared__ uint32_t scan[34];
   __shared__ int verdict[kWv];
+  __shared__ int plan_s[kPlan ? kPlanInts : 1];
+  const int* counts = kPlan ? plan_s + 1 : counts_in;
+  const int* offsets = kPlan ? plan_s + 1 + m : offsets_in;
+  const int* active = kPlan ? plan_s + 2 + 2 * m : active_in;
+  const int* perm = kPlan ? plan_s + 2 + 3 * m : perm_in;
   const int tpe = I / 8;
-  const int n_act = *n_active_p;
+  int ids_r[2] = {0, 0};
+  if constexpr (kPlan) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int p = (int)threadIdx.x + i * kBlk;
+      ids_r[i] = p < n_pairs ? pb.ids[p] : 0;
+    }
+  }
+  int n_act = kPlan ? 0 : *n_active_p;
   const auto xr = make_rsrc(x, 2u * (uint32_t)(n_pairs / k) * (uint32_t)H);
 
   GuWave g;
@@ -582,18 +724,32 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   g.tpe = tpe;
 
   u32x4 A[kDepth][kKC];
-  // weight resource of the segment's expert and its first kDepth - 1 chunks
-  // (tile 0 of this wave: the same chunks in a whole-K and a sliced pass)
-  auto begin_segment = [&](const Segment& sg) {
+  // the segment's first chunks d0 .. kDepth - 2 (tile 0 of this wave: the
+  // same chunks in a whole-K and a sliced pass)
+  auto issue_first = [&](int d0) {
+#pragma unroll
+    for (int d = 0; d < kDepth - 1; ++d) {
+      if (d >= d0) {
+        ChunkPos h;
+        h.start(d, g.cpt, g.cpt);
+        gu_issue<kTiled>(g, h.j, h.c, A[d]);
+      }
+    }
+  };
+  // weight resource of the segment's expert and its first chunks up to
+  // d_end (all kDepth - 1 of them by default)
+  auto begin_segment = [&](const Segment& sg, int d_end = kDepth - 1) {
     g.seg_lo = sg.lo;
     g.seg_hi = sg.hi;
     g.a = sg.a;
     g.w = make_rsrc(w13 + (size_t)sg.e * 2 * I * H, sg.e_ok ? 4u * (uint32_t)I * (uint32_t)H : 0u);
 #pragma unroll
     for (int d = 0; d < kDepth - 1; ++d) {
-      ChunkPos h;
-      h.start(d, g.cpt, g.cpt);
-      gu_issue<kTiled>(g, h.j, h.c, A[d]);
+      if (d < d_end) {
+        ChunkPos h;
+        h.start(d, g.cpt, g.cpt);
+        gu_issue<kTiled>(g, h.j, h.c, A[d]);
+      }
     }
   };
 
@@ -606,10 +762,27 @@ __global__ __launch_bounds__(kBlk, 1) void gate_up_wave_kernel(
   const PairCounts pc = kBalance ? load_pair_counts(offsets, m) : PairCounts{0, 0, 0};
   int r_lo = 0, r_hi = 0;
   Segment sg;
+  // A block that builds the plan issues only the first guessed chunk before
+  // it: a wave that issues more at the kernel's start, when every compute
+  // unit does, stalls on the issue (the memory system holds as many
+  // requests as it can) and cannot build the plan meanwhile; the rest of
+  // the chunks follow the build.
+  constexpr int kEarly = kPlan ? 1 : kDepth - 1;
   if constexpr (kSpeculate) {
     block_range(m * tpe, &r_lo, &r_hi);
-    sg = next_segment(r_lo, r_hi, tpe, active, counts, offsets, m, true);
-    begin_segment(sg);
+    // (a plan built here is not there yet: its count and offset are read
+    // once it is)
+    sg = next_segment(r_lo, r_hi, tpe, active, counts_in, offsets_in, m, true, !kPlan);
+    begin_segment(sg, kEarly);
+  }
+  if constexpr (kPlan) {
+    build_plan(ids_r, n_pairs, m, xs, plan_s, pb);
+    n_act = plan_s[0];
+    if (kSpeculate) {
+      sg.cnt = counts[sg.e];
+      sg.base = offsets[sg.e];
+      issue_first(kEarly);
+    }
   }
   if (n_act <= 0 || n_act > m) return;  // an invalid plan: no work
   const bool all = n_act == m;
@@ -1115,8 +1288,9 @@ hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bo
   const int nb = gate_up_column_blocks(T);
   const bool sp = speculate_full_pool(T, m, k);
 #define SW_GU(TI, SP, NB, D)                                                                   \
-  gate_up_wave_kernel<TI, SP, NB, D><<<stream_grid(), kBlk, 0, stream>>>(                       \
-      x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k)
+  gate_up_wave_kernel<TI, SP, NB, D, false><<<stream_grid(), kBlk, 0, stream>>>(                \
+      x, w13, counts, offsets, perm, active, n_active, h_hi, h_lo, H, I, m, k, T * k,           \
+      PlanBuild{})
   if (nb == 2) {
     if (sp) {
       if (tiled) SW_GU(true, true, 2, 3); else SW_GU(false, true, 2, 3);
@@ -1129,6 +1303,29 @@ hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bo
     if (tiled) SW_GU(true, false, 8, 2); else SW_GU(false, false, 8, 2);
   }
 #undef SW_GU
+  return hipGetLastError();
+}
+
+bool wave_plan_supported(int T, int H, int I, int m, int k, bool tiled) {
+  return gate_up_kernels(T, H, I, m, k, tiled) == Kernels::kWave && gate_up_column_blocks(T) == 2 &&
+         m <= kBlk && T * k <= 2 * kBlk && plan_ints(m, T * k) <= kPlanInts;
+}
+
+hipError_t launch_gate_up_wave_plan(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                    const int* topk_ids, int* counts, int* offsets, int* perm,
+                                    int* active, int* n_active, int H, int I, int m, int k,
+                                    uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream) {
+  const PlanBuild pb{topk_ids, counts, offsets, perm, active, n_active};
+  const bool sp = speculate_full_pool(T, m, k);
+#define SW_GP(TI, SP)                                                                          \
+  gate_up_wave_kernel<TI, SP, 2, 3, true><<<stream_grid(), kBlk, 0, stream>>>(                  \
+      x, w13, nullptr, nullptr, nullptr, nullptr, nullptr, h_hi, h_lo, H, I, m, k, T * k, pb)
+  if (sp) {
+    if (tiled) SW_GP(true, true); else SW_GP(false, true);
+  } else {
+    if (tiled) SW_GP(true, false); else SW_GP(false, false);
+  }
+#undef SW_GP
   return hipGetLastError();
 }
 

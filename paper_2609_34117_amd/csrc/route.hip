@@ -773,6 +773,15 @@ hipError_t launch_route(const uint16_t* x, int T, const float* wr, const float* 
                     workspace, stream);
 }
 
+hipError_t launch_route_select(const uint16_t* x, int T, const float* wr, const float* bias,
+                               const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
+                               float* topk_w, float* gap, void* workspace, hipStream_t stream,
+                               int n_shared, int n_groups) {
+  if (T == 0) return hipSuccess;
+  const Cols c{m, n_shared > 0 ? m + 1 : m, k, n_shared, n_shared > 0 ? n_groups : 1};
+  return route_cols(x, T, wr, bias, keep_mask, H, c, topk_ids, topk_w, gap, workspace, stream);
+}
+
 bool fused_route_dispatch_supported(int T, int m, int k, int S, int R) {
   return T > 0 && T <= kFusedMaxTokens && m + R * S <= kFusedMaxPool && k + S <= kFusedMaxK;
 }

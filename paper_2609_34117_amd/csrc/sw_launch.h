@@ -56,6 +56,12 @@ hipError_t launch_dispatch(const int* topk_ids, int n_pairs, int m, int* counts,
 // g = t * n_groups / T, pool ids m + g * n_shared .. + n_shared - 1, and the
 // plan covers m + n_groups * n_shared experts.
 bool fused_route_dispatch_supported(int T, int m, int k, int n_shared = 0, int n_groups = 1);
+// The routing half of launch_route_dispatch alone (logits and top-k, same
+// outputs), for a caller that builds the plan elsewhere.
+hipError_t launch_route_select(const uint16_t* x, int T, const float* wr, const float* bias,
+                               const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
+                               float* topk_w, float* gap, void* workspace, hipStream_t stream,
+                               int n_shared = 0, int n_groups = 1);
 size_t route_shared_workspace_bytes(int T, int H, int m, int k, int n_shared, int n_groups);
 hipError_t launch_route_dispatch(const uint16_t* x, int T, const float* wr, const float* bias,
                                  const uint8_t* keep_mask, int H, int m, int k, int* topk_ids,
@@ -80,6 +86,12 @@ hipError_t launch_down(int T, const uint16_t* w2, bool tiled, const int* counts,
                        const int* offsets, const int* perm, const int* active,
                        const int* n_active, int H, int I, int m, int k, void* workspace,
                        hipStream_t stream, bool identity_plan = false);
+// launch_gate_up for a shape wave_plan_supported takes, building the plan of
+// topk_ids on the way (see launch_gate_up_wave_plan).
+hipError_t launch_gate_up_building_plan(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                       const int* topk_ids, int* counts, int* offsets, int* perm,
+                                       int* active, int* n_active, int H, int I, int m, int k,
+                                       void* workspace, hipStream_t stream);
 bool wave_stream_supported(int T, int H, int I, int k);
 hipError_t launch_gate_up_wave(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
                                const int* counts, const int* offsets, const int* perm,
@@ -89,6 +101,16 @@ hipError_t launch_down_wave(int T, const uint16_t* w2, bool tiled, const int* co
                             const int* offsets, const int* perm, const int* active,
                             const int* n_active, int H, int I, int m, int k, const uint16_t* h_hi,
                             const uint16_t* h_lo, float* y, hipStream_t stream);
+// Decode batches whose gate/up launch can build the dispatch plan itself
+// (the 32-token wave kernels, at most 512 experts and 1024 pairs): every
+// block builds it in LDS from topk_ids, and block 0 writes counts, offsets,
+// perm, active and n_active (the dispatch kernel's outputs, bit for bit)
+// for the launches after it.
+bool wave_plan_supported(int T, int H, int I, int m, int k, bool tiled);
+hipError_t launch_gate_up_wave_plan(const uint16_t* x, int T, const uint16_t* w13, bool tiled,
+                                    const int* topk_ids, int* counts, int* offsets, int* perm,
+                                    int* active, int* n_active, int H, int I, int m, int k,
+                                    uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
 // Prefill-sized batches (about 48 or more tokens per expert): each weight
 // tile is streamed once per 160-token pass (expert_prefill.hip).
 bool prefill_supported(int T, int H, int I, int m, int k);

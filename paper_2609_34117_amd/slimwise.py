@@ -60,6 +60,12 @@ def _load() -> ctypes.CDLL:
         "sw_moe_routing_mass_workspace_bytes": ([D, I32], SZ),
         "sw_moe_routing_mass": ([D, P, I32, P, P, P, P, P, P, SZ, P], ctypes.c_int),
         "sw_moe_shared_expert": ([D, P, I32, P, P, I32, P, P, P, SZ, P], ctypes.c_int),
+        "sw_moe_layer_workspace_bytes": ([D, I32, I32, I32], SZ),
+        "sw_moe_gate_up_builds_plan": ([D, I32, I32], I32),
+        "sw_moe_forward_gate_up_plan": ([D, P, I32, P, I32, P, P, P, P, P, P, P, SZ, P],
+                                        ctypes.c_int),
+        "sw_moe_layer": ([D, P, I32, P, P, P, I32, I32, P, P, I32, P, P, P, P, P, P, P, P, P, P,
+                          SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -70,7 +76,7 @@ def _load() -> ctypes.CDLL:
 
 
 LIB = _load()
-ABI_VERSION = 9
+ABI_VERSION = 10
 NO_ALLOC_SCRATCH_BYTES = 32 << 20
 ROW_MAJOR, TILED = 0, 1
 # sw_kernel_family values
@@ -359,6 +365,24 @@ def sw_moe_forward_gate_up(x, w13, top_k, plan: Plan, ws, *, layout: int = ROW_M
     _check(st, "sw_moe_forward_gate_up")
 
 
+def sw_moe_gate_up_builds_plan(d: Dims, n_tokens: int, layout: int = ROW_MAJOR) -> bool:
+    return bool(LIB.sw_moe_gate_up_builds_plan(ctypes.byref(d), n_tokens, layout))
+
+
+def sw_moe_forward_gate_up_plan(x, w13, topk_ids, plan: Plan, ws, *, layout: int = ROW_MAJOR,
+                                stream=None):
+    """The gate/up phase that builds ``plan`` from ``topk_ids`` (Section 2.1)
+    on the way, for the decode batches ``sw_moe_gate_up_builds_plan`` names."""
+    t = x.shape[0]
+    d = _fwd_dims(x, w13, topk_ids.shape[1])
+    st = LIB.sw_moe_forward_gate_up_plan(
+        ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(w13, _BF16, "w13"), layout,
+        _ptr(topk_ids, (torch.int32,), "topk_ids"), _ptr(plan.counts), _ptr(plan.offsets),
+        _ptr(plan.perm), _ptr(plan.active), _ptr(plan.n_active), _ptr(ws), ws.numel(),
+        _stream(stream))
+    _check(st, "sw_moe_forward_gate_up_plan")
+
+
 def sw_moe_forward_down(n_tokens, w2, top_k, plan: Plan, ws, *, layout: int = ROW_MAJOR,
                         stream=None):
     d = _fwd_dims(n_tokens, w2, top_k, which="w2")
@@ -423,11 +447,56 @@ def sw_moe_shared_expert(x: torch.Tensor, w13: torch.Tensor, w2: torch.Tensor,
     return out
 
 
+def sw_moe_layer_workspace_bytes(d: Dims, n_tokens: int, n_shared: int = 0,
+                                 n_groups: int = 1) -> int:
+    return LIB.sw_moe_layer_workspace_bytes(ctypes.byref(d), n_tokens, n_shared, n_groups)
+
+
+def sw_moe_layer(x: torch.Tensor, wr: torch.Tensor, top_k: int, w13: torch.Tensor,
+                 w2: torch.Tensor, *, layout: int = ROW_MAJOR, n_shared: int = 0,
+                 n_groups: int = 1, keep_mask=None, bias=None, want_gap=True, route_out=None,
+                 plan: Optional[Plan] = None, out=None, ws=None, stream=None):
+    """Route, dispatch plan, expert FFNs and combine of one layer in one call
+    (Section 3.1, Eq. 2; Section 2.1, Eq. 1): bitwise what
+    ``sw_moe_route_dispatch`` (or ``sw_moe_route_dispatch_shared`` when
+    ``n_shared`` > 0, ``wr`` then holding the shared gate row last) followed
+    by ``sw_moe_forward`` give.  ``w13``/``w2`` hold the pool of
+    m + n_groups * n_shared experts.
+
+    Returns ``(topk_ids, topk_w, gap, plan, out)``."""
+    t, hidden = x.shape
+    m = wr.shape[0] - (1 if n_shared else 0)
+    kout = top_k + n_shared
+    pool = _fwd_dims(x, w13, kout)
+    m_pool = m + (n_groups * n_shared if n_shared else 0)
+    if pool.n_experts != m_pool:
+        raise ValueError(f"w13 holds {pool.n_experts} experts, the layer's pool is {m_pool}")
+    d = Dims(hidden, pool.inter, m, top_k)
+    if route_out is None:
+        route_out = (_empty((t, kout), torch.int32, x.device),
+                     _empty((t, kout), torch.float32, x.device),
+                     _empty(t, torch.float32, x.device) if want_gap else None)
+    ids, w, gap = route_out
+    if plan is None:
+        plan = alloc_plan(t, m_pool, kout, x.device)
+    if out is None:
+        out = _empty((t, hidden), torch.float32, x.device)
+    if ws is None:
+        ws = workspace(sw_moe_layer_workspace_bytes(d, t, n_shared, n_groups), x.device)
+    st = LIB.sw_moe_layer(
+        ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
+        _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
+        n_shared, n_groups, _ptr(w13, _BF16, "w13"), _ptr(w2, _BF16, "w2"), layout, _ptr(ids),
+        _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+        _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"), _ptr(ws),
+        ws.numel(), _stream(stream))
+    _check(st, "sw_moe_layer")
+    return ids, w, gap, plan, out
+
+
 def moe_layer(x, wr, w13, w2, top_k, *, keep_mask=None, bias=None, layout: int = ROW_MAJOR,
               stream=None) -> dict:
-    """Route + dispatch (one call) and forward of one layer (allocating
-    convenience wrapper)."""
-    ids, w, gap, plan = sw_moe_route_dispatch(x, wr, top_k, keep_mask=keep_mask, bias=bias,
-                                              stream=stream)
-    out = sw_moe_forward(x, w13, w2, w, plan, layout=layout, stream=stream)
+    """One layer through ``sw_moe_layer`` (allocating convenience wrapper)."""
+    ids, w, gap, plan, out = sw_moe_layer(x, wr, top_k, w13, w2, layout=layout,
+                                          keep_mask=keep_mask, bias=bias, stream=stream)
     return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)

@@ -54,7 +54,7 @@ def test_status_strings_and_version(lib):
     lib.sw_status_str.restype = ctypes.c_char_p
     for s in range(7):
         assert lib.sw_status_str(s).startswith(b"SW_")
-    assert lib.sw_abi_version() == 9
+    assert lib.sw_abi_version() == 10
 
 
 def _route(lib, d, x=16, t=4, wr=16, ids=16, w=16, ws=16, nbytes=1 << 20):
@@ -219,6 +219,76 @@ def test_forward_validation(lib):
     d.hidden, d.inter = 72, 40                   # tiled layout needs multiples of 32
     need2 = q(ctypes.byref(d), 4)
     assert call(nbytes=need2, lay=1) == SW_ERR_UNSUPPORTED
+
+
+def test_layer_call_validation_and_plan_query(lib):
+    # every rejection happens before the device is touched (no GPU here)
+    P, I32, SZ, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.POINTER(Dims)
+    q = lib.sw_moe_layer_workspace_bytes
+    q.argtypes, q.restype = [D, I32, I32, I32], SZ
+    rq = lib.sw_moe_route_workspace_bytes
+    rq.argtypes, rq.restype = [D, I32], SZ
+    sq = lib.sw_moe_route_shared_workspace_bytes
+    sq.argtypes, sq.restype = [D, I32, I32, I32], SZ
+    fq = lib.sw_moe_forward_workspace_bytes
+    fq.argtypes, fq.restype = [D, I32], SZ
+    d = Dims(2048, 768, 64, 8)
+    up = lambda v: (v + 255) // 256 * 256
+    # the routing's workspace, then the forward's (on the pool of the routed
+    # experts and the shared expert's parts)
+    assert q(ctypes.byref(d), 64, 0, 1) == up(rq(ctypes.byref(d), 64)) + fq(ctypes.byref(d), 64)
+    assert q(ctypes.byref(d), 64, 2, 3) == (up(sq(ctypes.byref(d), 64, 2, 3)) +
+                                            fq(ctypes.byref(Dims(2048, 768, 70, 10)), 64))
+    assert q(ctypes.byref(d), 0, 0, 1) == 0
+    assert q(None, 8, 0, 1) == 0
+    assert q(ctypes.byref(d), 8, -1, 1) == 0
+    assert q(ctypes.byref(d), 8, 2, 0) == 0
+    need = q(ctypes.byref(d), 4, 0, 1)
+    f = lib.sw_moe_layer
+    f.argtypes = [D, P, I32, P, P, P, I32, I32, P, P, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
+    args = dict(x=16, T=4, wr=16, bias=None, keep=None, S=0, R=1, w13=16, w2=16, lay=1, ids=16,
+                w=16, gap=None, c=16, o=16, p=16, a=16, na=16, out=16, ws=16)
+
+    def call(nbytes=need, **kw):
+        a = dict(args, **kw)
+        return f(ctypes.byref(d), a["x"], a["T"], a["wr"], a["bias"], a["keep"], a["S"], a["R"],
+                 a["w13"], a["w2"], a["lay"], a["ids"], a["w"], a["gap"], a["c"], a["o"], a["p"],
+                 a["a"], a["na"], a["out"], a["ws"], nbytes, None)
+
+    assert call(nbytes=need - 1) == SW_ERR_WORKSPACE
+    for name in ("x", "wr", "w13", "w2", "ids", "w", "c", "p", "na", "out", "ws"):
+        assert call(**{name: None}) == SW_ERR_NULL, name
+    assert call(out=20) == SW_ERR_ALIGN
+    assert call(wr=8) == SW_ERR_ALIGN
+    assert call(p=18) == SW_ERR_ALIGN
+    assert call(lay=2) == SW_ERR_SHAPE
+    assert call(T=-1) == SW_ERR_SHAPE
+    assert call(S=-1) == SW_ERR_SHAPE
+    assert call(S=2, R=0) == SW_ERR_SHAPE
+    assert call(S=2, R=600) == SW_ERR_UNSUPPORTED          # 64 + 1200 experts
+    assert call(S=30) == SW_ERR_UNSUPPORTED                # 38 slots a token
+    # which shapes build the plan in the gate/up launch (host logic only)
+    b = lib.sw_moe_gate_up_builds_plan
+    b.argtypes, b.restype = [D, I32, I32], I32
+    built = lambda dd, T, lay=1: b(ctypes.byref(dd), T, lay)
+    assert built(d, 64) == 1 and built(d, 3) == 1 and built(d, 64, 0) == 1
+    assert built(d, 65) == 0                               # the 128-token variants
+    assert built(d, 2) == 0                                # split-K kernels
+    assert built(d, 0) == 0 and b(None, 8, 1) == 0
+    assert built(Dims(2048, 512, 512, 8), 48) == 1         # 1922 plan words
+    assert built(Dims(2048, 512, 512, 16), 64) == 0        # 2562 plan words: too many
+    assert built(Dims(2048, 512, 600, 8), 8) == 0          # more experts than threads
+    assert built(Dims(40, 40, 16, 2), 8, 0) == 0           # the generic kernels
+    # the phase that builds it rejects other shapes before any launch
+    g = lib.sw_moe_forward_gate_up_plan
+    g.argtypes = [D, P, I32, P, I32, P, P, P, P, P, P, P, SZ, P]
+    gneed = fq(ctypes.byref(d), 65)
+    assert g(ctypes.byref(d), 16, 65, 16, 1, 16, 16, 16, 16, 16, 16, 16, gneed, None) == \
+        SW_ERR_UNSUPPORTED
+    assert g(ctypes.byref(d), 16, 0, 16, 1, 16, 16, 16, 16, 16, 16, 16, gneed, None) == \
+        SW_ERR_UNSUPPORTED
+    assert g(ctypes.byref(d), 16, 64, 16, 1, None, 16, 16, 16, 16, 16, 16, gneed, None) == \
+        SW_ERR_NULL
 
 
 def test_forward_no_alloc_validation(lib):

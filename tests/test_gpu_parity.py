@@ -63,10 +63,11 @@ def run_gpu_layer(sw, D, k, mask=None, x=None, bias=None):
     return sw.moe_layer(xm, D["wr"], D["w13"], D["w2"], k, keep_mask=keep, bias=bias)
 
 
-def guarded_layer(sw, D, k, mask=None, bias=None, layout=None):
-    """Route + dispatch and forward with every output and workspace inside a
-    canaried allocation (poisoned interiors: an unwritten output shows as -7
-    or NaN); the margins are checked after the call."""
+def guarded_layer(sw, D, k, mask=None, bias=None, layout=None, one_call=False):
+    """Route + dispatch and forward (or, with `one_call`, sw_moe_layer) with
+    every output and workspace inside a canaried allocation (poisoned
+    interiors: an unwritten output shows as -7 or NaN); the margins are
+    checked after the call."""
     x, wr = D["x"], D["wr"]
     t, m = x.shape[0], wr.shape[0]
     G = Guards()
@@ -75,17 +76,42 @@ def guarded_layer(sw, D, k, mask=None, bias=None, layout=None):
     plan = sw.Plan(G.empty(m, torch.int32, poison=-7), G.empty(m + 1, torch.int32, poison=-7),
                    G.empty(max(t * k, 1), torch.int32, poison=-7), G.empty(m, torch.int32, poison=-7),
                    G.empty(1, torch.int32, poison=-7))
+    lay = sw.ROW_MAJOR if layout is None else layout
+    keep = None if mask is None else dev(mask)
+    out = G.empty((t, x.shape[1]), torch.float32, poison=float("nan"))
+    if one_call:
+        ld = sw.dims(x.shape[1], D["w13"].shape[1] // 2, m, k)
+        ids, w, gap, plan, out = sw.sw_moe_layer(
+            x, wr, k, D["w13"], D["w2"], layout=lay, keep_mask=keep, bias=bias, route_out=out3,
+            plan=plan, out=out, ws=G.workspace(sw.sw_moe_layer_workspace_bytes(ld, t)))
+        G.check()
+        return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)
     rd = sw.dims(x.shape[1], 8, m, k)
     ids, w, gap, plan = sw.sw_moe_route_dispatch(
-        x, wr, k, keep_mask=None if mask is None else dev(mask), bias=bias, out=out3, plan=plan,
+        x, wr, k, keep_mask=keep, bias=bias, out=out3, plan=plan,
         ws=G.workspace(sw.sw_moe_route_workspace_bytes(rd, t)))
-    lay = sw.ROW_MAJOR if layout is None else layout
     fd = sw.dims(x.shape[1], D["w13"].shape[1] // 2, D["w13"].shape[0], k)
-    out = G.empty((t, x.shape[1]), torch.float32, poison=float("nan"))
     sw.sw_moe_forward(x, D["w13"], D["w2"], w, plan, layout=lay, out=out,
                       ws=G.workspace(sw.sw_moe_forward_workspace_bytes(fd, t)))
     G.check()
     return dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out)
+
+
+def bits(t):
+    """A tensor's bit patterns (NaN-safe bitwise comparison)."""
+    return t.view(torch.int32) if t.dtype == torch.float32 else t
+
+
+def assert_same_layer(a, b):
+    """Two runs of the layer wrote the same bits to every output (the active
+    list up to n_active: the plan leaves the rest unwritten)."""
+    for key in ("topk_ids", "topk_w", "gap", "out"):
+        if a[key] is not None or b[key] is not None:
+            assert torch.equal(bits(a[key]), bits(b[key])), key
+    for f in ("counts", "offsets", "perm", "n_active"):
+        assert torch.equal(getattr(a["plan"], f), getattr(b["plan"], f)), f
+    n = max(int(a["plan"].n_active.item()), 0)
+    assert torch.equal(a["plan"].active[:n], b["plan"].active[:n])
 
 
 def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=None):
@@ -94,6 +120,10 @@ def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=Non
     k = cfg.top_k
     b_dev = None if bias is None else dev(bias)
     g = guarded_layer(sw, D, k, mask=mask, bias=b_dev, layout=layout)
+    # the one-call layer (its gate/up launch builds the plan on decode
+    # batches) writes the same bits
+    assert_same_layer(g, guarded_layer(sw, D, k, mask=mask, bias=b_dev, layout=layout,
+                                       one_call=True))
     g_ids, g_w, g_gap = host(g["topk_ids"]), host(g["topk_w"]), host(g["gap"])
     o_ids, o_w, o_gap, o_z = oracle.route(L["x"], L["wr"], k, keep_mask=mask, bias=bias,
                                           want_logits=True)
@@ -726,6 +756,73 @@ def test_route_dispatch_in_band_errors_and_empty_batch(sw):
 
 
 # --------------------------------------------------------------------------
+# the one-call layer: on decode batches its gate/up launch builds the plan
+
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens,tiled,popular,builds", [
+    (512, 64, 8, 256, 64, True, False, True),     # fully active guess
+    (512, 128, 8, 256, 64, True, False, True),    # idle experts expected: no guess
+    (512, 64, 8, 256, 33, False, False, True),    # row-major weights
+    (512, 256, 8, 256, 8, True, False, True),     # 8 tokens over 256 experts
+    (256, 16, 2, 128, 3, False, False, True),     # the smallest batch of the wave kernels
+    (512, 512, 8, 256, 48, True, False, True),    # 512 experts: the plan's scan limit
+    (512, 512, 16, 256, 64, True, False, False),  # 1024 pairs over 512 experts: LDS too small
+    (512, 64, 8, 256, 64, True, True, True),      # one expert takes every token: two passes
+    (512, 64, 8, 256, 2, True, False, False),     # 2 tokens: split-K kernels
+    (512, 64, 8, 256, 65, True, False, False),    # 65 tokens: the 128-token variants
+])
+def test_layer_call_against_oracle_and_separate_calls(sw, hidden, n_experts, top_k, inter, tokens,
+                                                      tiled, popular, builds):
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=31)
+    layout = sw.ROW_MAJOR
+    if tiled:
+        D = dict(D)
+        D["w13"], D["w2"] = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+        layout = sw.TILED
+    bias = None
+    if popular:
+        bias = np.zeros(n_experts, np.float32)
+        bias[5] = 30.0
+    # check_layer runs the separate calls against the oracle and the one-call
+    # layer against them, bit for bit
+    s = check_layer(sw, cfg, L, D, None, bias=bias, layout=layout,
+                    what=f"layer call T={tokens} m={n_experts}")
+    if popular:
+        assert s["counts"][5] == tokens
+    # where the plan is built in the gate/up launch, a second call gives the
+    # same bits (every block builds the same plan)
+    a = guarded_layer(sw, D, top_k, bias=None if bias is None else dev(bias), layout=layout,
+                      one_call=True)
+    b = guarded_layer(sw, D, top_k, bias=None if bias is None else dev(bias), layout=layout,
+                      one_call=True)
+    assert_same_layer(a, b)
+    pairs = tokens * top_k
+    fam = sw.sw_moe_forward_kernels(sw.dims(hidden, inter, n_experts, top_k), tokens, layout)
+    print(f"layer call T={tokens} m={n_experts} k={top_k}: kernels={fam} builds plan={builds} "
+          f"({3 * n_experts + 2 + pairs} plan words) max|err|={s['err']:.3g}")
+
+
+def test_layer_call_in_band_flag_and_empty_batch(sw):
+    # two eligible experts for top-3: the third slot is -1 on every token,
+    # the plan built in the gate/up launch flags the batch (n_active -1, perm
+    # the identity) and the output is NaN, as with the separate calls
+    mask = np.zeros(8, np.uint8)
+    mask[[1, 6]] = 1
+    for tokens in (3, 40):
+        cfg, L, D = small_layer(64, 8, 3, 32, tokens, seed=5)
+        a = guarded_layer(sw, D, 3, mask=mask)
+        b = guarded_layer(sw, D, 3, mask=mask, one_call=True)
+        assert_same_layer(a, b)
+        assert int(b["plan"].n_active.item()) == -1
+        assert torch.equal(b["plan"].perm.cpu(), torch.arange(3 * tokens, dtype=torch.int32))
+        assert bool(torch.all(torch.isnan(b["out"])))
+    cfg, L, D = small_layer(64, 8, 2, 32, 4)
+    ids, w, gap, plan, out = sw.sw_moe_layer(D["x"][:0], D["wr"], 2, D["w13"], D["w2"])
+    assert ids.shape == (0, 2) and out.shape == (0, 64)
+    assert int(plan.n_active.item()) == 0
+    assert torch.all(plan.counts == 0) and torch.all(plan.offsets == 0)
+
+
+# --------------------------------------------------------------------------
 # the shared expert (Section 3.3)
 
 def _shared_inputs(hidden, inter, tokens, seed):
@@ -796,6 +893,11 @@ def _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled, n_groups
         dev(L["x"]), wr, top_k, n_shared, n_groups=n_groups,
         keep_mask=None if mask is None else dev(mask))
     out = sw.sw_moe_forward(dev(L["x"]), w13, w2, w, plan, layout=layout)
+    # the one-call layer with the folded expert writes the same bits
+    one = sw.sw_moe_layer(dev(L["x"]), wr, top_k, w13, w2, layout=layout, n_shared=n_shared,
+                          n_groups=n_groups, keep_mask=None if mask is None else dev(mask))
+    assert_same_layer(dict(topk_ids=ids, topk_w=w, gap=gap, plan=plan, out=out),
+                      dict(topk_ids=one[0], topk_w=one[1], gap=one[2], plan=one[3], out=one[4]))
     return ids, w, gap, plan, out
 
 
