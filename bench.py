@@ -147,8 +147,6 @@ class Runner:
         fd = sw.dims(H, Iw, self.m_plan, self.kout)
         self.fws = sw.workspace(sw.sw_moe_forward_workspace_bytes(fd, T), dev)
         self.lws = sw.workspace(sw.sw_moe_layer_workspace_bytes(d, T, S, pool.n_groups), dev)
-        # decode batches: the step's gate/up launch builds the plan itself
-        self.builds = sw.sw_moe_gate_up_builds_plan(fd, T, pool.layout)
         self.sws = None
         if pool.shared is not None:
             ds = sw.dims(H, pool.shared[1].shape[-1], 1, 1)
@@ -166,45 +164,50 @@ class Runner:
             sw.sw_moe_route_dispatch(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
                                      out=(self.ids, self.w, self.gap), plan=plan, ws=self.rws)
 
-    def plan_for(self, x):
-        """The routed ids and a dispatch plan of their own for batch `x`
-        (route + dispatch)."""
-        plan = self.sw.alloc_plan(self.T, self.m_plan, self.kout, x.device)
-        self.route(x, plan)
-        return self.ids.clone(), plan
+    def layer(self, x, c, phase=None, bufs=None):
+        """sw_moe_layer on batch `x` and pool copy `c` (one phase of it
+        with `phase`), into this runner's buffers or `bufs` (a tuple of
+        ids, w, gap, plan, out, workspace)."""
+        sw, p = self.sw, self.pool
+        ids, w, gap, plan, out, ws = bufs or (self.ids, self.w, self.gap, self.plan, self.out,
+                                             self.lws)
+        sw.sw_moe_layer(x, p.wr, self.cfg.top_k, p.w13[c], p.w2[c], layout=p.layout,
+                        n_shared=p.n_shared, n_groups=p.n_groups, bias=p.bias,
+                        keep_mask=p.keep_mask, route_out=(ids, w, gap), plan=plan, out=out,
+                        ws=ws, phase=phase)
+
+    def buffers(self):
+        """A set of layer buffers of its own (ids, w, gap, plan, out, workspace)."""
+        t, dev = self.torch, self.out.device
+        return (t.empty_like(self.ids), t.empty_like(self.w), t.empty_like(self.gap),
+                self.sw.alloc_plan(self.T, self.m_plan, self.kout, dev), t.empty_like(self.out),
+                t.empty_like(self.lws))
 
     def step(self, x, c, ev=None):
-        """One layer step.  Whole steps (ev None) are one sw_moe_layer call
-        (with a separate shared expert, route + dispatch, the forward and
-        the shared expert's call).  With ev, the same kernels with events
-        between the forward's phases: the routing (and, where the gate/up
-        launch does not build it, the dispatch), then gate/up, down and
-        combine."""
+        """One layer step: one sw_moe_layer call (with a separate shared
+        expert, route + dispatch, the forward and the shared expert's call).
+        With ev, the layer's four phases with events between them: the
+        routing, then gate/up, down and combine."""
         sw, p = self.sw, self.pool
-        if ev is None:
-            if p.shared is None:
-                sw.sw_moe_layer(x, p.wr, self.cfg.top_k, p.w13[c], p.w2[c], layout=p.layout,
-                                n_shared=p.n_shared, n_groups=p.n_groups, bias=p.bias,
-                                keep_mask=p.keep_mask, route_out=(self.ids, self.w, self.gap),
-                                plan=self.plan, out=self.out, ws=self.lws)
+        if p.shared is None:
+            if ev is None:
+                self.layer(x, c)
                 return
+            self.layer(x, c, phase=0)
+            for i in range(3):
+                ev[i].record()
+                self.layer(x, c, phase=i + 1)
+            ev[3].record()
+            return
+        if ev is None:
             self.route(x, self.plan)
             sw.sw_moe_forward(x, p.w13[c], p.w2[c], self.w, self.plan, layout=p.layout,
                               out=self.out, ws=self.fws)
             sw.sw_moe_shared_expert(x, *p.shared, self.out, layout=p.layout, ws=self.sws)
             return
-        plan_in_gate_up = self.builds and not p.n_shared
-        if plan_in_gate_up:
-            sw.sw_moe_route(x, p.wr, self.cfg.top_k, bias=p.bias, keep_mask=p.keep_mask,
-                            out=(self.ids, self.w, self.gap), ws=self.rws)
-        else:
-            self.route(x, self.plan)
+        self.route(x, self.plan)
         ev[0].record()
-        if plan_in_gate_up:
-            sw.sw_moe_forward_gate_up_plan(x, p.w13[c], self.ids, self.plan, self.fws,
-                                           layout=p.layout)
-        else:
-            sw.sw_moe_forward_gate_up(x, p.w13[c], self.kout, self.plan, self.fws, layout=p.layout)
+        sw.sw_moe_forward_gate_up(x, p.w13[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[1].record()
         sw.sw_moe_forward_down(self.T, p.w2[c], self.kout, self.plan, self.fws, layout=p.layout)
         ev[2].record()
@@ -275,24 +278,34 @@ def time_graph(torch, r: Runner, xs, reps):
 def time_kernels(torch, r: Runner, xs, steps):
     """Mean launch duration of gate_up and of down: `steps` launches of one
     kernel back to back between two HIP events on the launch stream, rotating
-    the batches (each with its own ids and plan) and the pool copies.  The
-    gate_up launch is the step's: on decode batches it builds the plan from
-    the ids on the way.  (The small kernels are shorter than a host call, so
-    their durations come from the kernel trace instead.)"""
+    the batches (each with layer buffers of its own, routed once) and the
+    pool copies.  Each is the step's own launch: phase 1 and phase 2 of
+    sw_moe_layer (on decode batches the gate/up launch selects the experts
+    and builds the plan on the way).  (The small kernels are shorter than a
+    host call, so their durations come from the kernel trace instead.)"""
     sw, p, k = r.sw, r.pool, r.kout
-    routed = [r.plan_for(x) for x in xs]
+    if p.shared is None:
+        bufs = [r.buffers() for _ in xs]
+        for j, x in enumerate(xs):
+            r.layer(x, 0, phase=0, bufs=bufs[j])
+            r.layer(x, 0, phase=1, bufs=bufs[j])
+    else:
+        plans = []
+        for x in xs:
+            plan = sw.alloc_plan(r.T, r.m_plan, r.kout, x.device)
+            r.route(x, plan)
+            plans.append(plan)
     torch.cuda.synchronize()
     out = {}
 
     def launch(name, s):
         j, c = s % len(xs), s % N_COPIES
-        ids, plan = routed[j]
-        if name == "down":
-            sw.sw_moe_forward_down(r.T, p.w2[c], k, plan, r.fws, layout=p.layout)
-        elif r.builds and p.shared is None:
-            sw.sw_moe_forward_gate_up_plan(xs[j], p.w13[c], ids, plan, r.fws, layout=p.layout)
+        if p.shared is None:
+            r.layer(xs[j], c, phase=1 if name == "gate_up" else 2, bufs=bufs[j])
+        elif name == "down":
+            sw.sw_moe_forward_down(r.T, p.w2[c], k, plans[j], r.fws, layout=p.layout)
         else:
-            sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plan, r.fws, layout=p.layout)
+            sw.sw_moe_forward_gate_up(xs[j], p.w13[c], k, plans[j], r.fws, layout=p.layout)
 
     for name in ("gate_up", "down"):
         for s in range(4):

@@ -428,6 +428,24 @@ sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
                        int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
                        float* out, void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * One of the four phases of sw_moe_layer, for callers that time them or
+ * interleave other work: calling phases 0, 1, 2, 3 in order with the same
+ * arguments is sw_moe_layer.  Phase 0 routes (plus the dispatch where the
+ * gate/up launch does not build the plan), 1 is the gate/up launch, 2 the
+ * down projection, 3 the combine.  The phases communicate through `workspace` and the plan
+ * arrays.  Arguments, errors and outputs as sw_moe_layer; a phase outside
+ * 0..3 is SW_ERR_SHAPE; with T = 0 phase 0 writes the empty plan and the
+ * others do nothing.
+ */
+sw_status sw_moe_layer_phase(int32_t phase, const sw_moe_dims* d, const uint16_t* x,
+                             int32_t n_tokens, const float* wr, const float* bias,
+                             const uint8_t* keep_mask, int32_t n_shared, int32_t n_groups,
+                             const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                             int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                             int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
+                             float* out, void* workspace, size_t workspace_bytes, void* stream);
+
 /* Workspace bytes sw_moe_routing_mass needs for T tokens (0 if T == 0). */
 size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens);
 

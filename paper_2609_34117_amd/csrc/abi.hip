@@ -455,12 +455,14 @@ size_t sw_moe_layer_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens, int3
   return layer_workspace_bytes(d, n_tokens, n_shared, n_groups);
 }
 
-sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
-                       const float* bias, const uint8_t* keep_mask, int32_t n_shared,
-                       int32_t n_groups, const uint16_t* w13, const uint16_t* w2, int32_t layout,
-                       int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
-                       int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
-                       float* out, void* workspace, size_t workspace_bytes, void* stream) {
+sw_status sw_moe_layer_phase(int32_t phase, const sw_moe_dims* d, const uint16_t* x,
+                             int32_t n_tokens, const float* wr, const float* bias,
+                             const uint8_t* keep_mask, int32_t n_shared, int32_t n_groups,
+                             const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                             int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                             int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
+                             float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  if (phase < 0 || phase > 3) return SW_ERR_SHAPE;
   SW_TRY(check_layer_dims(d, n_tokens, n_shared, n_groups));
   const sw_moe_dims pool = layer_pool_dims(d, n_shared, n_groups);
   if (!counts || !offsets || !active || !n_active) return SW_ERR_NULL;
@@ -468,6 +470,7 @@ sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
     return SW_ERR_ALIGN;
   const hipStream_t s = as_stream(stream);
   if (n_tokens == 0) {
+    if (phase != 0) return SW_OK;
     (void)hipGetLastError();
     return launched(sw::launch_dispatch(nullptr, 0, pool.n_experts, counts, offsets, nullptr,
                                         active, n_active, s));
@@ -486,22 +489,42 @@ sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens
   const bool tiled = layout == SW_LAYOUT_TILED;
   void* fws = static_cast<char*>(workspace) +
               sw::align_up(layer_route_bytes(d, n_tokens, n_shared, n_groups), 256);
-  if (!sw::wave_plan_supported(n_tokens, H, I, mp, kp, tiled)) {
-    SW_TRY(launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, H, m, k,
+  if (phase == 2)
+    return launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active,
+                                    H, I, mp, kp, fws, s));
+  if (phase == 3)
+    return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, mp, kp, fws, s));
+  if (sw::wave_plan_supported(n_tokens, H, I, mp, kp, tiled)) {
+    // 0: the routing; 1: gate/up, building the plan on the way
+    if (phase == 0)
+      return launched(sw::launch_route_select(x, n_tokens, wr, bias, keep_mask, H, m, k,
+                                              topk_ids, topk_w, gap, workspace, s, n_shared,
+                                              n_groups));
+    return launched(sw::launch_gate_up_building_plan(x, n_tokens, w13, tiled, topk_ids, counts,
+                                                     offsets, perm, active, n_active, H, I, mp,
+                                                     kp, fws, s));
+  }
+  // 0: routing and dispatch; 1: gate/up
+  if (phase == 0)
+    return launched(sw::launch_route_dispatch(x, n_tokens, wr, bias, keep_mask, H, m, k,
                                               topk_ids, topk_w, gap, counts, offsets, perm,
                                               active, n_active, workspace, s, n_shared,
-                                              n_groups)));
-    return launch_forward(&pool, x, n_tokens, w13, w2, layout, topk_w, counts, offsets, perm,
-                          active, n_active, out, fws, s);
-  }
-  SW_TRY(launched(sw::launch_route_select(x, n_tokens, wr, bias, keep_mask, H, m, k, topk_ids,
-                                          topk_w, gap, workspace, s, n_shared, n_groups)));
-  SW_TRY(launched(sw::launch_gate_up_building_plan(x, n_tokens, w13, tiled, topk_ids, counts,
-                                                   offsets, perm, active, n_active, H, I, mp,
-                                                   kp, fws, s)));
-  SW_TRY(launched(sw::launch_down(n_tokens, w2, tiled, counts, offsets, perm, active, n_active,
-                                  H, I, mp, kp, fws, s)));
-  return launched(sw::launch_combine(n_tokens, topk_w, n_active, out, H, I, mp, kp, fws, s));
+                                              n_groups));
+  return launched(sw::launch_gate_up(x, n_tokens, w13, tiled, counts, offsets, perm, active,
+                                     n_active, H, I, mp, kp, fws, s));
+}
+
+sw_status sw_moe_layer(const sw_moe_dims* d, const uint16_t* x, int32_t n_tokens, const float* wr,
+                       const float* bias, const uint8_t* keep_mask, int32_t n_shared,
+                       int32_t n_groups, const uint16_t* w13, const uint16_t* w2, int32_t layout,
+                       int32_t* topk_ids, float* topk_w, float* gap, int32_t* counts,
+                       int32_t* offsets, int32_t* perm, int32_t* active, int32_t* n_active,
+                       float* out, void* workspace, size_t workspace_bytes, void* stream) {
+  for (int32_t phase = 0; phase < 4; ++phase)
+    SW_TRY(sw_moe_layer_phase(phase, d, x, n_tokens, wr, bias, keep_mask, n_shared, n_groups,
+                              w13, w2, layout, topk_ids, topk_w, gap, counts, offsets, perm,
+                              active, n_active, out, workspace, workspace_bytes, stream));
+  return SW_OK;
 }
 
 size_t sw_moe_routing_mass_workspace_bytes(const sw_moe_dims* d, int32_t n_tokens) {

@@ -66,6 +66,8 @@ def _load() -> ctypes.CDLL:
                                         ctypes.c_int),
         "sw_moe_layer": ([D, P, I32, P, P, P, I32, I32, P, P, I32, P, P, P, P, P, P, P, P, P, P,
                           SZ, P], ctypes.c_int),
+        "sw_moe_layer_phase": ([I32, D, P, I32, P, P, P, I32, I32, P, P, I32, P, P, P, P, P, P, P,
+                                P, P, P, SZ, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(lib, name)
@@ -455,13 +457,15 @@ def sw_moe_layer_workspace_bytes(d: Dims, n_tokens: int, n_shared: int = 0,
 def sw_moe_layer(x: torch.Tensor, wr: torch.Tensor, top_k: int, w13: torch.Tensor,
                  w2: torch.Tensor, *, layout: int = ROW_MAJOR, n_shared: int = 0,
                  n_groups: int = 1, keep_mask=None, bias=None, want_gap=True, route_out=None,
-                 plan: Optional[Plan] = None, out=None, ws=None, stream=None):
+                 plan: Optional[Plan] = None, out=None, ws=None, stream=None, phase=None):
     """Route, dispatch plan, expert FFNs and combine of one layer in one call
     (Section 3.1, Eq. 2; Section 2.1, Eq. 1): bitwise what
     ``sw_moe_route_dispatch`` (or ``sw_moe_route_dispatch_shared`` when
     ``n_shared`` > 0, ``wr`` then holding the shared gate row last) followed
     by ``sw_moe_forward`` give.  ``w13``/``w2`` hold the pool of
     m + n_groups * n_shared experts.
+
+    ``phase`` (0-3) runs one phase of the call (``sw_moe_layer_phase``).
 
     Returns ``(topk_ids, topk_w, gap, plan, out)``."""
     t, hidden = x.shape
@@ -483,14 +487,16 @@ def sw_moe_layer(x: torch.Tensor, wr: torch.Tensor, top_k: int, w13: torch.Tenso
         out = _empty((t, hidden), torch.float32, x.device)
     if ws is None:
         ws = workspace(sw_moe_layer_workspace_bytes(d, t, n_shared, n_groups), x.device)
-    st = LIB.sw_moe_layer(
-        ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
-        _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
-        n_shared, n_groups, _ptr(w13, _BF16, "w13"), _ptr(w2, _BF16, "w2"), layout, _ptr(ids),
-        _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
-        _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"), _ptr(ws),
-        ws.numel(), _stream(stream))
-    _check(st, "sw_moe_layer")
+    args = (ctypes.byref(d), _ptr(x, _BF16, "x"), t, _ptr(wr, (torch.float32,), "wr"),
+            _ptr(bias, (torch.float32,), "bias"), _ptr(keep_mask, (torch.uint8,), "keep_mask"),
+            n_shared, n_groups, _ptr(w13, _BF16, "w13"), _ptr(w2, _BF16, "w2"), layout, _ptr(ids),
+            _ptr(w), _ptr(gap), _ptr(plan.counts), _ptr(plan.offsets), _ptr(plan.perm),
+            _ptr(plan.active), _ptr(plan.n_active), _ptr(out, (torch.float32,), "out"), _ptr(ws),
+            ws.numel(), _stream(stream))
+    if phase is None:
+        _check(LIB.sw_moe_layer(*args), "sw_moe_layer")
+    else:
+        _check(LIB.sw_moe_layer_phase(phase, *args), "sw_moe_layer_phase")
     return ids, w, gap, plan, out
 
 

@@ -267,6 +267,13 @@ def test_layer_call_validation_and_plan_query(lib):
     assert call(S=2, R=0) == SW_ERR_SHAPE
     assert call(S=2, R=600) == SW_ERR_UNSUPPORTED          # 64 + 1200 experts
     assert call(S=30) == SW_ERR_UNSUPPORTED                # 38 slots a token
+    ph = lib.sw_moe_layer_phase
+    ph.argtypes = [I32] + f.argtypes
+    for bad_phase in (-1, 4):
+        assert ph(bad_phase, ctypes.byref(d), 16, 4, 16, None, None, 0, 1, 16, 16, 1, 16, 16, None,
+                  16, 16, 16, 16, 16, 16, 16, need, None) == SW_ERR_SHAPE
+    assert ph(1, ctypes.byref(d), 16, 4, 16, None, None, 0, 1, 16, 16, 1, 16, 16, None, 16, 16,
+              16, 16, 16, 16, 16, need - 1, None) == SW_ERR_WORKSPACE
     # which shapes build the plan in the gate/up launch (host logic only)
     b = lib.sw_moe_gate_up_builds_plan
     b.argtypes, b.restype = [D, I32, I32], I32

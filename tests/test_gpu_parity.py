@@ -801,6 +801,26 @@ def test_layer_call_against_oracle_and_separate_calls(sw, hidden, n_experts, top
           f"({3 * n_experts + 2 + pairs} plan words) max|err|={s['err']:.3g}")
 
 
+@pytest.mark.parametrize("hidden,n_experts,top_k,inter,tokens", [
+    (512, 64, 8, 256, 64),    # gate/up builds the plan, the pool fully active
+    (512, 256, 8, 256, 40),   # gate/up builds the plan, idle experts expected
+    (512, 64, 8, 256, 100),   # routing + dispatch, then the forward's launches
+])
+def test_layer_phases_in_order_are_the_layer_call(sw, hidden, n_experts, top_k, inter, tokens):
+    cfg, L, D = small_layer(hidden, n_experts, top_k, inter, tokens, seed=41)
+    w13, w2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    whole = sw.sw_moe_layer(D["x"], D["wr"], top_k, w13, w2, layout=sw.TILED)
+    d = sw.dims(hidden, inter, n_experts, top_k)
+    bufs = ((torch.empty_like(whole[0]), torch.empty_like(whole[1]), torch.empty_like(whole[2])),
+            sw.alloc_plan(tokens, n_experts, top_k, "cuda"), torch.empty_like(whole[4]),
+            sw.workspace(sw.sw_moe_layer_workspace_bytes(d, tokens), "cuda"))
+    for phase in range(4):
+        res = sw.sw_moe_layer(D["x"], D["wr"], top_k, w13, w2, layout=sw.TILED, route_out=bufs[0],
+                              plan=bufs[1], out=bufs[2], ws=bufs[3], phase=phase)
+    names = ("topk_ids", "topk_w", "gap", "plan", "out")
+    assert_same_layer(dict(zip(names, whole)), dict(zip(names, res)))
+
+
 def test_layer_call_in_band_flag_and_empty_batch(sw):
     # two eligible experts for top-3: the third slot is -1 on every token,
     # the plan built in the gate/up launch flags the batch (n_active -1, perm
