@@ -80,7 +80,7 @@ const char* sw_status_str(int status);
  * its results can differ from theirs in the last bits. */
 typedef enum {
   SW_KERNELS_NONE = 0,    /* T == 0: nothing is launched */
-  SW_KERNELS_PREFILL = 1, /* >= 48 tokens per expert, pool >= 16, H and I multiples of 128 */
+  SW_KERNELS_PREFILL = 1, /* >= 16 pairs per expert, pool >= 16, H and I multiples of 128 */
   SW_KERNELS_SPLIT_K = 2, /* few tiles with a long K (a token or two, the shared expert) */
   SW_KERNELS_WAVE = 3,    /* the decode streaming kernels (and any tiled pool otherwise) */
   SW_KERNELS_GENERIC = 4  /* row-major shapes outside the others' limits */

@@ -111,7 +111,7 @@ hipError_t launch_gate_up_wave_plan(const uint16_t* x, int T, const uint16_t* w1
                                     const int* topk_ids, int* counts, int* offsets, int* perm,
                                     int* active, int* n_active, int H, int I, int m, int k,
                                     uint16_t* h_hi, uint16_t* h_lo, hipStream_t stream);
-// Prefill-sized batches (about 48 or more tokens per expert): each weight
+// Batches of 16 or more pairs per expert (prefill, large decode): each weight
 // tile is streamed once per 160-token pass (expert_prefill.hip).
 bool prefill_supported(int T, int H, int I, int m, int k);
 hipError_t launch_gate_up_prefill(const uint16_t* x, int T, const uint16_t* w13, bool tiled,

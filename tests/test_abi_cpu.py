@@ -347,8 +347,11 @@ def test_forward_kernel_families(lib):
     pre = Dims(2048, 512, 256, 8)     # the 4096-token prefill layer
     assert _families(lib, pre, 4096) == (SW_OK, PREFILL, PREFILL)
     assert _families(lib, pre, 4096, layout=0) == (SW_OK, PREFILL, PREFILL)
-    # under ~48 tokens per expert, or a pool under 16, the decode kernels
-    assert _families(lib, pre, 1024)[1:] == (WAVE, WAVE)
+    # from 16 pairs per expert on, the prefill kernels; under it, or on a
+    # pool under 16, the decode kernels
+    assert _families(lib, pre, 512)[1:] == (PREFILL, PREFILL)
+    assert _families(lib, pre, 511)[1:] == (WAVE, WAVE)
+    assert _families(lib, pre, 256)[1:] == (WAVE, WAVE)
     assert _families(lib, Dims(256, 128, 8, 2), 400)[1:] == (WAVE, WAVE)
     # the prefill test shapes (hidden 256 and 384, I 128) do take the prefill kernels
     assert _families(lib, Dims(256, 128, 16, 4), 512)[1:] == (PREFILL, PREFILL)

@@ -1,5 +1,6 @@
 """GPU parity: the HIP library (through its C ABI) against the CPU oracle on the
 same seeded inputs.  Tolerances and the near-tie rule are in parity.py."""
+import dataclasses
 import functools
 
 import numpy as np
@@ -168,6 +169,8 @@ def test_decode_sweep_parity(sw, batch, pruning):
     L2 = dict(L, x=x)
     D2 = dict(D, x=dev(x))
     s = check_layer(sw, cfg, L2, D2, mask, what=f"sweep B={batch} p={pruning}")
+    # the router mask keeps the full pool: at most 8 pairs per expert on
+    # average, the decode kernels
     d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
     fam = sw.sw_moe_forward_kernels(d, batch, sw.ROW_MAJOR)
     if batch >= 64:
@@ -179,6 +182,21 @@ def test_decode_sweep_parity(sw, batch, pruning):
     print(f"sweep B={batch} p={pruning}: kernels={fam} n_active={s['n_active']} "
           f"max pairs/expert={s['counts'].max()} near_ties={s['n_near']} "
           f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+    n_keep = cfg.n_keep(pruning)
+    if pruning and batch * cfg.top_k >= 16 * n_keep:
+        # the compacted pool (the one the benchmark times) has 16 or more
+        # pairs per expert here: the prefill kernels, against the oracle on
+        # the compacted layer
+        _, _, _, w13c, w2c, wrc, _ = oracle.prune_compact(L["importance"], n_keep, cfg.top_k,
+                                                          w13=L["w13"], w2=L["w2"], wr=L["wr"])
+        cc = dataclasses.replace(cfg, n_experts=n_keep)
+        dc = sw.dims(cfg.hidden, cfg.inter, n_keep, cfg.top_k)
+        assert sw.sw_moe_forward_kernels(dc, batch, sw.ROW_MAJOR) == ("prefill", "prefill")
+        sc = check_layer(sw, cc, dict(L2, w13=w13c, w2=w2c, wr=wrc),
+                         dict(D2, w13=dev(w13c), w2=dev(w2c), wr=dev(wrc)), None,
+                         what=f"sweep compacted B={batch} p={pruning}")
+        print(f"  compacted pool ({n_keep} experts): kernels=prefill max pairs/expert="
+              f"{sc['counts'].max()} max|err|={sc['err']:.3g} rel={sc['rel']:.3g}")
 
 
 def test_prefill_shape_parity(sw):
@@ -213,7 +231,7 @@ def test_skew_routed_batch256_parity(sw, pruning):
 
 
 # --------------------------------------------------------------------------
-# the prefill-sized path (about 48 or more tokens per expert)
+# the prefill-sized path (16 or more pairs per expert)
 
 def _layer_in_batches(sw, D, k, nb, layout, mask=None, bias=None):
     """The layer over the tokens in batches of nb (small enough for the
