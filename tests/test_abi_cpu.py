@@ -285,6 +285,8 @@ def test_layer_call_validation_and_plan_query(lib):
     assert built(Dims(2048, 512, 512, 8), 48) == 1         # 1922 plan words
     assert built(Dims(2048, 512, 512, 16), 64) == 0        # 2562 plan words: too many
     assert built(Dims(2048, 512, 600, 8), 8) == 0          # more experts than threads
+    assert built(Dims(256, 128, 480, 16), 63) == 1         # 2450 plan words
+    assert built(Dims(256, 128, 480, 16), 64) == 0         # 2466
     assert built(Dims(40, 40, 16, 2), 8, 0) == 0           # the generic kernels
     # the phase that builds it rejects other shapes before any launch
     g = lib.sw_moe_forward_gate_up_plan

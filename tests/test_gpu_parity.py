@@ -787,6 +787,9 @@ def test_route_dispatch_in_band_errors_and_empty_batch(sw):
     (512, 64, 8, 256, 64, True, True, True),      # one expert takes every token: two passes
     (512, 64, 8, 256, 2, True, False, False),     # 2 tokens: split-K kernels
     (512, 64, 8, 256, 65, True, False, False),    # 65 tokens: the 128-token variants
+    (256, 480, 16, 128, 63, True, False, True),   # 2450 plan words: just within the LDS plan
+    (256, 480, 16, 128, 64, True, False, False),  # 2466 plan words: just past it
+    (256, 512, 14, 128, 64, False, False, True),  # 512 experts and 896 pairs: 2434 plan words
 ])
 def test_layer_call_against_oracle_and_separate_calls(sw, hidden, n_experts, top_k, inter, tokens,
                                                       tiled, popular, builds):
