@@ -165,20 +165,11 @@ __global__ __launch_bounds__(256) void gate_up_generic_kernel(
       for (int q = 0; q < 4; ++q) u[q] = __shfl_xor(c[q], 32);
       const int slot = t0 + nb * 16 + r;
       if (lane < 32 && slot < cnt) {
-        uint32_t hw[2], lw[2];
+        float hv[4];
 #pragma unroll
-        for (int q = 0; q < 4; q += 2) {
-          uint16_t hb[2], lb[2];
-#pragma unroll
-          for (int d = 0; d < 2; ++d) {
-            const float g = c[q + d];
-            const float hv = (g / (1.0f + expf(-g))) * u[q + d];
-            hb[d] = f32_to_bf16(hv);
-            lb[d] = f32_to_bf16(hv - bf16_to_f32(hb[d]));
-          }
-          hw[q / 2] = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-          lw[q / 2] = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
-        }
+        for (int q = 0; q < 4; ++q) hv[q] = swiglu(c[q], u[q]);
+        u32x2 hw, lw;
+        split_bf16x4(hv, hw, lw);
         const size_t off = (size_t)(base + slot) * I + ib * 8 + kg * 4;
         *reinterpret_cast<uint2*>(h_hi + off) = make_uint2(hw[0], hw[1]);
         *reinterpret_cast<uint2*>(h_lo + off) = make_uint2(lw[0], lw[1]);
@@ -377,20 +368,11 @@ __device__ __forceinline__ void gu_epilogue(const GateUpCtx& c, const ExpertTile
     for (int q = 0; q < 4; ++q) u[q] = __shfl_xor(v[q], 32);
     const int slot = t0 + nb * 16 + c.r;
     if (lane < 32 && slot < t.cnt) {
-      uint32_t hw[2], lw[2];
+      float hv[4];
 #pragma unroll
-      for (int q = 0; q < 4; q += 2) {
-        uint16_t hb[2], lb[2];
-#pragma unroll
-        for (int d = 0; d < 2; ++d) {
-          const float g = v[q + d];
-          const float hv = (g / (1.0f + expf(-g))) * u[q + d];
-          hb[d] = f32_to_bf16(hv);
-          lb[d] = f32_to_bf16(hv - bf16_to_f32(hb[d]));
-        }
-        hw[q / 2] = (uint32_t)hb[0] | ((uint32_t)hb[1] << 16);
-        lw[q / 2] = (uint32_t)lb[0] | ((uint32_t)lb[1] << 16);
-      }
+      for (int q = 0; q < 4; ++q) hv[q] = swiglu(v[q], u[q]);
+      u32x2 hw, lw;
+      split_bf16x4(hv, hw, lw);
       const size_t off = (size_t)(t.base + slot) * c.I + t.sub * 8 + c.kg * 4;
       *reinterpret_cast<uint2*>(c.h_hi + off) = make_uint2(hw[0], hw[1]);
       *reinterpret_cast<uint2*>(c.h_lo + off) = make_uint2(lw[0], lw[1]);

@@ -227,18 +227,11 @@ __global__ __launch_bounds__(64 * waves_of<NB>(), 1) void gate_up_skinny_kernel(
             f32x4 u4;
 #pragma unroll
             for (int i = 0; i < 4; ++i) u4[i] = __shfl_xor(g4[i], 32);
-            uint16_t hb[4], lb[4];
+            float hv[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const float gt = g4[i];
-              const float hv = (gt / (1.0f + expf(-gt))) * u4[i];
-              hb[i] = f32_to_bf16(hv);
-              lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
-            }
-            const u32x2 hw = {(uint32_t)hb[0] | ((uint32_t)hb[1] << 16),
-                              (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
-            const u32x2 lw = {(uint32_t)lb[0] | ((uint32_t)lb[1] << 16),
-                              (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+            for (int i = 0; i < 4; ++i) hv[i] = swiglu(g4[i], u4[i]);
+            u32x2 hw, lw;
+            split_bf16x4(hv, hw, lw);
             const int sl = p0 + nb * 16 + r;
             uint32_t off = kOutOfRange;
             if (lane < 32 && sl < cnt) off = ((uint32_t)sl * I + (uint32_t)(ib * 8 + kg * 4)) * 2u;

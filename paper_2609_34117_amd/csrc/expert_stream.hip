@@ -467,16 +467,10 @@ __device__ __forceinline__ void gu_compute(const GuWave& g, const ChunkPos& at,
       f32x4 u;
 #pragma unroll
       for (int i = 0; i < 4; ++i) u[i] = __shfl_xor(v[i], 32);
-      uint16_t hb[4], lb[4];
+      float hv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float gt = v[i];
-        const float hv = (gt / (1.0f + expf(-gt))) * u[i];
-        hb[i] = f32_to_bf16(hv);
-        lb[i] = f32_to_bf16(hv - bf16_to_f32(hb[i]));
-      }
-      hw = u32x2{(uint32_t)hb[0] | ((uint32_t)hb[1] << 16), (uint32_t)hb[2] | ((uint32_t)hb[3] << 16)};
-      lw = u32x2{(uint32_t)lb[0] | ((uint32_t)lb[1] << 16), (uint32_t)lb[2] | ((uint32_t)lb[3] << 16)};
+      for (int i = 0; i < 4; ++i) hv[i] = swiglu(v[i], u[i]);
+      split_bf16x4(hv, hw, lw);
       const int slot = g.p0 + nb * 16 + g.r;
       if (g.lane < 32 && slot < g.cnt)
         off = ((uint32_t)slot * g.I + (uint32_t)(ib * 8 + g.kg * 4)) * 2u;

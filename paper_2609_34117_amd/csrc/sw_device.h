@@ -10,6 +10,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
@@ -63,12 +65,50 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
   return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }
 
-// fp32 -> bf16 with round-to-nearest-even (NaN stays NaN).
+// fp32 -> bf16 with round-to-nearest-even (NaN stays NaN, quieted): gfx950's
+// conversion instruction, which rounds exactly like adding 0x7fff plus the
+// kept lsb to the bits and truncating (checked bit for bit against that
+// formula on 2^24 inputs: every exponent, the halfway cases, denormals,
+// infinities and NaN payloads).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
+  return __builtin_bit_cast(uint16_t, static_cast<__bf16>(f));
+}
+
+// Two fp32 values rounded to bf16 in one instruction, a in the low half.
+__device__ __forceinline__ uint32_t bf16x2_of(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
+}
+
+// SiLU(g) * u in fp32, the SwiGLU of the expert FFN (Section 3.1).  exp(-g)
+// is the hardware base-2 exponential of -g log2(e), with the rounding error
+// of that product put back to first order (an FMA residual, times ln 2);
+// 1 / (1 + exp(-g)) is the hardware reciprocal.  A few ulp from the exact
+// value, for a third of the instructions of expf and an IEEE division.  g is
+// clamped to [-88, 88] inside the exponential only: beyond, 1 + exp(-g) is
+// either 1 or so large that the product is below 1e-36.  Contraction is off
+// and the FMAs are explicit, so every kernel that inlines this (and the
+// split below) rounds the same way: the paths agree bit for bit.
+__device__ __forceinline__ float swiglu(float g, float u) {
+#pragma clang fp contract(off)
+  constexpr float kL2e = 1.44269502162933349609375f;  // log2(e) rounded to fp32
+  constexpr float kL2eLo = 1.9259629911266175e-08f;   // log2(e) - kL2e
+  constexpr float kLn2 = 0.693147180559945309f;
+  const float gc = __builtin_amdgcn_fmed3f(g, -88.0f, 88.0f);
+  const float t = -gc * kL2e;
+  const float r = fmaf(-gc, kL2eLo, fmaf(-gc, kL2e, -t));  // -gc log2(e) - t
+  const float den = fmaf(__builtin_amdgcn_exp2f(t), fmaf(r, kLn2, 1.0f), 1.0f);
+  return g * __builtin_amdgcn_rcpf(den) * u;
+}
+
+// Four fp32 values as bf16 pairs v = hi + lo (hi = v rounded to nearest
+// even, lo = the remainder, exact in fp32, rounded likewise), packed two a
+// word in order.
+__device__ __forceinline__ void split_bf16x4(const float (&v)[4], u32x2& hi, u32x2& lo) {
+#pragma clang fp contract(off)
+  hi = u32x2{bf16x2_of(v[0], v[1]), bf16x2_of(v[2], v[3])};
+  const float h0 = __uint_as_float(hi[0] << 16), h1 = __uint_as_float(hi[0] & 0xffff0000u);
+  const float h2 = __uint_as_float(hi[1] << 16), h3 = __uint_as_float(hi[1] & 0xffff0000u);
+  lo = u32x2{bf16x2_of(v[0] - h0, v[1] - h1), bf16x2_of(v[2] - h2, v[3] - h3)};
 }
 
 // Monotone map from fp32 to uint32 (a < b  <=>  key(a) < key(b) for
