@@ -78,16 +78,16 @@ PAPER_CONTEXT = {
 # HBM traffic of one gate_up launch on the default workload (batch 64, 50%
 # pruned, tiled pool), from two rocprofv3 --pmc passes of
 # `bench.py --no-cpu-baseline --steps 20 --warmup 5` (summary in
-# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197820.45 KiB x
+# profiles/gate_up_wave_decode_b64_hbm_traffic.md): FETCH_SIZE 197812.39 KiB x
 # 1.99982 (the ratio of bytes copied to FETCH_SIZE over 12 plain device copies
-# of 192-768 MiB) + WRITE_SIZE 1567.95 KiB x 1.0 (WRITE_SIZE of the copies is
+# of 192-768 MiB) + WRITE_SIZE 1570.74 KiB x 1.0 (WRITE_SIZE of the copies is
 # exact).  The figure holds while the gate/up kernel's sources hash as below.
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h",
                   "paper_2609_34117_amd/csrc/dispatch_block.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="1378b1c4a0efa02b0c70c69e5c27b025cca140b1043c4aa37c0cca8fc2810dce",
+GATE_UP_TRAFFIC = dict(sources_sha256="82ab6384af89cffd095704f8da27f9eadb277994251cc67cdd0891a4b3988187",
                        workload=("decode_b64", 64, 0.5, "tiled"),
-                       bytes_per_launch=int(round((197839.90 * 1.99982 + 1570.75) * 1024)))
+                       bytes_per_launch=int(round((197812.39 * 1.99982 + 1570.74) * 1024)))
 
 
 def parse():
