@@ -115,9 +115,12 @@ def assert_same_layer(a, b):
     assert torch.equal(a["plan"].active[:n], b["plan"].active[:n])
 
 
-def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=None):
+def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=None, out_scale=1.0):
     """Route, dispatch and forward on the GPU vs the oracle; returns stats.
-    The forward is compared on every token unless `rows` names a subset."""
+    The forward is compared on every token unless `rows` names a subset;
+    both outputs are divided by `out_scale` first (inputs scaled up by s
+    scale the output by about s^2, and the absolute bound is for unit
+    scale)."""
     k = cfg.top_k
     b_dev = None if bias is None else dev(bias)
     g = guarded_layer(sw, D, k, mask=mask, bias=b_dev, layout=layout)
@@ -141,7 +144,7 @@ def check_layer(sw, cfg, L, D, mask, bias=None, rows=None, layout=None, what=Non
     # forward: against the oracle on the GPU's routing
     rows = np.arange(g_ids.shape[0]) if rows is None else np.asarray(rows)
     o_out = oracle_forward_rows(oracle.forward, L["x"], L["w13"], L["w2"], g_ids, g_w, rows)
-    err, rel = compare_out(host(g["out"])[rows], o_out)
+    err, rel = compare_out(host(g["out"])[rows] / out_scale, o_out / out_scale)
     return dict(n_near=r["near_ties"], routing=r, n_active=n_active, err=err, rel=rel, gpu=g,
                 counts=counts)
 
@@ -157,6 +160,43 @@ def test_layer_parity(sw, name, pruning):
     s = check_layer(sw, cfg, L, D, mask, what=f"{name} p={pruning}")
     print(f"{name} p={pruning}: n_active={s['n_active']} near_ties={s['n_near']} "
           f"max|err|={s['err']:.3g} rel={s['rel']:.3g}")
+
+
+@pytest.mark.parametrize("name,batch,pruning,family", [("decode_b64", 64, 0.5, "wave"),
+                                                       ("decode_b64", 1, 0.0, "split_k"),
+                                                       ("decode_sweep", 256, 0.75, "prefill")])
+def test_layer_parity_with_saturating_gates(sw, name, batch, pruning, family):
+    # Gate/up weights scaled by 32 (exact in bf16), so that the SwiGLU gate g
+    # runs far past the range of the exponential both ways (g > 88: silu(g)
+    # = g to fp32 precision; g < -88: silu(g) * u vanishes), on each kernel
+    # family's epilogue; the router and its tolerances are untouched.  The
+    # outputs (32^2 times larger) are compared at unit scale.
+    cfg, L, D = layer_inputs(name)
+    s = 32.0
+    x = I.make_x(cfg, tokens=batch, rep=300 + batch)
+    mask = mask_for(cfg, L, pruning)
+    w13, w2, wr = L["w13"], L["w2"], L["wr"]
+    if pruning:  # the compacted pool, as the benchmark runs it
+        n_keep = cfg.n_keep(pruning)
+        _, _, _, w13, w2, wr, _ = oracle.prune_compact(L["importance"], n_keep, cfg.top_k,
+                                                       w13=w13, w2=w2, wr=wr)
+        cfg = dataclasses.replace(cfg, n_experts=n_keep)
+        mask = None
+    w13 = I.to_bf16_bits(I.bf16_bits_to_f32(w13) * np.float32(s))
+    L2 = dict(L, x=x, w13=w13, w2=w2, wr=wr)
+    D2 = dict(D, x=dev(x), w13=dev(w13), w2=dev(w2), wr=dev(wr))
+    d = sw.dims(cfg.hidden, cfg.inter, cfg.n_experts, cfg.top_k)
+    assert sw.sw_moe_forward_kernels(d, batch, sw.ROW_MAJOR)[0] == family
+    st = check_layer(sw, cfg, L2, D2, mask, what=f"saturating {name} B={batch}",
+                     out_scale=s * s)
+    # the gates of the routed pairs do reach both saturated ranges
+    ids = host(st["gpu"]["topk_ids"])
+    xf = I.bf16_bits_to_f32(x).astype(np.float64)
+    g = np.concatenate([I.bf16_bits_to_f32(w13[ids[t, j], :cfg.inter]).astype(np.float64) @ xf[t]
+                        for t in range(ids.shape[0]) for j in range(ids.shape[1])])
+    assert (g > 88).any() and (g < -88).any(), (g.min(), g.max())
+    print(f"saturating {name} B={batch}: g in [{g.min():.0f}, {g.max():.0f}] "
+          f"max|err|={st['err']:.3g} rel={st['rel']:.3g} (unit scale)")
 
 
 @pytest.mark.parametrize("batch", I.SWEEP_BATCHES)
