@@ -85,7 +85,7 @@ PAPER_CONTEXT = {
 KERNEL_SOURCES = ("paper_2609_34117_amd/csrc/expert_stream.hip",
                   "paper_2609_34117_amd/csrc/sw_device.h",
                   "paper_2609_34117_amd/csrc/dispatch_block.h")
-GATE_UP_TRAFFIC = dict(sources_sha256="82ab6384af89cffd095704f8da27f9eadb277994251cc67cdd0891a4b3988187",
+GATE_UP_TRAFFIC = dict(sources_sha256="fde0ac45004e4df8a0f3889d303304bd170f73ac8af53e0be8cb7b9e4dc5deac",
                        workload=("decode_b64", 64, 0.5, "tiled"),
                        bytes_per_launch=int(round((197812.39 * 1.99982 + 1570.74) * 1024)))
 

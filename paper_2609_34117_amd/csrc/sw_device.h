@@ -79,7 +79,8 @@ __device__ __forceinline__ uint32_t bf16x2_of(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
-// SiLU(g) * u in fp32, the SwiGLU of the expert FFN (Section 3.1).  exp(-g)
+// SiLU(g) * u in fp32: the expert FFN's activation (the experts of Section
+// 2.1 read as SwiGLU FFNs, gate rows first in W13), silu(g) = g / (1 + e^-g).  exp(-g)
 // is the hardware base-2 exponential of -g log2(e), with the rounding error
 // of that product put back to first order (an FMA residual, times ln 2);
 // 1 / (1 + exp(-g)) is the hardware reciprocal.  A few ulp from the exact
