@@ -705,6 +705,31 @@ def test_tiled_forward_parity_and_bitwise_equal_to_row_major(sw, name, pruning, 
     compare_out(host(tl["out"]), o_out)
 
 
+def test_benchmark_configuration_parity(sw):
+    # The configuration the decode benchmark times: the batch-64 layer pruned
+    # to 64 of its 128 experts by the library's own compaction of the tiled
+    # pool, one sw_moe_layer call (the gate/up launch builds the plan and,
+    # every kept expert being active, takes the fully-active guess), against
+    # the oracle on the oracle's compacted layer, every token.
+    cfg, L, D = layer_inputs("decode_b64")
+    n_keep = cfg.n_keep(0.5)
+    t13, t2 = sw.sw_moe_pack_experts(D["w13"], D["w2"])
+    c = sw.sw_moe_prune_compact(D["importance"], n_keep, cfg.top_k, w13=t13, w2=t2, wr=D["wr"])
+    kept, _, _, w13c, w2c, wrc, _ = oracle.prune_compact(L["importance"], n_keep, cfg.top_k,
+                                                         w13=L["w13"], w2=L["w2"], wr=L["wr"])
+    np.testing.assert_array_equal(host(c["kept"]), kept)
+    cc = dataclasses.replace(cfg, n_experts=n_keep)
+    d = sw.dims(cfg.hidden, cfg.inter, n_keep, cfg.top_k)
+    assert sw.sw_moe_gate_up_builds_plan(d, cfg.tokens, sw.TILED)
+    assert sw.sw_moe_forward_kernels(d, cfg.tokens, sw.TILED) == ("wave", "wave")
+    Lc = dict(L, w13=w13c, w2=w2c, wr=wrc)
+    Dc = dict(D, w13=c["w13"], w2=c["w2"], wr=c["wr"])
+    st = check_layer(sw, cc, Lc, Dc, None, layout=sw.TILED, what="benchmark configuration")
+    assert st["n_active"] == n_keep  # the fully-active guess holds
+    print(f"benchmark configuration: n_active={st['n_active']} near_ties={st['n_near']} "
+          f"max|err|={st['err']:.3g} rel={st['rel']:.3g}")
+
+
 def test_compacting_a_tiled_pool_equals_tiling_the_compacted_pool(sw):
     cfg, L, D = layer_inputs("decode_b64")
     n_keep = cfg.n_keep(0.5)
