@@ -1019,6 +1019,8 @@ def _folded_layer(sw, L, w13s, w2s, gate, top_k, n_shared, mask, tiled, n_groups
     (2048, 256, 8, 512, 100, 2, False, True, 4),  # four groups of 25 tokens
     (1024, 200, 14, 256, 40, 2, True, False, 3),  # k + parts = 16: the row form at its limit
     (2048, 96, 6, 512, 200, 4, False, False, 1),  # 4 parts: 200-token parts over gate/up passes
+    (2048, 128, 8, 512, 64, 2, False, True, 4),   # the shared-expert benchmark's shape: 128
+                                                  # experts, 2 parts in 4 groups of 16 tokens
 ])
 def test_shared_expert_folded_into_the_plan(sw, hidden, n_experts, top_k, inter, tokens, n_shared,
                                             masked, tiled, groups):
